@@ -1,0 +1,186 @@
+"""Pi_Sec-Approx-MatMul (Section 4.2 protocol box; Section 4.1 for depth 1),
+written in the paper's orientation and notation over Z_{2^32}.
+
+Paper orientation: W is m x n (weights), X is n x l (activations), Y = W X.
+The build's row-major activations are A = X^T (l x n) and its outputs are
+Y^T (l x m); ``run`` converts at the boundary only.
+
+Readings where the paper is ambiguous (listed with reasons in the design notes):
+* the sparse masks are S_{i+1} in Z^{m x r_i} and T_{i+1} in Z^{r_i x l}, the
+  only dimensions under which S_{i+1} (M_i ... M_1) and N_1 ... N_i T_{i+1}
+  are defined (the box prints r_i x r_{i-1} and r_{i-1} x r_i);
+* the chains M_i ... M_1 and N_1 ... N_i start from M_1 in Z^{r_1 x n} and
+  N_1 in Z^{n x r_1} (r_0 = n);
+* activation-side random matrices (R, E_x, T_i) are drawn element by element
+  in the build's row-major order of their transposes (the order in which the
+  GPU visits them); weight-side ones in the paper's orientation.
+
+Init W computes U_w, J_i and W' = W + U_w (box "Init W" steps 1-5; the
+Freivalds vector of step 4 is omitted: integrity checking is not part of the
+masked product). Init X samples R, E_x, T_i and forms U_x and K (steps 1a-1c).
+The server returns Y' = W' X' and Q_i = (M_i ... M_1) X'; unmasking outputs
+Y' - K - L Q_d - sum_i S_{i+1} Q_i.
+
+Expanding W' X' shows that this unmasked value equals (W + E_w)(X + E_x)
+exactly in the ring, for any mask draw; that is the identity the tests pin.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+from . import sampling as smp
+from .ring import ring_add, ring_matmul, ring_sub, to_ring
+
+
+@dataclass
+class WeightState:
+    W: np.ndarray                       # m x n plaintext embedded in the ring
+    E_w: np.ndarray                     # m x n
+    L: np.ndarray                       # m x r_d
+    M: List[np.ndarray]                 # M_i, r_i x r_{i-1}
+    N: List[np.ndarray]                 # N_i, r_{i-1} x r_i
+    S: List[Optional[np.ndarray]]       # S[i] = S_{i+1} (m x r_i) for i = 1..d-1; index 0 unused
+    Mc: List[np.ndarray]                # Mc[i-1] = M_i ... M_1 (r_i x n)
+    Nc: List[np.ndarray]                # Nc[i-1] = N_1 ... N_i (n x r_i)
+    J: List[np.ndarray]                 # J[i-1] = (W + E_w) N_1 ... N_i (m x r_i)
+    U_w: np.ndarray                     # m x n
+    W_masked: np.ndarray                # W' (m x n)
+
+
+@dataclass
+class CallState:
+    R: np.ndarray                       # r_d x l
+    E_x: np.ndarray                     # n x l
+    T: List[Optional[np.ndarray]]       # T[i] = T_{i+1} (r_i x l); index 0 unused
+    U_x: np.ndarray                     # n x l
+    K: np.ndarray                       # m x l
+
+
+def _noise(params, rows, cols, seed, stream, instance, transposed=False):
+    nz = params.noise
+    if nz.kind == "zero":
+        return np.zeros((rows, cols), dtype=np.uint32)
+    if transposed:
+        return smp.sample_matrix("dgauss", cols, rows, seed, stream, instance,
+                                 sigma=nz.sigma, bound=nz.bound).T.copy()
+    return smp.sample_matrix("dgauss", rows, cols, seed, stream, instance,
+                             sigma=nz.sigma, bound=nz.bound)
+
+
+def init_w(W_plain: np.ndarray, params, seed: int, weight_id: int) -> WeightState:
+    """Init W of the protocol box for a plaintext m x n weight matrix."""
+    W = to_ring(W_plain)
+    m, n = W.shape
+    r = list(params.ranks)
+    d = len(r)
+    dims = [n] + r                                    # r_0 = n
+    # step 1: sample L, M_i, N_i, E_w, S_i
+    L = smp.sample_matrix("uniform", m, r[d - 1], seed, smp.STREAM_L, weight_id)
+    M = [smp.sample_matrix("uniform", dims[i], dims[i - 1], seed, smp.STREAM_M + i, weight_id)
+         for i in range(1, d + 1)]
+    N = [smp.sample_matrix("uniform", dims[i - 1], dims[i], seed, smp.STREAM_N + i, weight_id)
+         for i in range(1, d + 1)]
+    E_w = _noise(params, m, n, seed, smp.STREAM_EW, weight_id)
+    S: List[Optional[np.ndarray]] = [None] * d
+    for i in range(1, d):
+        S[i] = smp.sample_matrix("sparse", m, r[i - 1], seed, smp.STREAM_S + i + 1, weight_id,
+                                 log2_inv_density=params.sparse_log2_inv_density)
+    # chains M_i ... M_1 and N_1 ... N_i
+    Mc = [M[0]]
+    Nc = [N[0]]
+    for i in range(2, d + 1):
+        Mc.append(ring_matmul(M[i - 1], Mc[-1]))
+        Nc.append(ring_matmul(Nc[-1], N[i - 1]))
+    # step 2: U_w = L (M_d ... M_1) + sum_{i=1}^{d-1} S_{i+1} (M_i ... M_1) + E_w
+    U_w = ring_matmul(L, Mc[d - 1])
+    for i in range(1, d):
+        U_w = ring_add(U_w, ring_matmul(S[i], Mc[i - 1]))
+    U_w = ring_add(U_w, E_w)
+    # step 3: J_i = (W + E_w) N_1 ... N_i
+    WE = ring_add(W, E_w)
+    J = [ring_matmul(WE, Nc[i - 1]) for i in range(1, d + 1)]
+    # step 5: W' = W + U_w
+    return WeightState(W=W, E_w=E_w, L=L, M=M, N=N, S=S, Mc=Mc, Nc=Nc, J=J,
+                       U_w=U_w, W_masked=ring_add(W, U_w))
+
+
+def init_x(ws: WeightState, l: int, params, seed: int, call_id: int) -> CallState:
+    """Init X (box, online step 1): sample R, E_x, T_i; form U_x and K."""
+    r = list(params.ranks)
+    d = len(r)
+    n = ws.W.shape[1]
+    # step 1a; activation-side matrices are drawn in row-major order of their transposes
+    R = smp.sample_matrix("uniform", l, r[d - 1], seed, smp.STREAM_R, call_id).T.copy()
+    E_x = _noise(params, n, l, seed, smp.STREAM_EX, call_id, transposed=True)
+    T: List[Optional[np.ndarray]] = [None] * d
+    for i in range(1, d):
+        T[i] = smp.sample_matrix("sparse", l, r[i - 1], seed, smp.STREAM_T + i + 1, call_id,
+                                 log2_inv_density=params.sparse_log2_inv_density).T.copy()
+    # step 1b: U_x = N_1...N_d R + sum_{i=1}^{d-1} N_1...N_i T_{i+1} + E_x
+    U_x = ring_matmul(ws.Nc[d - 1], R)
+    for i in range(1, d):
+        U_x = ring_add(U_x, ring_matmul(ws.Nc[i - 1], T[i]))
+    U_x = ring_add(U_x, E_x)
+    # step 1c: K = J_d R + sum_{i=1}^{d-1} J_i T_{i+1}
+    K = ring_matmul(ws.J[d - 1], R)
+    for i in range(1, d):
+        K = ring_add(K, ring_matmul(ws.J[i - 1], T[i]))
+    return CallState(R=R, E_x=E_x, T=T, U_x=U_x, K=K)
+
+
+def mask(X: np.ndarray, cs: CallState) -> np.ndarray:
+    """Online step 2: X' = X + U_x."""
+    return ring_add(to_ring(X), cs.U_x)
+
+
+def server(ws: WeightState, X_masked: np.ndarray):
+    """Online step 3 (untrusted accelerator): Y' = W' X', Q_i = (M_i...M_1) X'."""
+    Y_masked = ring_matmul(ws.W_masked, X_masked)
+    Q = [ring_matmul(ws.Mc[i], X_masked) for i in range(len(ws.Mc))]
+    return Y_masked, Q
+
+
+def unmask(ws: WeightState, cs: CallState, Y_masked: np.ndarray, Q: List[np.ndarray]) -> np.ndarray:
+    """Online step 5: Y = Y' - K - L Q_d - sum_{i=1}^{d-1} S_{i+1} Q_i."""
+    d = len(Q)
+    Y = ring_sub(Y_masked, cs.K)
+    Y = ring_sub(Y, ring_matmul(ws.L, Q[d - 1]))
+    for i in range(1, d):
+        Y = ring_sub(Y, ring_matmul(ws.S[i], Q[i - 1]))
+    return Y
+
+
+@dataclass
+class RunResult:
+    ws: WeightState
+    cs: CallState
+    X_masked: np.ndarray
+    Y_masked: np.ndarray
+    Q: List[np.ndarray]
+    Y: np.ndarray                        # m x l ring element
+    extras: dict = field(default_factory=dict)
+
+    # build-orientation views (row-major, tokens first)
+    @property
+    def A_masked(self):
+        return self.X_masked.T
+
+    @property
+    def Y_out(self):
+        return self.Y.T
+
+
+def run(A_plain: np.ndarray, W_plain: np.ndarray, params, seed: int, weight_id: int = 0,
+        call_id: int = 0) -> RunResult:
+    """Init W, Init X, mask, server product and unmask for A (l x n, build
+    orientation) and W (m x n)."""
+    ws = init_w(W_plain, params, seed, weight_id)
+    X = np.asarray(A_plain).T
+    cs = init_x(ws, X.shape[1], params, seed, call_id)
+    Xm = mask(X, cs)
+    Ym, Q = server(ws, Xm)
+    Y = unmask(ws, cs, Ym, Q)
+    return RunResult(ws=ws, cs=cs, X_masked=Xm, Y_masked=Ym, Q=Q, Y=Y)

@@ -1,0 +1,119 @@
+"""Samplers for the mask material of Pi_Sec-Approx-MatMul (Section 4.2 protocol
+box), drawn from Philox-4x32-10 streams.
+
+Stream definition (a reading: the paper names no generator). A stream is
+identified by (seed, stream_id, instance). Its word t (t >= 0) is word (t mod 4)
+of Philox-4x32-10 with
+
+    key     = (seed mod 2^32, seed div 2^32)
+    counter = (b mod 2^32, b div 2^32, stream_id, instance),   b = t div 4.
+
+A logical ``rows x cols`` matrix indexes its elements row-major,
+e = i * cols + j, and consumes words in that order:
+
+* uniform over Z_{2^32} (the paper's U(Z_{2^k}), Section 4.1): element e is
+  word e;
+* discrete Gaussian N(Z_{2^k}; 0, sigma^2) (Section 4.1, "Bounded protocol
+  error": Pr[k] proportional to exp(-k^2 / (2 sigma^2))), truncated to
+  [-B, B]: element e is -B + #{k : word e >= T_k} for the cumulative
+  thresholds T_0 <= ... <= T_{2B-1} of ``dgauss_thresholds``;
+* sparse LPN noise S(.; mu) (Background, "LWE and LPN": sparse uniform with
+  noise rate mu), mu = 2^-s: element e takes words 2e (gate) and 2e+1 (value)
+  and is the value word if the top s bits of the gate word are zero, else 0;
+* random signs d in {+1, -1}^n (Section 5, "Random Hadamard rotation"):
+  d_j = +1 if bit 31 of word j is 0, else -1.
+"""
+from __future__ import annotations
+
+from decimal import Decimal, getcontext
+from typing import List
+
+import numpy as np
+
+from .philox import philox4x32_np
+
+# Stream identifiers (counter word 2) of every random matrix of the protocol.
+# Weight-side material uses instance = weight-matrix id; activation-side
+# material uses instance = call id.
+STREAM_EW = 0x10          # E_w, full-rank LWE error on the weights
+STREAM_L = 0x11           # L, secret left factor (m x r_d)
+STREAM_M = 0x20           # + i: M_i, public (r_i x r_{i-1})
+STREAM_N = 0x30           # + i: N_i, public (r_{i-1} x r_i)
+STREAM_S = 0x40           # + i: S_i, sparse LPN mask (m x r_{i-1})
+STREAM_EX = 0x50          # E_x, full-rank LWE error on the activations
+STREAM_R = 0x51           # R, secret right factor
+STREAM_T = 0x60           # + i: T_i, sparse LPN mask on the activations
+STREAM_SIGNS = 0x70       # d, Hadamard rotation signs
+
+
+def stream_words(seed: int, stream: int, instance: int, t0: int, count: int) -> np.ndarray:
+    """Words t0 .. t0+count-1 of the stream, as uint32."""
+    if count <= 0:
+        return np.zeros(0, dtype=np.uint32)
+    t = np.arange(t0, t0 + count, dtype=np.uint64)
+    b = t >> np.uint64(2)
+    lane = (t & np.uint64(3)).astype(np.int64)
+    # evaluate each distinct block once
+    b_first = int(b[0])
+    b_last = int(b[-1])
+    blocks = np.arange(b_first, b_last + 1, dtype=np.uint64)
+    k0 = seed & 0xFFFFFFFF
+    k1 = (seed >> 32) & 0xFFFFFFFF
+    out = philox4x32_np(blocks & np.uint64(0xFFFFFFFF), blocks >> np.uint64(32),
+                        np.full(blocks.shape, stream, dtype=np.uint64),
+                        np.full(blocks.shape, instance, dtype=np.uint64), k0, k1)
+    words = np.stack(out, axis=1)           # (n_blocks, 4)
+    idx = (b - np.uint64(b_first)).astype(np.int64)
+    return words[idx, lane].astype(np.uint32)
+
+
+def dgauss_thresholds(sigma: float, bound: int) -> List[int]:
+    """Cumulative thresholds T_k = floor(2^32 * F_k + 1/2), k = 0 .. 2B-1, where
+    F_k = sum_{j=-B}^{-B+k} p_j and p_j = exp(-j^2 / (2 sigma^2)) / Z over the
+    support j in [-B, B]. Computed with 60-digit decimal arithmetic."""
+    if bound < 0:
+        raise ValueError("bound must be >= 0")
+    getcontext().prec = 60
+    s = Decimal(repr(float(sigma)))
+    if s == 0:
+        w = [Decimal(1) if j == 0 else Decimal(0) for j in range(-bound, bound + 1)]
+    else:
+        w = [(-(Decimal(j) ** 2) / (2 * s * s)).exp() for j in range(-bound, bound + 1)]
+    z = sum(w)
+    out = []
+    acc = Decimal(0)
+    for k in range(2 * bound):
+        acc += w[k]
+        out.append(int((acc / z * Decimal(2 ** 32) + Decimal("0.5")).to_integral_value(rounding="ROUND_FLOOR")))
+    return out
+
+
+def sample_matrix(kind: str, rows: int, cols: int, seed: int, stream: int, instance: int,
+                  sigma: float = 0.5, bound: int = 4, log2_inv_density: int = 6) -> np.ndarray:
+    """A logical rows x cols matrix over Z_{2^32} (uint32, two's complement)."""
+    n = rows * cols
+    if kind == "zero":
+        return np.zeros((rows, cols), dtype=np.uint32)
+    if kind == "uniform":
+        return stream_words(seed, stream, instance, 0, n).reshape(rows, cols)
+    if kind == "dgauss":
+        u = stream_words(seed, stream, instance, 0, n).astype(np.uint64)
+        th = dgauss_thresholds(sigma, bound)
+        v = np.full(n, -bound, dtype=np.int64)
+        for t in th:
+            v += (u >= np.uint64(t)).astype(np.int64)
+        return v.astype(np.int32).view(np.uint32).reshape(rows, cols)
+    if kind == "sparse":
+        w = stream_words(seed, stream, instance, 0, 2 * n)
+        gate = w[0::2]
+        val = w[1::2]
+        s = int(log2_inv_density)
+        keep = (gate >> np.uint32(32 - s)) == 0 if s > 0 else np.ones(n, dtype=bool)
+        return np.where(keep, val, np.uint32(0)).astype(np.uint32).reshape(rows, cols)
+    raise ValueError(f"unknown distribution {kind!r}")
+
+
+def sample_signs(n: int, seed: int, instance: int = 0, stream: int = STREAM_SIGNS) -> np.ndarray:
+    """d in {+1, -1}^n as int8."""
+    w = stream_words(seed, stream, instance, 0, n)
+    return np.where((w >> np.uint32(31)) == 0, 1, -1).astype(np.int8)

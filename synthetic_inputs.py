@@ -1,0 +1,108 @@
+"""Seeded synthetic inputs for the MOSAIC hot path.
+
+This module is shared by the CPU oracle, the tests and the benchmark. It holds
+only input generation (plaintext operands, activations, protocol parameter
+sets); none of the method's arithmetic lives here.
+
+Every generator uses ``numpy.random.default_rng(seed)`` and is deterministic.
+Layouts follow the build convention: activations ``A`` are tokens x features
+(M x K) and weights ``W`` are out-features x in-features (N x K), so the
+plaintext product is ``A @ W.T`` (M x N). In the paper's notation
+(Section 4, Y = W X with W m x n and X n x l) this is ``A = X^T``, ``W = W``,
+M = l, K = n, N = m.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Tuple
+
+import numpy as np
+
+
+# ---------------------------------------------------------------------------
+# protocol parameter sets (data only)
+# ---------------------------------------------------------------------------
+@dataclass(frozen=True)
+class NoiseSpec:
+    """Distribution of the full-rank LWE error terms E_w and E_x.
+
+    kind: "dgauss" (discrete Gaussian of parameter sigma, support [-bound, bound])
+          or "zero" (no error term).
+    """
+    kind: str = "dgauss"
+    sigma: float = 0.5
+    bound: int = 4
+
+
+@dataclass(frozen=True)
+class ProtocolParams:
+    """Parameters of the nested LWE/LPN mask (Section 4.2 protocol box).
+
+    ranks: (r_1, ..., r_d); depth d = len(ranks); r_1 > r_2 > ... > r_d.
+    sparse_log2_inv_density: the LPN masks S_i, T_i have density 2^-k.
+    noise: the LWE error E_w / E_x.
+    """
+    ranks: Tuple[int, ...] = (128,)
+    noise: NoiseSpec = field(default_factory=NoiseSpec)
+    sparse_log2_inv_density: int = 6
+
+    @property
+    def depth(self) -> int:
+        return len(self.ranks)
+
+
+# Depth-1 (LWE only) with small noise, as in the deployed parameterisation.
+PARAMS_D1_SMALL_R128 = ProtocolParams(ranks=(128,), noise=NoiseSpec("dgauss", 0.5, 4))
+# Depth-2 (LWE + one LPN level), sparse masks at density 1/64 and no E.
+PARAMS_D2_SPARSE = ProtocolParams(ranks=(128, 64), noise=NoiseSpec("zero", 0.0, 0))
+# Depth-3 with sparse masks and small noise.
+PARAMS_D3_SPARSE_SMALL = ProtocolParams(ranks=(192, 128, 64), noise=NoiseSpec("dgauss", 0.5, 4))
+# The paper's LWE rank at lambda = 140 (r_1 = 1536, sigma = 0.5), depth 1.
+PARAMS_PAPER_D1 = ProtocolParams(ranks=(1536,), noise=NoiseSpec("dgauss", 0.5, 4))
+# Depth 2 with the paper's first two ranks (1536, 1024), sparse, no E.
+PARAMS_PAPER_D2_SPARSE = ProtocolParams(ranks=(1536, 1024), noise=NoiseSpec("zero", 0.0, 0))
+
+
+# ---------------------------------------------------------------------------
+# plaintext operands
+# ---------------------------------------------------------------------------
+def int8_operands(M: int, K: int, N: int, seed: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Uniform int8 plaintext in [-127, 127]: A (M x K) first, then W (N x K)."""
+    rng = np.random.default_rng(seed)
+    A = rng.integers(-127, 128, size=(M, K), dtype=np.int8)
+    W = rng.integers(-127, 128, size=(N, K), dtype=np.int8)
+    return A, W
+
+
+def int8_matrix(rows: int, cols: int, seed: int) -> np.ndarray:
+    rng = np.random.default_rng(seed)
+    return rng.integers(-127, 128, size=(rows, cols), dtype=np.int8)
+
+
+def outlier_activations(rows: int, n: int, seed: int, p_outlier: float = 1e-3,
+                        scale: float = 50.0) -> np.ndarray:
+    """fp32 activations: N(0, 1) entries, each independently an outlier with
+    probability ``p_outlier``, outliers multiplied by ``scale``."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((rows, n))
+    mask = rng.random((rows, n)) < p_outlier
+    x = np.where(mask, x * scale, x)
+    return x.astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# workload shapes
+# ---------------------------------------------------------------------------
+# Single masked matmul: A 64 x 512, W 512 x 512 (seed 0).
+SMALL_CASE = dict(M=64, K=512, N=512, seed=0)
+# Decode-shaped GEMMs at 8B-layer shapes (seed 1).
+DECODE_M = (1, 8, 64)
+DECODE_KN: List[Tuple[int, int]] = [(4096, 4096), (4096, 14336), (14336, 4096)]
+DECODE_SEED = 1
+# Prefill-shaped GEMMs at 70B-layer shapes (seed 2).
+PREFILL_M = 2048
+PREFILL_KN: List[Tuple[int, int]] = [(8192, 8192), (8192, 28672), (28672, 8192)]
+PREFILL_SEED = 2
+# Random-Hadamard rotation: 4096 x 8192 fp32, signs seed 3.
+HADAMARD_SHAPE = (4096, 8192)
+HADAMARD_SEED = 3
