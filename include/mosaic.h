@@ -1,0 +1,206 @@
+/*
+ * mosaic.h -- C ABI of the MOSAIC hot path on AMD Instinct MI355X (gfx950).
+ *
+ * MOSAIC (arxiv 2607.29221) lets a trusted client outsource W X to an
+ * untrusted accelerator by masking both operands over the ring Z_{2^32}
+ * (protocol Pi_Sec-Approx-MatMul, Section 4.2) and recovering the product up
+ * to a small error; a random Hadamard rotation (Section 5) keeps the
+ * fixed-point error small. This library implements the data-parallel steps:
+ * sampling of the mask material, the mask pass, the server's ring product,
+ * unmasking and the rotation.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Orientation. Matrices are row-major. Activations are tokens x features
+ * (A is M x K, the transpose of the paper's X) and weights are
+ * out-features x in-features (W is N x K, the paper's W). Products are
+ * C = A B^T (M x N), the transpose of the paper's W X.
+ *
+ * Ring elements are uint32 holding residues mod 2^32; the signed value of a
+ * result is the same 32 bits read as int32 (two's complement).
+ *
+ * Digit layout. The ring product consumes its operands as balanced base-256
+ * digits: x = d_0 + 256 d_1 + 256^2 d_2 + 256^3 d_3 (mod 2^32), each d_t an
+ * int8 in [-128, 127] (unique for every x). A rows x K ring matrix in digit
+ * layout is an int8 array [rows][Kp/16][4][16] with Kp = 64 * ceil(K/64):
+ * byte (i, g, t, b) at offset i * pitch + 64 g + 16 t + b is digit t of
+ * element (i, 16 g + b); columns K .. Kp-1 hold zero digits. ``pitch`` is the
+ * row pitch in bytes, a multiple of 64 and at least 4 * Kp. Blocks of
+ * columns whose offsets are multiples of 64 can be placed side by side in
+ * one wider digit matrix (this is how the protocol concatenates factors).
+ *
+ * Random streams. Mask material is drawn from Philox-4x32-10 (Salmon et al.,
+ * SC'11). Stream (seed, stream, instance) has word t equal to word (t mod 4)
+ * of Philox with key (seed mod 2^32, seed div 2^32) and counter
+ * (b mod 2^32, b div 2^32, stream, instance), b = t div 4. A logical
+ * rows x cols matrix visits its elements row-major, e = i * cols + j:
+ *   UNIFORM  element e is word e (uniform over Z_{2^32});
+ *   DGAUSS   element e is -B + #{k : word e >= T_k} with the thresholds of
+ *            mosaic_dgauss_thresholds (discrete Gaussian of Section 4.1,
+ *            truncated to [-B, B]);
+ *   SPARSE   element e is word 2e+1 if the top s bits of word 2e are zero,
+ *            else 0 (LPN noise of rate 2^-s, Section 3);
+ *   ZERO     element e is 0.
+ *
+ * Memory. Every pointer argument except ``mosaic_rng`` structs and the
+ * threshold output of mosaic_dgauss_thresholds is a DEVICE pointer owned by
+ * the caller. The library allocates nothing and keeps no state between
+ * calls; calls are asynchronous on ``stream`` (a hipStream_t, NULL for the
+ * default stream) and may be issued from several host threads.
+ *
+ * Empty matrices. A call whose output has no elements does nothing and
+ * returns MOSAIC_OK; pointers of operands without elements may be NULL. A
+ * product with K = 0 writes zeros.
+ *
+ * Errors. Arguments are validated before anything is launched; on error no
+ * output is touched and a negative mosaic_status is returned. MOSAIC_ERR_HIP
+ * means a launch failed; mosaic_last_error_message() describes the last
+ * failure on the calling thread.
+ */
+#ifndef MOSAIC_H
+#define MOSAIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOSAIC_ABI_VERSION 1
+
+typedef enum mosaic_status {
+  MOSAIC_OK = 0,
+  MOSAIC_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad size or pitch */
+  MOSAIC_ERR_UNSUPPORTED = -2, /* valid but unsupported shape or option */
+  MOSAIC_ERR_HIP = -3          /* a HIP launch failed */
+} mosaic_status;
+
+typedef enum mosaic_dist {
+  MOSAIC_DIST_ZERO = 0,
+  MOSAIC_DIST_UNIFORM = 1,
+  MOSAIC_DIST_DGAUSS = 2,
+  MOSAIC_DIST_SPARSE = 3
+} mosaic_dist;
+
+typedef enum mosaic_dtype {
+  MOSAIC_I8 = 0,  /* int8, sign-extended into the ring */
+  MOSAIC_I16 = 1, /* int16, sign-extended */
+  MOSAIC_I32 = 2, /* int32, two's complement */
+  MOSAIC_U32 = 3  /* ring element */
+} mosaic_dtype;
+
+/* A random matrix drawn from a Philox stream (host struct, read at call
+ * time). ``transposed`` != 0 writes logical element (j, i) of a cols x rows
+ * matrix to output position (i, j): the same matrix stored transposed. */
+typedef struct mosaic_rng {
+  uint64_t seed;
+  uint32_t stream;
+  uint32_t instance;
+  int32_t dist;             /* mosaic_dist */
+  int32_t bound;            /* DGAUSS: support [-bound, bound], 0 <= bound <= 15 */
+  double sigma;             /* DGAUSS: parameter sigma >= 0 */
+  int32_t log2_inv_density; /* SPARSE: density 2^-s, 0 <= s <= 31 */
+  int32_t transposed;
+} mosaic_rng;
+
+/* ABI version (MOSAIC_ABI_VERSION of the built library). */
+int32_t mosaic_abi_version(void);
+
+/* Message for the last error on the calling thread ("" if none). */
+const char* mosaic_last_error_message(void);
+
+/* Host-only. Discrete Gaussian thresholds T_0 .. T_{2B-1} (Section 4.1,
+ * "Bounded protocol error": Pr[k] proportional to exp(-k^2 / (2 sigma^2)),
+ * here restricted to [-B, B]): T_k = floor(2^32 F_k + 1/2), F_k the
+ * probability of the values -B .. -B+k. ``out`` is a host array of 2B
+ * entries. Touches no GPU. */
+mosaic_status mosaic_dgauss_thresholds(double sigma, int32_t bound, uint64_t* out);
+
+/* a1. Fill a rows x cols matrix from the stream ``rng`` (protocol box, Init W
+ * step 1 and Init X step 1a: uniform L, M_i, N_i, R; discrete Gaussian E_w,
+ * E_x; sparse S_i, T_i). Writes ring elements to ``out`` (leading dimension
+ * ``ldo`` elements) and/or digits to ``out_dig`` (row pitch ``dig_pitch``
+ * bytes); each output may be NULL but not both. */
+mosaic_status mosaic_sample(const mosaic_rng* rng, int64_t rows, int64_t cols,
+                            uint32_t* out, int64_t ldo,
+                            int8_t* out_dig, int64_t dig_pitch, void* stream);
+
+/* a4. Mask (protocol box, online step 2: X' = X + U_x, here in the build's
+ * orientation A' = A + U_a):
+ *     out(i, j) = x(i, j) + u(i, j) + e(i, j)   (mod 2^32)
+ * x: plaintext of type ``x_dtype`` at x[i * x_rs + j * x_cs] (element
+ * strides; NULL means 0); u: ring matrix, leading dimension ``ldu`` (NULL
+ * means 0); e: drawn from ``noise`` (NULL means 0), so the Init X error can be
+ * generated in the same pass. Outputs as in mosaic_sample. With x and noise
+ * NULL this converts a ring matrix to digit layout. */
+mosaic_status mosaic_mask(const void* x, int32_t x_dtype, int64_t x_rs, int64_t x_cs,
+                          const uint32_t* u, int64_t ldu, const mosaic_rng* noise,
+                          int64_t rows, int64_t cols,
+                          uint32_t* out, int64_t ldo,
+                          int8_t* out_dig, int64_t dig_pitch, void* stream);
+
+/* a5. The untrusted accelerator's product (protocol box, online step 3,
+ * Y' = W' X' and Q_i = (M_i ... M_1) X'; Section 6.1 emulation with 8-bit
+ * limbs): C = A B^T over Z_{2^32}.
+ * A: M x K digits (pitch a_pitch); B: N x K digits (pitch b_pitch);
+ * C: M x N uint32, leading dimension ldc >= N. Stacking the rows of
+ * M_i ... M_1 under W' in B returns [Y' | Q] from one call. */
+mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch,
+                                   const int8_t* b_dig, int64_t b_pitch,
+                                   int64_t M, int64_t N, int64_t K,
+                                   uint32_t* c, int64_t ldc, void* stream);
+
+/* a6. Unmask (protocol box, online step 5, in the build's orientation:
+ * Y = Y' - K - Q_d L^T - sum_i Q_i S_{i+1}^T):
+ *     y(i, j) = ym(i, j) - kc(i, j) - sum_{r < R} q(i, r) l(j, r)  (mod 2^32)
+ * ym: M x N (ldy); kc: M x N (ldk, NULL means 0); q: M x R digits (q_pitch),
+ * l: N x R digits (l_pitch) -- the factors concatenated along R; R may be 0
+ * (then q and l are ignored). y: M x N int32 (ldo), the centred lift.
+ * Optional dequantisation (Pi_Sec-Linear, online step 3): if y_f32 is not
+ * NULL it receives (float)y(i, j) * s_rows[i] * s_cols[j] (ldf); y may then
+ * be NULL. */
+mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy,
+                            const uint32_t* kc, int64_t ldk,
+                            const int8_t* q_dig, int64_t q_pitch,
+                            const int8_t* l_dig, int64_t l_pitch,
+                            int64_t M, int64_t N, int64_t R,
+                            int32_t* y, int64_t ldo,
+                            const float* s_rows, const float* s_cols,
+                            float* y_f32, int64_t ldf, void* stream);
+
+/* a1 (signs). Random sign vector of the rotation (Section 5: d drawn
+ * uniformly from {+1, -1}^n): out[j] = +1 if bit 31 of word j of the stream
+ * (rng->seed, rng->stream, rng->instance) is 0, else -1. ``out`` is a device
+ * int8 array of n entries. rng->dist and rng->transposed are ignored. */
+mosaic_status mosaic_sample_signs(const mosaic_rng* rng, int64_t n, int8_t* out, void* stream);
+
+/* a7. Random Hadamard rotation (Section 5, R = H D, applied with Fino's fast
+ * transform). Per row v of x (rows x n, leading dimension ldx):
+ *     forward:  y = H_b (d * v) / sqrt(b)     inverse: y = d * (H_b v) / sqrt(b)
+ * blockwise on consecutive blocks of length b = ``block`` (b a power of two,
+ * 16 <= b <= 32768, n a multiple of b; b = n is the plain rotation). H_b is
+ * the Sylvester-ordered Walsh-Hadamard matrix, H[i][j] = (-1)^popcount(i&j),
+ * so the inverse undoes the forward rotation. ``signs`` is a device int8
+ * vector of n entries +-1 (NULL means d = 1). y may equal x (in place, then
+ * ldy == ldx); otherwise the two must not overlap. x, y 16-byte aligned,
+ * ldx and ldy multiples of 4. fp32 throughout. */
+mosaic_status mosaic_hadamard_rotate(const float* x, int64_t ldx, float* y, int64_t ldy,
+                                     int64_t rows, int64_t n, int64_t block,
+                                     const int8_t* signs, int32_t inverse, void* stream);
+
+/* a8. Per-row fixed-point quantisation (Pi_Sec-Linear, Init W step 2 and
+ * online step 1): s_i = max_j |x(i, j)| / qmax (1 for an all-zero row),
+ * q(i, j) = round-half-even(x(i, j) / s_i), both in fp32 arithmetic.
+ * Writes q as int32 (ldq) and/or directly as digits (q_dig, q_pitch), and
+ * the scales (rows floats). 1 <= qmax <= 2^24. */
+mosaic_status mosaic_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64_t n,
+                                   int32_t qmax, int32_t* q, int64_t ldq,
+                                   int8_t* q_dig, int64_t q_pitch,
+                                   float* scale, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOSAIC_H */

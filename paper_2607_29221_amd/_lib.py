@@ -1,0 +1,68 @@
+"""ctypes loader for libmosaic.so (the C ABI of include/mosaic.h).
+
+The library must have been built in-tree (``python -m
+paper_2607_29221_amd.build``); there is no fallback implementation, so a
+missing library is an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmosaic.so")
+
+c_i32 = ctypes.c_int32
+c_i64 = ctypes.c_int64
+c_u32 = ctypes.c_uint32
+c_u64 = ctypes.c_uint64
+c_ptr = ctypes.c_void_p
+
+
+class MosaicRng(ctypes.Structure):
+    _fields_ = [
+        ("seed", c_u64),
+        ("stream", c_u32),
+        ("instance", c_u32),
+        ("dist", c_i32),
+        ("bound", c_i32),
+        ("sigma", ctypes.c_double),
+        ("log2_inv_density", c_i32),
+        ("transposed", c_i32),
+    ]
+
+
+# name -> argument types (all return mosaic_status as int32 unless listed)
+_SIGNATURES = {
+    "mosaic_abi_version": ([], c_i32),
+    "mosaic_last_error_message": ([], ctypes.c_char_p),
+    "mosaic_dgauss_thresholds": ([ctypes.c_double, c_i32, ctypes.POINTER(c_u64)], c_i32),
+    "mosaic_sample": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr], c_i32),
+    "mosaic_mask": ([c_ptr, c_i32, c_i64, c_i64, c_ptr, c_i64, ctypes.POINTER(MosaicRng), c_i64, c_i64,
+                     c_ptr, c_i64, c_ptr, c_i64, c_ptr], c_i32),
+    "mosaic_masked_matmul": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i64, c_ptr], c_i32),
+    "mosaic_unmask": ([c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64,
+                       c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
+    "mosaic_sample_signs": ([ctypes.POINTER(MosaicRng), c_i64, c_ptr, c_ptr], c_i32),
+    "mosaic_hadamard_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
+    "mosaic_quantize_rows": ([c_ptr, c_i64, c_i64, c_i64, c_i32, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_ptr],
+                             c_i32),
+}
+
+EXPORTED = tuple(_SIGNATURES)
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2607_29221_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = lib
+    return _lib

@@ -1,0 +1,304 @@
+// C ABI of libmosaic (declared in include/mosaic.h): argument validation,
+// translation of mosaic_rng into kernel parameters, and dispatch to the
+// kernels. Nothing here allocates device memory or keeps state between calls
+// except the per-thread error message.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/mosaic.h"
+#include "internal.h"
+
+using namespace mosaic;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+mosaic_status fail(mosaic_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+mosaic_status fail(mosaic_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+mosaic_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return MOSAIC_OK;
+  return fail(MOSAIC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t padded_k(int64_t k) { return 64 * ((k + 63) / 64); }
+
+constexpr int64_t kMaxGridThreads = (int64_t(1) << 32) - 256;
+
+// Discrete Gaussian thresholds in extended precision (see mosaic.h).
+void dgauss_table(double sigma, int bound, uint64_t* out) {
+  long double w[2 * kMaxDgaussBound + 1];
+  long double z = 0.0L;
+  for (int j = -bound; j <= bound; ++j) {
+    long double p;
+    if (sigma == 0.0)
+      p = (j == 0) ? 1.0L : 0.0L;
+    else
+      p = expl(-((long double)j * (long double)j) / (2.0L * (long double)sigma * (long double)sigma));
+    w[j + bound] = p;
+    z += p;
+  }
+  long double acc = 0.0L;
+  for (int k = 0; k < 2 * bound; ++k) {
+    acc += w[k];
+    const long double v = floorl(acc / z * 4294967296.0L + 0.5L);
+    out[k] = (uint64_t)v;
+  }
+}
+
+mosaic_status rng_args(const mosaic_rng* r, RngArgs* a) {
+  if (r == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "rng is NULL");
+  *a = RngArgs{};
+  a->k0 = (uint32_t)(r->seed & 0xFFFFFFFFu);
+  a->k1 = (uint32_t)(r->seed >> 32);
+  a->stream = r->stream;
+  a->instance = r->instance;
+  a->dist = r->dist;
+  a->transposed = r->transposed != 0;
+  a->sparse_shift = 32;
+  switch (r->dist) {
+    case MOSAIC_DIST_ZERO:
+    case MOSAIC_DIST_UNIFORM:
+      break;
+    case MOSAIC_DIST_DGAUSS:
+      if (r->bound < 0 || r->bound > kMaxDgaussBound)
+        return fail(MOSAIC_ERR_INVALID_ARG, "dgauss bound %d outside [0, %d]", r->bound, kMaxDgaussBound);
+      if (!(r->sigma >= 0.0) || !std::isfinite(r->sigma))
+        return fail(MOSAIC_ERR_INVALID_ARG, "dgauss sigma must be finite and >= 0");
+      a->bound = r->bound;
+      dgauss_table(r->sigma, r->bound, a->th);
+      break;
+    case MOSAIC_DIST_SPARSE:
+      if (r->log2_inv_density < 0 || r->log2_inv_density > 31)
+        return fail(MOSAIC_ERR_INVALID_ARG, "sparse log2_inv_density %d outside [0, 31]", r->log2_inv_density);
+      a->sparse_shift = 32 - r->log2_inv_density;
+      break;
+    default:
+      return fail(MOSAIC_ERR_INVALID_ARG, "unknown distribution %d", r->dist);
+  }
+  return MOSAIC_OK;
+}
+
+// Digit-layout operand of rows x cols; a matrix without elements may be NULL.
+mosaic_status check_digits(const int8_t* p, int64_t pitch, int64_t rows, int64_t cols, const char* name) {
+  if (rows == 0 || cols == 0) {
+    if (pitch < 0 || pitch % 64 != 0) return fail(MOSAIC_ERR_INVALID_ARG, "%s pitch must be a multiple of 64", name);
+    return MOSAIC_OK;
+  }
+  if (p == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned16(p)) return fail(MOSAIC_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  if (pitch % 64 != 0 || pitch < 4 * padded_k(cols))
+    return fail(MOSAIC_ERR_INVALID_ARG, "%s pitch %lld must be a multiple of 64 and >= %lld", name,
+                (long long)pitch, (long long)(4 * padded_k(cols)));
+  return MOSAIC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t mosaic_abi_version(void) { return MOSAIC_ABI_VERSION; }
+
+const char* mosaic_last_error_message(void) { return g_last_error.c_str(); }
+
+mosaic_status mosaic_dgauss_thresholds(double sigma, int32_t bound, uint64_t* out) {
+  if (out == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "out is NULL");
+  if (bound < 0 || bound > kMaxDgaussBound)
+    return fail(MOSAIC_ERR_INVALID_ARG, "bound %d outside [0, %d]", bound, kMaxDgaussBound);
+  if (!(sigma >= 0.0) || !std::isfinite(sigma)) return fail(MOSAIC_ERR_INVALID_ARG, "sigma must be finite and >= 0");
+  dgauss_table(sigma, bound, out);
+  return MOSAIC_OK;
+}
+
+mosaic_status mosaic_mask(const void* x, int32_t x_dtype, int64_t x_rs, int64_t x_cs, const uint32_t* u,
+                          int64_t ldu, const mosaic_rng* noise, int64_t rows, int64_t cols, uint32_t* out,
+                          int64_t ldo, int8_t* out_dig, int64_t dig_pitch, void* stream) {
+  if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || cols == 0) return MOSAIC_OK;
+  if (out == nullptr && out_dig == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "no output given");
+  if (x != nullptr && (x_dtype < MOSAIC_I8 || x_dtype > MOSAIC_U32))
+    return fail(MOSAIC_ERR_INVALID_ARG, "unknown x_dtype %d", x_dtype);
+  if (u != nullptr && ldu < cols) return fail(MOSAIC_ERR_INVALID_ARG, "ldu < cols");
+  if (out != nullptr && ldo < cols) return fail(MOSAIC_ERR_INVALID_ARG, "ldo < cols");
+  if (out_dig != nullptr) {
+    const mosaic_status st = check_digits(out_dig, dig_pitch, rows, cols, "out_dig");
+    if (st != MOSAIC_OK) return st;
+  }
+  MaskLaunch a{};
+  a.x = x;
+  a.x_dtype = x_dtype;
+  a.x_rs = x_rs;
+  a.x_cs = x_cs;
+  a.u = u;
+  a.ldu = ldu;
+  a.has_noise = 0;
+  if (noise != nullptr) {
+    const mosaic_status st = rng_args(noise, &a.noise);
+    if (st != MOSAIC_OK) return st;
+    a.has_noise = noise->dist != MOSAIC_DIST_ZERO;
+  }
+  a.rows = rows;
+  a.cols = cols;
+  a.out = out;
+  a.ldo = ldo;
+  a.dig = out_dig;
+  a.pitch = dig_pitch;
+  const int64_t groups = out_dig ? padded_k(cols) / 16 : (cols + 15) / 16;
+  if (rows > 0 && groups > kMaxGridThreads / rows) return fail(MOSAIC_ERR_UNSUPPORTED, "matrix too large for one launch");
+  return hip_status(launch_mask(a, (hipStream_t)stream), "mask launch");
+}
+
+mosaic_status mosaic_sample(const mosaic_rng* rng, int64_t rows, int64_t cols, uint32_t* out, int64_t ldo,
+                            int8_t* out_dig, int64_t dig_pitch, void* stream) {
+  if (rng == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "rng is NULL");
+  return mosaic_mask(nullptr, MOSAIC_U32, 0, 0, nullptr, 0, rng, rows, cols, out, ldo, out_dig, dig_pitch, stream);
+}
+
+mosaic_status mosaic_sample_signs(const mosaic_rng* rng, int64_t n, int8_t* out, void* stream) {
+  if (n < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rng == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "rng is NULL");
+  if (n == 0) return MOSAIC_OK;
+  if (out == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "out is NULL");
+  if (rng == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "rng is NULL");
+  if (n > 4 * kMaxGridThreads) return fail(MOSAIC_ERR_UNSUPPORTED, "vector too long");
+  RngArgs a{};
+  a.k0 = (uint32_t)(rng->seed & 0xFFFFFFFFu);
+  a.k1 = (uint32_t)(rng->seed >> 32);
+  a.stream = rng->stream;
+  a.instance = rng->instance;
+  return hip_status(launch_signs(a, n, out, (hipStream_t)stream), "signs launch");
+}
+
+mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch, const int8_t* b_dig, int64_t b_pitch,
+                                   int64_t M, int64_t N, int64_t K, uint32_t* c, int64_t ldc, void* stream) {
+  if (M < 0 || N < 0 || K < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (K >= 32768) return fail(MOSAIC_ERR_UNSUPPORTED, "K = %lld: the int32 shift-class accumulators need K < 32768", (long long)K);
+  if (M == 0 || N == 0) return MOSAIC_OK;
+  if (c == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "c is NULL");
+  if (ldc < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldc < N");
+  mosaic_status st = check_digits(a_dig, a_pitch, M, K, "a_dig");
+  if (st != MOSAIC_OK) return st;
+  st = check_digits(b_dig, b_pitch, N, K, "b_dig");
+  if (st != MOSAIC_OK) return st;
+  if (a_pitch > (int64_t(1) << 23) || b_pitch > (int64_t(1) << 23))
+    return fail(MOSAIC_ERR_UNSUPPORTED, "digit pitch above 8 MiB");
+  GemmLaunch g{};
+  g.a = a_dig;
+  g.a_pitch = a_pitch;
+  g.b = b_dig;
+  g.b_pitch = b_pitch;
+  g.M = M;
+  g.N = N;
+  g.Kp = padded_k(K);
+  g.c = c;
+  g.ldc = ldc;
+  return hip_status(launch_ring_gemm(g, EPI_STORE, (hipStream_t)stream), "ring product launch");
+}
+
+mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy, const uint32_t* kc, int64_t ldk, const int8_t* q_dig,
+                            int64_t q_pitch, const int8_t* l_dig, int64_t l_pitch, int64_t M, int64_t N, int64_t R,
+                            int32_t* y, int64_t ldo, const float* s_rows, const float* s_cols, float* y_f32,
+                            int64_t ldf, void* stream) {
+  if (M < 0 || N < 0 || R < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (R >= 32768) return fail(MOSAIC_ERR_UNSUPPORTED, "R must be < 32768");
+  if (M == 0 || N == 0) return MOSAIC_OK;
+  if (ym == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "ym is NULL");
+  if (ldy < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldy < N");
+  if (kc != nullptr && ldk < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldk < N");
+  if (y == nullptr && y_f32 == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "no output given");
+  if (y != nullptr && ldo < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldo < N");
+  if (y_f32 != nullptr && (ldf < N || s_rows == nullptr || s_cols == nullptr))
+    return fail(MOSAIC_ERR_INVALID_ARG, "y_f32 needs ldf >= N and both scale vectors");
+  GemmLaunch g{};
+  g.M = M;
+  g.N = N;
+  g.ym = ym;
+  g.ldy = ldy;
+  g.kc = kc;
+  g.ldk = ldk;
+  g.y = y;
+  g.ldo = ldo;
+  g.s_rows = s_rows;
+  g.s_cols = s_cols;
+  g.y_f32 = y_f32;
+  g.ldf = ldf;
+  if (R == 0) {
+    if (M > 0 && N > kMaxGridThreads / M) return fail(MOSAIC_ERR_UNSUPPORTED, "matrix too large for one launch");
+    return hip_status(launch_unmask_elementwise(g, (hipStream_t)stream), "unmask launch");
+  }
+  mosaic_status st = check_digits(q_dig, q_pitch, M, R, "q_dig");
+  if (st != MOSAIC_OK) return st;
+  st = check_digits(l_dig, l_pitch, N, R, "l_dig");
+  if (st != MOSAIC_OK) return st;
+  if (q_pitch > (int64_t(1) << 23) || l_pitch > (int64_t(1) << 23))
+    return fail(MOSAIC_ERR_UNSUPPORTED, "digit pitch above 8 MiB");
+  g.a = q_dig;
+  g.a_pitch = q_pitch;
+  g.b = l_dig;
+  g.b_pitch = l_pitch;
+  g.Kp = padded_k(R);
+  return hip_status(launch_ring_gemm(g, EPI_UNMASK, (hipStream_t)stream), "unmask launch");
+}
+
+mosaic_status mosaic_hadamard_rotate(const float* x, int64_t ldx, float* y, int64_t ldy, int64_t rows, int64_t n,
+                                     int64_t block, const int8_t* signs, int32_t inverse, void* stream) {
+  if (rows < 0 || n < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || n == 0) return MOSAIC_OK;
+  if (x == nullptr || y == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "x or y is NULL");
+  if (!aligned16(x) || !aligned16(y)) return fail(MOSAIC_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
+  if (block < 16 || block > 32768 || (block & (block - 1)) != 0)
+    return fail(MOSAIC_ERR_UNSUPPORTED, "block %lld must be a power of two in [16, 32768]", (long long)block);
+  if (n % block != 0) return fail(MOSAIC_ERR_INVALID_ARG, "n must be a multiple of block");
+  if (ldx < n || ldy < n || ldx % 4 != 0 || ldy % 4 != 0)
+    return fail(MOSAIC_ERR_INVALID_ARG, "ldx and ldy must be >= n and multiples of 4");
+  if (signs != nullptr && !aligned16(signs)) return fail(MOSAIC_ERR_INVALID_ARG, "signs must be 16-byte aligned");
+  if (rows > 0 && n > 0) {
+    const char* xb = (const char*)x;
+    const char* xe = (const char*)(x + (rows - 1) * ldx + n);
+    const char* yb = (const char*)y;
+    const char* ye = (const char*)(y + (rows - 1) * ldy + n);
+    if ((const float*)x != y && xb < ye && yb < xe) return fail(MOSAIC_ERR_INVALID_ARG, "x and y overlap");
+    if ((const float*)x == y && ldx != ldy) return fail(MOSAIC_ERR_INVALID_ARG, "in place needs ldx == ldy");
+  }
+  const int64_t blocks = rows * (n / (block > 0 ? block : 1));
+  if (blocks >= (int64_t(1) << 31)) return fail(MOSAIC_ERR_UNSUPPORTED, "too many blocks");
+  int lb = 0;
+  while ((int64_t(1) << lb) < block) ++lb;
+  return hip_status(launch_hadamard(x, ldx, y, ldy, rows, n, lb, signs, inverse != 0, (hipStream_t)stream),
+                    "hadamard launch");
+}
+
+mosaic_status mosaic_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64_t n, int32_t qmax, int32_t* q,
+                                   int64_t ldq, int8_t* q_dig, int64_t q_pitch, float* scale, void* stream) {
+  if (rows < 0 || n < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || n == 0) return MOSAIC_OK;
+  if (x == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "x is NULL");
+  if (ldx < n) return fail(MOSAIC_ERR_INVALID_ARG, "ldx < n");
+  if (qmax < 1 || qmax > (1 << 24)) return fail(MOSAIC_ERR_INVALID_ARG, "qmax outside [1, 2^24]");
+  if (q == nullptr && q_dig == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "no output given");
+  if (q != nullptr && ldq < n) return fail(MOSAIC_ERR_INVALID_ARG, "ldq < n");
+  if (q_dig != nullptr) {
+    const mosaic_status st = check_digits(q_dig, q_pitch, rows, n, "q_dig");
+    if (st != MOSAIC_OK) return st;
+  }
+  if (rows >= (int64_t(1) << 31)) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  return hip_status(launch_quantize_rows(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, (hipStream_t)stream),
+                    "quantize launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,120 @@
+// Device helpers shared by the MOSAIC kernels: the Philox-4x32-10 generator,
+// the mask-material samplers and the signed-digit form of ring elements.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mosaic {
+
+constexpr int kMaxDgaussBound = 15;
+
+// Parameters of one random stream as the kernels see them (passed by value).
+struct RngArgs {
+  uint32_t k0, k1;        // Philox key: seed low / high word
+  uint32_t stream;        // counter word 2
+  uint32_t instance;      // counter word 3
+  int32_t dist;           // mosaic_dist
+  int32_t bound;          // DGAUSS support [-bound, bound]
+  int32_t sparse_shift;   // SPARSE: 32 - s (gate kept when gate >> shift == 0); 32 keeps all
+  int32_t transposed;
+  uint64_t th[2 * kMaxDgaussBound];  // DGAUSS thresholds (33-bit values)
+};
+
+// Philox-4x32 with 10 rounds (Salmon et al., SC'11): each round multiplies
+// words 0 and 2 by fixed odd constants into 64-bit products and outputs
+// (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0)); the key
+// advances by the Weyl increments between rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+__device__ __forceinline__ uint4 philox_block(const RngArgs& r, uint64_t b) {
+  return philox4x32_10(make_uint4((uint32_t)b, (uint32_t)(b >> 32), r.stream, r.instance), r.k0, r.k1);
+}
+
+__device__ __forceinline__ uint32_t pick(const uint4& v, uint32_t lane) {
+  return lane == 0 ? v.x : lane == 1 ? v.y : lane == 2 ? v.z : v.w;
+}
+
+__device__ __forceinline__ uint32_t stream_word(const RngArgs& r, uint64_t t) {
+  return pick(philox_block(r, t >> 2), (uint32_t)(t & 3));
+}
+
+__device__ __forceinline__ uint32_t dgauss_from_word(const RngArgs& r, uint32_t u) {
+  int32_t v = -r.bound;
+  const uint64_t uu = u;
+  for (int k = 0; k < 2 * r.bound; ++k) v += (uu >= r.th[k]) ? 1 : 0;
+  return (uint32_t)v;
+}
+
+__device__ __forceinline__ uint32_t sparse_from_words(const RngArgs& r, uint32_t gate, uint32_t val) {
+  const bool keep = (r.sparse_shift >= 32) ? true : ((gate >> r.sparse_shift) == 0u);
+  return keep ? val : 0u;
+}
+
+// Element e of the stream's matrix (any alignment).
+__device__ __forceinline__ uint32_t sample_elem(const RngArgs& r, uint64_t e) {
+  switch (r.dist) {
+    case 1: return stream_word(r, e);
+    case 2: return dgauss_from_word(r, stream_word(r, e));
+    case 3: {
+      const uint4 blk = philox_block(r, (2 * e) >> 2);   // words 2e, 2e+1 share a block
+      const uint32_t lane = (uint32_t)((2 * e) & 3);
+      return sparse_from_words(r, pick(blk, lane), pick(blk, lane + 1));
+    }
+    default: return 0u;
+  }
+}
+
+// Elements e0 .. e0+3 with e0 a multiple of 4: one Philox block (two for SPARSE).
+__device__ __forceinline__ void sample4_aligned(const RngArgs& r, uint64_t e0, uint32_t out[4]) {
+  if (r.dist == 1 || r.dist == 2) {
+    const uint4 w = philox_block(r, e0 >> 2);
+    out[0] = w.x; out[1] = w.y; out[2] = w.z; out[3] = w.w;
+    if (r.dist == 2) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] = dgauss_from_word(r, out[i]);
+    }
+  } else if (r.dist == 3) {
+    const uint4 a = philox_block(r, (2 * e0) >> 2);
+    const uint4 b = philox_block(r, ((2 * e0) >> 2) + 1);
+    out[0] = sparse_from_words(r, a.x, a.y);
+    out[1] = sparse_from_words(r, a.z, a.w);
+    out[2] = sparse_from_words(r, b.x, b.y);
+    out[3] = sparse_from_words(r, b.z, b.w);
+  } else {
+    out[0] = out[1] = out[2] = out[3] = 0u;
+  }
+}
+
+// Balanced base-256 digits of x packed in one word: byte t is digit t as an
+// int8. Adding 0x80 to every byte position maps each balanced digit d to the
+// ordinary byte d + 128 of x + 0x80808080; flipping bit 7 of every byte
+// subtracts the 128 again in two's complement.
+__device__ __forceinline__ uint32_t digit_word(uint32_t x) {
+  return (x + 0x80808080u) ^ 0x80808080u;
+}
+
+// Transpose four digit words (elements k..k+3) into four words holding digit
+// t of those four elements (byte b = element k+b).
+__device__ __forceinline__ void digit_transpose4(const uint32_t w[4], uint32_t out[4]) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int s = 8 * t;
+    out[t] = ((w[0] >> s) & 0xFFu) | (((w[1] >> s) & 0xFFu) << 8) |
+             (((w[2] >> s) & 0xFFu) << 16) | (((w[3] >> s) & 0xFFu) << 24);
+  }
+}
+
+}  // namespace mosaic

@@ -1,0 +1,180 @@
+// Elementwise passes of the MOSAIC path: the mask pass (x + u + e -> ring
+// elements and/or digit layout), sampling (the same pass with only e), the
+// rotation's sign vector, and unmasking without a product term.
+//
+// One thread owns one 16-column digit group of one row: it reads 16 plaintext
+// values, 16 ring words of u, draws 16 noise values (four Philox blocks when
+// the group starts on a block boundary), and writes the four 16-byte digit
+// planes of the group -- contiguous 64-byte chunks, so a wave writes 4 KiB of
+// consecutive memory.
+#include "internal.h"
+
+namespace mosaic {
+namespace {
+
+__device__ __forceinline__ uint32_t load_x(const void* x, int32_t dt, int64_t off) {
+  switch (dt) {
+    case 0: return (uint32_t)(int32_t)((const int8_t*)x)[off];
+    case 1: return (uint32_t)(int32_t)((const int16_t*)x)[off];
+    case 2: return (uint32_t)((const int32_t*)x)[off];
+    default: return ((const uint32_t*)x)[off];
+  }
+}
+
+__global__ __launch_bounds__(256) void mask_kernel(MaskLaunch a, int64_t groups) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = gid / groups;
+  const int64_t g = gid - i * groups;
+  if (i >= a.rows) return;
+  const int64_t j0 = 16 * g;
+  const bool full = (j0 + 16 <= a.cols);
+  uint32_t v[16];
+
+  // plaintext
+  if (a.x != nullptr) {
+    if (full && a.x_dtype == 0 && a.x_cs == 1 &&
+        ((((uintptr_t)a.x) + i * a.x_rs + j0) & 15) == 0) {
+      const uint4 w = *(const uint4*)((const int8_t*)a.x + i * a.x_rs + j0);
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) v[4 * q + b] = (uint32_t)(int32_t)(int8_t)(ww[q] >> (8 * b));
+    } else {
+#pragma unroll
+      for (int b = 0; b < 16; ++b) {
+        const int64_t j = j0 + b;
+        v[b] = (j < a.cols) ? load_x(a.x, a.x_dtype, i * a.x_rs + j * a.x_cs) : 0u;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int b = 0; b < 16; ++b) v[b] = 0u;
+  }
+
+  // precomputed ring mask
+  if (a.u != nullptr) {
+    const uint32_t* up = a.u + i * a.ldu + j0;
+    if (full && ((((uintptr_t)up) & 15) == 0)) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint4 w = ((const uint4*)up)[q];
+        v[4 * q + 0] += w.x; v[4 * q + 1] += w.y; v[4 * q + 2] += w.z; v[4 * q + 3] += w.w;
+      }
+    } else {
+#pragma unroll
+      for (int b = 0; b < 16; ++b)
+        if (j0 + b < a.cols) v[b] += up[b];
+    }
+  }
+
+  // noise drawn in the pass
+  if (a.has_noise) {
+    const RngArgs& r = a.noise;
+    if (!r.transposed) {
+      const uint64_t e0 = (uint64_t)i * (uint64_t)a.cols + (uint64_t)j0;
+      if (full && (e0 & 3) == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t e4[4];
+          sample4_aligned(r, e0 + 4 * q, e4);
+          v[4 * q + 0] += e4[0]; v[4 * q + 1] += e4[1]; v[4 * q + 2] += e4[2]; v[4 * q + 3] += e4[3];
+        }
+      } else {
+        for (int b = 0; b < 16; ++b)
+          if (j0 + b < a.cols) v[b] += sample_elem(r, e0 + b);
+      }
+    } else {
+      // logical matrix is cols x rows; output (i, j) is its element (j, i)
+      for (int b = 0; b < 16; ++b) {
+        const int64_t j = j0 + b;
+        if (j < a.cols) v[b] += sample_elem(r, (uint64_t)j * (uint64_t)a.rows + (uint64_t)i);
+      }
+    }
+  }
+
+  // padding columns of a digit group are zero
+  if (!full) {
+#pragma unroll
+    for (int b = 0; b < 16; ++b)
+      if (j0 + b >= a.cols) v[b] = 0u;
+  }
+
+  if (a.out != nullptr) {
+    uint32_t* op = a.out + i * a.ldo + j0;
+    if (full && ((((uintptr_t)op) & 15) == 0)) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        ((uint4*)op)[q] = make_uint4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    } else {
+      for (int b = 0; b < 16; ++b)
+        if (j0 + b < a.cols) op[b] = v[b];
+    }
+  }
+
+  if (a.dig != nullptr) {
+    uint32_t planes[4][4];  // [digit t][word q]: digit t of elements 4q .. 4q+3
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t w[4] = {digit_word(v[4 * q]), digit_word(v[4 * q + 1]),
+                             digit_word(v[4 * q + 2]), digit_word(v[4 * q + 3])};
+      uint32_t t4[4];
+      digit_transpose4(w, t4);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) planes[t][q] = t4[t];
+    }
+    uint4* dp = (uint4*)(a.dig + i * a.pitch + 64 * g);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) dp[t] = make_uint4(planes[t][0], planes[t][1], planes[t][2], planes[t][3]);
+  }
+}
+
+__global__ __launch_bounds__(256) void signs_kernel(RngArgs r, int64_t n, int8_t* out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t e0 = 4 * i;
+  if (e0 >= n) return;
+  const uint4 w = philox_block(r, (uint64_t)i);
+  const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (e0 + q < n) out[e0 + q] = (ww[q] >> 31) ? (int8_t)-1 : (int8_t)1;
+}
+
+__global__ __launch_bounds__(256) void unmask_elementwise_kernel(GemmLaunch g) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = gid / g.N;
+  const int64_t j = gid - i * g.N;
+  if (i >= g.M) return;
+  uint32_t v = g.ym[i * g.ldy + j];
+  if (g.kc != nullptr) v -= g.kc[i * g.ldk + j];
+  if (g.y != nullptr) g.y[i * g.ldo + j] = (int32_t)v;
+  if (g.y_f32 != nullptr)
+    g.y_f32[i * g.ldf + j] = (float)(int32_t)v * g.s_rows[i] * g.s_cols[j];
+}
+
+}  // namespace
+
+hipError_t launch_mask(const MaskLaunch& a, hipStream_t s) {
+  const int64_t groups = (a.dig != nullptr) ? (64 * ((a.cols + 63) / 64)) / 16 : (a.cols + 15) / 16;
+  const int64_t threads = a.rows * groups;
+  if (threads == 0) return hipSuccess;
+  const int64_t blocks = (threads + 255) / 256;
+  hipLaunchKernelGGL(mask_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, groups);
+  return hipGetLastError();
+}
+
+hipError_t launch_signs(const RngArgs& r, int64_t n, int8_t* out, hipStream_t s) {
+  const int64_t threads = (n + 3) / 4;
+  if (threads == 0) return hipSuccess;
+  hipLaunchKernelGGL(signs_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, r, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_unmask_elementwise(const GemmLaunch& g, hipStream_t s) {
+  const int64_t threads = g.M * g.N;
+  if (threads == 0) return hipSuccess;
+  hipLaunchKernelGGL(unmask_elementwise_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+}  // namespace mosaic

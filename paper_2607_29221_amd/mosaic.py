@@ -1,0 +1,169 @@
+"""Python binding of the MOSAIC C ABI (include/mosaic.h).
+
+Each function has the name of the ABI entry point it calls and only marshals
+arguments: torch tensors (device memory, on the current HIP stream) become
+pointers, leading dimensions and sizes. All arithmetic runs in the HIP
+kernels of libmosaic.so.
+
+Digit-layout matrices are ``Digits`` views: an int8 tensor of shape
+(rows, pitch) plus a column offset (a multiple of 64), so several factors can
+share one buffer side by side.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import torch
+
+from . import _lib
+
+DIST_ZERO, DIST_UNIFORM, DIST_DGAUSS, DIST_SPARSE = 0, 1, 2, 3
+DT_I8, DT_I16, DT_I32, DT_U32 = 0, 1, 2, 3
+_TORCH_DT = {torch.int8: DT_I8, torch.int16: DT_I16, torch.int32: DT_I32}
+
+
+class MosaicError(RuntimeError):
+    def __init__(self, status: int, name: str):
+        msg = _lib.load().mosaic_last_error_message().decode(errors="replace")
+        super().__init__(f"{name} failed with status {status}: {msg}")
+        self.status = status
+
+
+def _check(status: int, name: str) -> None:
+    if status != 0:
+        raise MosaicError(status, name)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def padded_k(k: int) -> int:
+    return 64 * ((k + 63) // 64)
+
+
+@dataclass
+class Digits:
+    """rows x cols ring matrix in digit layout, at column ``col0`` of ``buf``."""
+    buf: torch.Tensor          # int8, (rows, pitch)
+    cols: int
+    col0: int = 0
+
+    @property
+    def rows(self) -> int:
+        return self.buf.shape[0]
+
+    @property
+    def pitch(self) -> int:
+        return self.buf.shape[1]
+
+    @property
+    def ptr(self) -> int:
+        return self.buf.data_ptr() + 4 * self.col0
+
+    @staticmethod
+    def empty(rows: int, cols: int, device="cuda") -> "Digits":
+        return Digits(torch.empty((rows, 4 * padded_k(cols)), dtype=torch.int8, device=device), cols)
+
+    @staticmethod
+    def concat(rows: int, cols: Sequence[int], device="cuda") -> List["Digits"]:
+        """Factors side by side in one buffer (each padded to 64 columns)."""
+        total = sum(padded_k(c) for c in cols)
+        buf = torch.empty((rows, 4 * max(total, 64)), dtype=torch.int8, device=device)
+        out, off = [], 0
+        for c in cols:
+            out.append(Digits(buf, c, off))
+            off += padded_k(c)
+        return out
+
+    def whole(self, cols: int) -> "Digits":
+        """The full buffer seen as one matrix of ``cols`` columns from column 0."""
+        return Digits(self.buf, cols, 0)
+
+
+def rng(seed: int, stream: int, instance: int, dist: int, sigma: float = 0.5, bound: int = 4,
+        log2_inv_density: int = 6, transposed: bool = False) -> _lib.MosaicRng:
+    return _lib.MosaicRng(seed=seed & 0xFFFFFFFFFFFFFFFF, stream=stream, instance=instance, dist=dist,
+                          bound=bound, sigma=sigma, log2_inv_density=log2_inv_density,
+                          transposed=1 if transposed else 0)
+
+
+def mosaic_abi_version() -> int:
+    return _lib.load().mosaic_abi_version()
+
+
+def mosaic_dgauss_thresholds(sigma: float, bound: int) -> List[int]:
+    arr = (ctypes.c_uint64 * max(2 * bound, 1))()
+    _check(_lib.load().mosaic_dgauss_thresholds(sigma, bound, arr), "mosaic_dgauss_thresholds")
+    return [int(arr[i]) for i in range(2 * bound)]
+
+
+def mosaic_sample(r: _lib.MosaicRng, rows: int, cols: int, out: Optional[torch.Tensor] = None,
+                  out_dig: Optional[Digits] = None) -> None:
+    ldo = out.stride(0) if out is not None else 0
+    _check(_lib.load().mosaic_sample(ctypes.byref(r), rows, cols, _ptr(out), ldo,
+                                     out_dig.ptr if out_dig else None, out_dig.pitch if out_dig else 0,
+                                     _stream()), "mosaic_sample")
+
+
+def mosaic_mask(x: Optional[torch.Tensor], u: Optional[torch.Tensor], noise: Optional[_lib.MosaicRng],
+                rows: int, cols: int, out: Optional[torch.Tensor] = None,
+                out_dig: Optional[Digits] = None, x_transposed: bool = False) -> None:
+    """out = x + u + noise (mod 2^32). ``x_transposed`` reads x[j, i] for
+    element (i, j) (x then has shape (cols, rows))."""
+    if x is not None:
+        dt = _TORCH_DT[x.dtype]   # int32 and uint32 embed identically into the ring
+        rs, cs = (x.stride(1), x.stride(0)) if x_transposed else (x.stride(0), x.stride(1))
+    else:
+        dt, rs, cs = DT_U32, 0, 0
+    ldu = u.stride(0) if u is not None else 0
+    ldo = out.stride(0) if out is not None else 0
+    _check(_lib.load().mosaic_mask(_ptr(x), dt, rs, cs, _ptr(u), ldu,
+                                   ctypes.byref(noise) if noise is not None else None, rows, cols,
+                                   _ptr(out), ldo, out_dig.ptr if out_dig else None,
+                                   out_dig.pitch if out_dig else 0, _stream()), "mosaic_mask")
+
+
+def mosaic_masked_matmul(a: Digits, b: Digits, M: int, N: int, K: int, c: torch.Tensor) -> None:
+    """c[:M, :N] = A B^T over Z_{2^32} (c is an int32 tensor holding ring words)."""
+    _check(_lib.load().mosaic_masked_matmul(a.ptr, a.pitch, b.ptr, b.pitch, M, N, K, c.data_ptr(),
+                                            c.stride(0), _stream()), "mosaic_masked_matmul")
+
+
+def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digits], l: Optional[Digits],
+                  M: int, N: int, R: int, y: Optional[torch.Tensor] = None,
+                  s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,
+                  y_f32: Optional[torch.Tensor] = None) -> None:
+    _check(_lib.load().mosaic_unmask(ym.data_ptr(), ym.stride(0), _ptr(kc), kc.stride(0) if kc is not None else 0,
+                                     q.ptr if q else None, q.pitch if q else 0,
+                                     l.ptr if l else None, l.pitch if l else 0, M, N, R,
+                                     _ptr(y), y.stride(0) if y is not None else 0,
+                                     _ptr(s_rows), _ptr(s_cols), _ptr(y_f32),
+                                     y_f32.stride(0) if y_f32 is not None else 0, _stream()), "mosaic_unmask")
+
+
+def mosaic_sample_signs(r: _lib.MosaicRng, n: int, out: torch.Tensor) -> None:
+    _check(_lib.load().mosaic_sample_signs(ctypes.byref(r), n, out.data_ptr(), _stream()), "mosaic_sample_signs")
+
+
+def mosaic_hadamard_rotate(x: torch.Tensor, y: torch.Tensor, block: Optional[int] = None,
+                           signs: Optional[torch.Tensor] = None, inverse: bool = False) -> None:
+    rows, n = x.shape
+    _check(_lib.load().mosaic_hadamard_rotate(x.data_ptr(), x.stride(0), y.data_ptr(), y.stride(0), rows, n,
+                                              n if block is None else block, _ptr(signs), 1 if inverse else 0,
+                                              _stream()), "mosaic_hadamard_rotate")
+
+
+def mosaic_quantize_rows(x: torch.Tensor, qmax: int, q: Optional[torch.Tensor] = None,
+                         q_dig: Optional[Digits] = None, scale: Optional[torch.Tensor] = None) -> None:
+    rows, n = x.shape
+    _check(_lib.load().mosaic_quantize_rows(x.data_ptr(), x.stride(0), rows, n, qmax, _ptr(q),
+                                            q.stride(0) if q is not None else 0,
+                                            q_dig.ptr if q_dig else None, q_dig.pitch if q_dig else 0,
+                                            _ptr(scale), _stream()), "mosaic_quantize_rows")

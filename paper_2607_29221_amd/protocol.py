@@ -1,0 +1,220 @@
+"""Pi_Sec-Approx-MatMul on one GPU (Section 4.2 protocol box), sequenced from
+the C ABI. This module only allocates device buffers and orders the calls;
+every arithmetic step is a libmosaic kernel.
+
+Orientation (build layout): activations A are M x K (tokens x features),
+weights W are N x K (out x in), outputs are M x N. In the paper's notation
+A = X^T and the output is (W X)^T; every product below is the transpose of
+the box's product and is computed as C = A B^T by mosaic_masked_matmul.
+
+Factors of different levels are concatenated along the inner dimension, in
+the slot order (level d, level 1, ..., level d-1):
+    Lcat  = [L | S_2 | ... | S_d]                       N x R   (client)
+    Jcat  = [J_d | J_1 | ... | J_{d-1}]                 N x R   (client)
+    Nccat = [N_1..N_d | N_1 | ... | N_1..N_{d-1}]       K x R   (client)
+    rho   = [R^T | T_2^T | ... | T_d^T]                 M x R   (client, per call)
+    Bext  = [W' ; M_d..M_1 ; M_1 ; ... ; M_{d-1}..M_1]  (N + R) x K (server)
+so that U_a = rho Nccat^T, K_c = rho Jcat^T, [Y' | Q] = A' Bext^T and the
+unmask term is Q Lcat^T, exactly the sums of the protocol box.
+
+Random matrices come from Philox streams keyed by the seed: weight-side
+material uses the weight id as the counter's instance word, per-call
+material the call id.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import List, Optional
+
+import torch
+
+from . import mosaic as m
+from .mosaic import Digits, padded_k
+
+# stream identifiers (counter word 2), one per random matrix of the protocol
+STREAM_EW = 0x10
+STREAM_L = 0x11
+STREAM_M = 0x20     # + i
+STREAM_N = 0x30     # + i
+STREAM_S = 0x40     # + i
+STREAM_EX = 0x50
+STREAM_R = 0x51
+STREAM_T = 0x60     # + i
+STREAM_SIGNS = 0x70
+
+
+def _noise_rng(params, seed: int, stream: int, instance: int):
+    nz = params.noise
+    if nz.kind == "zero":
+        return None
+    if nz.kind != "dgauss":
+        raise ValueError(f"unsupported noise kind {nz.kind!r}")
+    return m.rng(seed, stream, instance, m.DIST_DGAUSS, sigma=nz.sigma, bound=nz.bound)
+
+
+def _ring_empty(rows: int, cols: int, device) -> torch.Tensor:
+    return torch.empty((rows, cols), dtype=torch.int32, device=device)
+
+
+class MaskedWeight:
+    """Init W of the protocol box for one plaintext weight matrix W (N x K,
+    int8/int16/int32 on the GPU). Holds the server's Bext and the client's
+    unmasking material."""
+
+    def __init__(self, W: torch.Tensor, params, seed: int, weight_id: int = 0):
+        dev = W.device
+        N, K = W.shape
+        r = list(params.ranks)
+        d = len(r)
+        self.params, self.seed, self.weight_id = params, seed, weight_id
+        self.N, self.K, self.d = N, K, d
+        self.slot_levels = [d] + list(range(1, d))            # level of each slot
+        self.slot_ranks = [r[lv - 1] for lv in self.slot_levels]
+        self.R = sum(padded_k(c) for c in self.slot_ranks)    # padded inner width
+        U = m.DIST_UNIFORM
+        s = seed
+
+        Kp = padded_k(K)
+        slot_of = {lv: k for k, lv in enumerate(self.slot_levels)}
+        # destinations: the server's Bext rows, and the client's concatenated
+        # factors (one buffer each, slots side by side)
+        self.Bext = Digits(torch.zeros((N + self.R, 4 * Kp), dtype=torch.int8, device=dev), K)
+        self.q_cols, row = [], N
+        for ri in self.slot_ranks:
+            self.q_cols.append(row)          # column of this slot's Q in [Y' | Q]
+            row += padded_k(ri)
+        self.n_out = N + self.R
+        McTcat = Digits.concat(K, self.slot_ranks, dev)
+        bx = torch.empty((K + N, 4 * max(self.R, 64)), dtype=torch.int8, device=dev)
+        self.Bx = Digits(bx, self.R)         # [Nccat ; Jcat], the per-call product's operand
+        slot_col = [sum(padded_k(c) for c in self.slot_ranks[:k]) for k in range(d)]
+
+        def mc_dst(i):    # M_i ... M_1 (r_i x K): rows of Bext
+            r0 = self.q_cols[slot_of[i]]
+            return Digits(self.Bext.buf[r0: r0 + r[i - 1]], K)
+
+        def mct_dst(i):   # (M_i ... M_1)^T (K x r_i)
+            return McTcat[slot_of[i]]
+
+        def nc_dst(i):    # N_1 ... N_i (K x r_i): upper rows of Bx
+            return Digits(bx[:K], r[i - 1], slot_col[slot_of[i]])
+
+        NcT: List[Digits] = []                # (N_1 ... N_i)^T (r_i x K)
+        for i in range(1, d + 1):
+            ri = r[i - 1]
+            nct = Digits.empty(ri, K, dev)
+            if i == 1:
+                m.mosaic_sample(m.rng(s, STREAM_M + 1, weight_id, U), ri, K, out_dig=mc_dst(1))
+                m.mosaic_sample(m.rng(s, STREAM_M + 1, weight_id, U, transposed=True), K, ri, out_dig=mct_dst(1))
+                m.mosaic_sample(m.rng(s, STREAM_N + 1, weight_id, U), K, ri, out_dig=nc_dst(1))
+                m.mosaic_sample(m.rng(s, STREAM_N + 1, weight_id, U, transposed=True), ri, K, out_dig=nct)
+            else:
+                rp = r[i - 2]
+                Mi = Digits.empty(ri, rp, dev)                  # M_i (r_i x r_{i-1})
+                NiT = Digits.empty(ri, rp, dev)                 # N_i^T
+                m.mosaic_sample(m.rng(s, STREAM_M + i, weight_id, U), ri, rp, out_dig=Mi)
+                m.mosaic_sample(m.rng(s, STREAM_N + i, weight_id, U, transposed=True), ri, rp, out_dig=NiT)
+                self._product_to_digits(Mi, mct_dst(i - 1), ri, K, rp, mc_dst(i))    # M_i Mc_{i-1}
+                self._product_to_digits(mct_dst(i - 1), Mi, K, ri, rp, mct_dst(i))   # McT_{i-1} M_i^T
+                self._product_to_digits(nc_dst(i - 1), NiT, K, ri, rp, nc_dst(i))    # Nc_{i-1} N_i
+                self._product_to_digits(NiT, nc_dst(i - 1), ri, K, rp, nct)          # N_i^T Nc_{i-1}^T
+            NcT.append(nct)
+
+        # client: Lcat = [L | S_2 | ... | S_d]
+        self.Lcat = Digits.concat(N, self.slot_ranks, dev)
+        m.mosaic_sample(m.rng(s, STREAM_L, weight_id, U), N, r[d - 1], out_dig=self.Lcat[0])
+        for slot, lv in enumerate(self.slot_levels[1:], start=1):
+            m.mosaic_sample(m.rng(s, STREAM_S + lv + 1, weight_id, m.DIST_SPARSE,
+                                  log2_inv_density=params.sparse_log2_inv_density),
+                            N, r[lv - 1], out_dig=self.Lcat[slot])
+
+        # U_w = Lcat McTcat^T (= L Mc_d + sum S_{i+1} Mc_i); W' = W + U_w + E_w
+        U_w = _ring_empty(N, K, dev)
+        m.mosaic_masked_matmul(self.Lcat[0].whole(self.R), McTcat[0].whole(self.R), N, K, self.R, U_w)
+        del McTcat
+        ew = _noise_rng(params, s, STREAM_EW, weight_id)
+        m.mosaic_mask(W, U_w, ew, N, K, out_dig=Digits(self.Bext.buf[:N], K))
+        del U_w
+
+        # client: J_i = (W + E_w) Nc_i, stored in the lower rows of Bx
+        WE = Digits.empty(N, K, dev)
+        m.mosaic_mask(W, None, ew, N, K, out_dig=WE)
+        for lv in range(1, d + 1):
+            ri = r[lv - 1]
+            J = _ring_empty(N, ri, dev)
+            m.mosaic_masked_matmul(WE, NcT[lv - 1], N, ri, K, J)
+            m.mosaic_mask(None, J, None, N, ri, out_dig=Digits(bx[K:], ri, slot_col[slot_of[lv]]))
+        del WE, NcT
+
+    @staticmethod
+    def _product_to_digits(a: Digits, b: Digits, rows: int, cols: int, inner: int, out: Digits) -> None:
+        tmp = _ring_empty(rows, cols, a.buf.device)
+        m.mosaic_masked_matmul(a, b, rows, cols, inner, tmp)
+        m.mosaic_mask(None, tmp, None, rows, cols, out_dig=out)
+
+
+@dataclass
+class CallBuffers:
+    rho: List[Digits]          # [R^T | T_2^T | ...] slots, M x R
+    UK: torch.Tensor           # [U_a | K_c], M x (K + N)
+    A_masked: Digits           # A' (M x K digits)
+    YQ: torch.Tensor           # [Y' | Q], M x (N + R)
+    Qdig: List[Digits]         # Q slots in digit layout, M x R
+    Y: torch.Tensor            # unmasked output, M x N int32
+
+
+def alloc_call(w: MaskedWeight, M: int, device="cuda") -> CallBuffers:
+    return CallBuffers(
+        rho=Digits.concat(M, w.slot_ranks, device),
+        UK=_ring_empty(M, w.K + w.N, device),
+        A_masked=Digits.empty(M, w.K, device),
+        YQ=_ring_empty(M, w.n_out, device),
+        Qdig=Digits.concat(M, w.slot_ranks, device),
+        Y=_ring_empty(M, w.N, device),
+    )
+
+
+def init_x(w: MaskedWeight, M: int, call_id: int, buf: CallBuffers) -> None:
+    """Init X (box, online step 1): sample R and T_i, then U_a and K_c in one
+    product (E_x is drawn later, inside the mask pass)."""
+    p, s, r = w.params, w.seed, list(w.params.ranks)
+    m.mosaic_sample(m.rng(s, STREAM_R, call_id, m.DIST_UNIFORM), M, r[w.d - 1], out_dig=buf.rho[0])
+    for slot, lv in enumerate(w.slot_levels[1:], start=1):
+        m.mosaic_sample(m.rng(s, STREAM_T + lv + 1, call_id, m.DIST_SPARSE,
+                              log2_inv_density=p.sparse_log2_inv_density),
+                        M, r[lv - 1], out_dig=buf.rho[slot])
+    m.mosaic_masked_matmul(buf.rho[0].whole(w.R), w.Bx, M, w.K + w.N, w.R, buf.UK)
+
+
+def mask(w: MaskedWeight, A: torch.Tensor, call_id: int, buf: CallBuffers) -> None:
+    """Online step 2: A' = A + U_a + E_a, written in digit layout."""
+    M = A.shape[0]
+    ex = _noise_rng(w.params, w.seed, STREAM_EX, call_id)
+    m.mosaic_mask(A, buf.UK[:, : w.K], ex, M, w.K, out_dig=buf.A_masked)
+
+
+def server(w: MaskedWeight, M: int, buf: CallBuffers) -> None:
+    """Online step 3 on the untrusted side: [Y' | Q] = A' Bext^T."""
+    m.mosaic_masked_matmul(buf.A_masked, w.Bext, M, w.n_out, w.K, buf.YQ)
+
+
+def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tensor] = None,
+           s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None) -> None:
+    """Online step 5: Y = Y' - K_c - Q Lcat^T (digits of Q first)."""
+    r = list(w.params.ranks)
+    for slot, lv in enumerate(w.slot_levels):
+        c0 = w.q_cols[slot]
+        m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
+    m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
+                    M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
+
+
+def run_call(w: MaskedWeight, A: torch.Tensor, call_id: int, buf: Optional[CallBuffers] = None) -> CallBuffers:
+    M = A.shape[0]
+    if buf is None:
+        buf = alloc_call(w, M, A.device)
+    init_x(w, M, call_id, buf)
+    mask(w, A, call_id, buf)
+    server(w, M, buf)
+    unmask(w, M, buf)
+    return buf

@@ -1,0 +1,148 @@
+"""Host-side checks of the C ABI (no GPU needed): the built library loads,
+exports every function include/mosaic.h declares, rejects invalid arguments
+before launching anything, and computes the same sampler thresholds as the
+oracle."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle.sampling import dgauss_thresholds
+from paper_2607_29221_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mosaic.h")
+
+INVALID, UNSUPPORTED = -1, -2
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:mosaic_status|int32_t|const char\*)\s+(mosaic_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(_lib.EXPORTED)
+
+
+def test_abi_version(lib):
+    m = re.search(r"#define MOSAIC_ABI_VERSION (\d+)", open(HEADER).read())
+    assert lib.mosaic_abi_version() == int(m.group(1))
+
+
+@pytest.mark.parametrize("sigma,bound", [(0.5, 4), (1.0, 8), (0.0, 4), (3.2, 15), (0.25, 2), (2.0, 1)])
+def test_dgauss_thresholds_match_oracle(lib, sigma, bound):
+    arr = (ctypes.c_uint64 * (2 * bound))()
+    assert lib.mosaic_dgauss_thresholds(sigma, bound, arr) == 0
+    assert [int(v) for v in arr] == dgauss_thresholds(sigma, bound)
+
+
+def test_dgauss_thresholds_rejects(lib):
+    arr = (ctypes.c_uint64 * 40)()
+    assert lib.mosaic_dgauss_thresholds(0.5, 16, arr) == INVALID
+    assert lib.mosaic_dgauss_thresholds(-1.0, 4, arr) == INVALID
+    assert lib.mosaic_dgauss_thresholds(float("nan"), 4, arr) == INVALID
+    assert lib.mosaic_dgauss_thresholds(0.5, 4, None) == INVALID
+
+
+FAKE = 1 << 20      # an aligned non-null address; never dereferenced on these paths
+
+
+def test_mask_validation(lib):
+    r = _lib.MosaicRng(seed=1, stream=2, instance=3, dist=1)
+    # no output
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, ctypes.byref(r), 4, 4, None, 0, None, 0, None) == INVALID
+    # bad pitch (must be a multiple of 64 and >= 4 * padded K)
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, ctypes.byref(r), 4, 100, None, 0, FAKE, 256, None) == INVALID
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, ctypes.byref(r), 4, 100, None, 0, FAKE, 520, None) == INVALID
+    # misaligned digits
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, ctypes.byref(r), 4, 64, None, 0, FAKE + 8, 256, None) == INVALID
+    # ldu / ldo too small, bad dtype, negative size
+    assert lib.mosaic_mask(None, 0, 0, 0, FAKE, 3, None, 4, 4, FAKE, 4, None, 0, None) == INVALID
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, None, 4, 4, FAKE, 3, None, 0, None) == INVALID
+    assert lib.mosaic_mask(FAKE, 9, 4, 1, None, 0, None, 4, 4, FAKE, 4, None, 0, None) == INVALID
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, None, -1, 4, FAKE, 4, None, 0, None) == INVALID
+    # bad distributions
+    for bad in (_lib.MosaicRng(dist=7), _lib.MosaicRng(dist=2, bound=16, sigma=0.5),
+                _lib.MosaicRng(dist=2, bound=4, sigma=-1.0), _lib.MosaicRng(dist=3, log2_inv_density=32)):
+        assert lib.mosaic_mask(None, 0, 0, 0, None, 0, ctypes.byref(bad), 4, 4, FAKE, 4, None, 0, None) == INVALID
+    assert len(lib.mosaic_last_error_message()) > 0
+
+
+def test_matmul_validation(lib):
+    # K at the accumulator limit
+    assert lib.mosaic_masked_matmul(FAKE, 4 * 32768, FAKE, 4 * 32768, 1, 1, 32768, FAKE, 1, None) == UNSUPPORTED
+    assert lib.mosaic_masked_matmul(FAKE, 256, FAKE, 256, 1, 1, 64, None, 1, None) == INVALID
+    assert lib.mosaic_masked_matmul(FAKE, 256, FAKE, 256, 1, 2, 64, FAKE, 1, None) == INVALID   # ldc < N
+    assert lib.mosaic_masked_matmul(FAKE, 192, FAKE, 256, 1, 1, 64, FAKE, 1, None) == INVALID   # pitch
+    assert lib.mosaic_masked_matmul(None, 256, FAKE, 256, 1, 1, 64, FAKE, 1, None) == INVALID
+    assert lib.mosaic_masked_matmul(FAKE, 256, FAKE, 256, -1, 1, 64, FAKE, 1, None) == INVALID
+
+
+def test_unmask_validation(lib):
+    args = dict(ym=FAKE, ldy=8, kc=None, ldk=0, q=FAKE, qp=256, l=FAKE, lp=256, M=2, N=8, R=64,
+                y=FAKE, ldo=8, sr=None, sc=None, yf=None, ldf=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return lib.mosaic_unmask(a["ym"], a["ldy"], a["kc"], a["ldk"], a["q"], a["qp"], a["l"], a["lp"], a["M"],
+                                 a["N"], a["R"], a["y"], a["ldo"], a["sr"], a["sc"], a["yf"], a["ldf"], None)
+    assert call(ym=None) == INVALID
+    assert call(y=None) == INVALID
+    assert call(ldy=7) == INVALID
+    assert call(kc=FAKE, ldk=4) == INVALID
+    assert call(qp=128) == INVALID
+    assert call(l=None) == INVALID
+    assert call(yf=FAKE, ldf=8) == INVALID          # fp32 output without scales
+    assert call(R=40000, qp=4 * 40000 + 64, lp=4 * 40000 + 64) == UNSUPPORTED
+
+
+def test_hadamard_validation(lib):
+    def call(x=FAKE, ldx=64, y=FAKE + (1 << 24), ldy=64, rows=2, n=64, block=64, signs=None, inv=0):
+        return lib.mosaic_hadamard_rotate(x, ldx, y, ldy, rows, n, block, signs, inv, None)
+    assert call(block=48) == UNSUPPORTED
+    assert call(block=8) == UNSUPPORTED
+    assert call(block=65536, n=65536, ldx=65536, ldy=65536) == UNSUPPORTED
+    assert call(n=96, block=64, ldx=96, ldy=96) == INVALID      # n not a multiple of block
+    assert call(ldx=62) == INVALID
+    assert call(x=FAKE + 4) == INVALID                           # misaligned
+    assert call(y=FAKE + 64) == INVALID                          # overlapping, not in place
+    assert call(y=FAKE, ldy=128, ldx=64) == INVALID              # in place with different ld
+    assert call(x=None) == INVALID
+
+
+def test_quantize_validation(lib):
+    assert lib.mosaic_quantize_rows(FAKE, 8, 2, 8, 0, FAKE, 8, None, 0, None, None) == INVALID
+    assert lib.mosaic_quantize_rows(FAKE, 8, 2, 8, 127, None, 0, None, 0, None, None) == INVALID
+    assert lib.mosaic_quantize_rows(FAKE, 8, 2, 8, 127, FAKE, 4, None, 0, None, None) == INVALID
+    assert lib.mosaic_quantize_rows(FAKE, 8, 2, 8, 127, None, 0, FAKE, 64, None, None) == INVALID
+
+
+def test_signs_validation(lib):
+    r = _lib.MosaicRng(seed=1)
+    assert lib.mosaic_sample_signs(ctypes.byref(r), 8, None, None) == INVALID
+    assert lib.mosaic_sample_signs(None, 8, FAKE, None) == INVALID
+    assert lib.mosaic_sample_signs(ctypes.byref(r), -1, FAKE, None) == INVALID
+
+
+def test_zero_sized_calls_are_noops(lib):
+    r = _lib.MosaicRng(seed=1, dist=1)
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, ctypes.byref(r), 0, 5, None, 0, None, 0, None) == 0
+    assert lib.mosaic_mask(None, 0, 0, 0, None, 0, ctypes.byref(r), 5, 0, None, 0, None, 0, None) == 0
+    assert lib.mosaic_sample(ctypes.byref(r), 0, 0, None, 0, None, 0, None) == 0
+    assert lib.mosaic_masked_matmul(None, 0, None, 0, 0, 7, 64, None, 7, None) == 0
+    assert lib.mosaic_masked_matmul(None, 0, None, 0, 7, 0, 64, None, 0, None) == 0
+    assert lib.mosaic_unmask(None, 0, None, 0, None, 0, None, 0, 0, 4, 64, None, 0, None, None, None, 0, None) == 0
+    assert lib.mosaic_sample_signs(ctypes.byref(r), 0, None, None) == 0
+    assert lib.mosaic_hadamard_rotate(None, 64, None, 64, 0, 64, 64, None, 0, None) == 0
+    assert lib.mosaic_quantize_rows(None, 8, 0, 8, 127, None, 0, None, 0, None, None) == 0

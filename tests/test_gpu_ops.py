@@ -1,0 +1,246 @@
+"""Parity of each HIP entry point with the CPU oracle on seeded inputs that
+span several tiles and ragged tails. Ring results must match bit for bit; the
+rotation to 1e-5 of each row's peak (fp32 against the float64 oracle)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import hadamard as ohad
+from oracle import quant as oquant
+from oracle import sampling as smp
+from oracle.ring import ring_matmul, ring_sub, signed_digits
+from paper_2607_29221_amd import mosaic as m
+from paper_2607_29221_amd.mosaic import Digits
+from tests.gpu_util import pad_is_zero, to_dev_ring, to_np_u32, unpack_digits
+
+pytestmark = pytest.mark.gpu
+
+SEED = 0x5EED_0001_2345_6789
+
+
+def _rng_np(seed):
+    return np.random.default_rng(seed)
+
+
+@pytest.mark.parametrize("rows,cols", [(1, 1), (5, 37), (64, 512), (33, 130)])
+@pytest.mark.parametrize("kind", ["uniform", "dgauss", "sparse"])
+@pytest.mark.parametrize("transposed", [False, True])
+def test_sample(rows, cols, kind, transposed):
+    dist = {"uniform": m.DIST_UNIFORM, "dgauss": m.DIST_DGAUSS, "sparse": m.DIST_SPARSE}[kind]
+    r = m.rng(SEED, 0x33, 7, dist, sigma=0.5, bound=4, log2_inv_density=2, transposed=transposed)
+    out = torch.empty((rows, cols), dtype=torch.int32, device="cuda")
+    dig = Digits.empty(rows, cols)
+    m.mosaic_sample(r, rows, cols, out=out, out_dig=dig)
+    torch.cuda.synchronize()
+    if transposed:
+        ref = smp.sample_matrix(kind, cols, rows, SEED, 0x33, 7, sigma=0.5, bound=4, log2_inv_density=2).T
+    else:
+        ref = smp.sample_matrix(kind, rows, cols, SEED, 0x33, 7, sigma=0.5, bound=4, log2_inv_density=2)
+    assert np.array_equal(to_np_u32(out), ref)
+    assert np.array_equal(unpack_digits(dig), ref)
+    assert pad_is_zero(dig)
+
+
+def test_digit_bytes_are_balanced_digits():
+    x = _rng_np(1).integers(0, 2 ** 32, (3, 80), dtype=np.uint64).astype(np.uint32)
+    x[0, :8] = [0, 1, 0x7F, 0x80, 0xFF, 0x80808080, 0x7F7F7F80, 0xFFFFFFFF]
+    dig = Digits.empty(3, 80)
+    m.mosaic_mask(to_dev_ring(x), None, None, 3, 80, out_dig=dig)
+    raw = dig.buf.cpu().numpy().reshape(3, 128 // 16, 4, 16)
+    d = signed_digits(x)                          # (3, 80, 4)
+    for k in range(80):
+        g, b = divmod(k, 16)
+        assert np.array_equal(raw[:, g, :, b], d[:, k, :])
+
+
+def test_signs():
+    for n in (1, 7, 8192, 28672):
+        out = torch.empty(n, dtype=torch.int8, device="cuda")
+        m.mosaic_sample_signs(m.rng(SEED, 0x70, 3, 0), n, out)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), smp.sample_signs(n, SEED, 3))
+
+
+@pytest.mark.parametrize("dtype", [torch.int8, torch.int16, torch.int32])
+@pytest.mark.parametrize("rows,cols", [(7, 100), (64, 512), (2, 16)])
+def test_mask(dtype, rows, cols):
+    rng = _rng_np(rows * cols)
+    info = {torch.int8: (-128, 128), torch.int16: (-32768, 32768), torch.int32: (-2 ** 31, 2 ** 31)}[dtype]
+    x = rng.integers(info[0], info[1], (rows, cols)).astype({torch.int8: np.int8, torch.int16: np.int16,
+                                                             torch.int32: np.int32}[dtype])
+    u = rng.integers(0, 2 ** 32, (rows, cols + 3), dtype=np.uint64).astype(np.uint32)
+    noise = m.rng(SEED, 0x50, 9, m.DIST_DGAUSS, sigma=0.5, bound=4)
+    out = torch.empty((rows, cols), dtype=torch.int32, device="cuda")
+    dig = Digits.empty(rows, cols)
+    u_dev = to_dev_ring(u)
+    m.mosaic_mask(torch.from_numpy(x).cuda(), u_dev[:, :cols], noise, rows, cols, out=out, out_dig=dig)
+    torch.cuda.synchronize()
+    e = smp.sample_matrix("dgauss", rows, cols, SEED, 0x50, 9)
+    ref = ((x.astype(np.int64) & 0xFFFFFFFF) + u[:, :cols].astype(np.int64) + e.astype(np.int64)) & 0xFFFFFFFF
+    assert np.array_equal(to_np_u32(out), ref.astype(np.uint32))
+    assert np.array_equal(unpack_digits(dig), ref.astype(np.uint32))
+
+
+def test_mask_transposed_input_and_sparse_noise():
+    rows, cols = 40, 72
+    xt = _rng_np(3).integers(-127, 128, (cols, rows)).astype(np.int8)      # stored transposed
+    noise = m.rng(SEED, 0x41, 1, m.DIST_SPARSE, log2_inv_density=3)
+    dig = Digits.empty(rows, cols)
+    m.mosaic_mask(torch.from_numpy(xt).cuda(), None, noise, rows, cols, out_dig=dig, x_transposed=True)
+    torch.cuda.synchronize()
+    e = smp.sample_matrix("sparse", rows, cols, SEED, 0x41, 1, log2_inv_density=3)
+    ref = ((xt.T.astype(np.int64) & 0xFFFFFFFF) + e) & 0xFFFFFFFF
+    assert np.array_equal(unpack_digits(dig), ref.astype(np.uint32))
+
+
+def _random_ring(rng, shape, edge=False):
+    x = rng.integers(0, 2 ** 32, shape, dtype=np.uint64).astype(np.uint32)
+    if edge:
+        flat = x.reshape(-1)
+        vals = np.array([0, 1, 0x7FFFFFFF, 0x80000000, 0xFFFFFFFF, 0x80808080, 0x7F7F7F80], dtype=np.uint32)
+        flat[: min(flat.size, 64)] = np.resize(vals, min(flat.size, 64))
+    return x
+
+
+def _gemm(a_np, b_np):
+    M, K = a_np.shape
+    N = b_np.shape[0]
+    A, B = Digits.empty(M, K), Digits.empty(N, K)
+    m.mosaic_mask(to_dev_ring(a_np), None, None, M, K, out_dig=A)
+    m.mosaic_mask(to_dev_ring(b_np), None, None, N, K, out_dig=B)
+    C = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    m.mosaic_masked_matmul(A, B, M, N, K, C)
+    torch.cuda.synchronize()
+    return to_np_u32(C)
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 512, 512), (1, 1, 1), (300, 260, 1000), (130, 129, 70),
+                                   (128, 128, 64), (257, 3, 192), (5, 300, 4096), (0, 10, 64), (10, 10, 0)])
+def test_masked_matmul(M, N, K):
+    rng = _rng_np(M * 7 + N * 3 + K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    got = _gemm(a, b)
+    assert np.array_equal(got, ring_matmul(a, b.T))
+
+
+def test_masked_matmul_accumulator_extreme():
+    """All digits -128 (x = 0x7F7F7F80) at the largest supported K: every
+    limb product is +2^14, the four-product class reaches 4 K 2^14 < 2^31."""
+    M, N, K = 130, 70, 32767
+    a = np.full((M, K), 0x7F7F7F80, dtype=np.uint32)
+    b = np.full((N, K), 0x7F7F7F80, dtype=np.uint32)
+    got = _gemm(a, b)
+    ref = (K * (0x7F7F7F80 ** 2)) % (1 << 32)
+    assert np.all(got == ref)
+
+
+def test_masked_matmul_ldc_and_offsets():
+    """Output with a leading dimension > N and operands at a column offset in
+    a wider digit buffer."""
+    rng = _rng_np(11)
+    M, N, K = 70, 50, 130
+    a = _random_ring(rng, (M, K))
+    b = _random_ring(rng, (N, K))
+    left = Digits.concat(M, [64, K])
+    right = Digits.concat(N, [K, 100])
+    m.mosaic_mask(to_dev_ring(a), None, None, M, K, out_dig=left[1])
+    m.mosaic_mask(to_dev_ring(b), None, None, N, K, out_dig=right[0])
+    C = torch.zeros((M, N + 17), dtype=torch.int32, device="cuda")
+    m.mosaic_masked_matmul(left[1], right[0], M, N, K, C[:, 5:5 + N])
+    torch.cuda.synchronize()
+    got = to_np_u32(C)
+    assert np.array_equal(got[:, 5:5 + N], ring_matmul(a, b.T))
+    assert np.all(got[:, :5] == 0) and np.all(got[:, 5 + N:] == 0)
+
+
+@pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192)])
+@pytest.mark.parametrize("with_k", [True, False])
+def test_unmask(M, N, R, with_k):
+    rng = _rng_np(M + N + R)
+    ym = _random_ring(rng, (M, N))
+    kc = _random_ring(rng, (M, N)) if with_k else None
+    q = _random_ring(rng, (M, R))
+    l = _random_ring(rng, (N, R))
+    Q, L = Digits.empty(M, max(R, 1)), Digits.empty(N, max(R, 1))
+    if R:
+        m.mosaic_mask(to_dev_ring(q), None, None, M, R, out_dig=Q)
+        m.mosaic_mask(to_dev_ring(l), None, None, N, R, out_dig=L)
+    y = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    m.mosaic_unmask(to_dev_ring(ym), to_dev_ring(kc) if with_k else None, Q if R else None, L if R else None,
+                    M, N, R, y=y)
+    torch.cuda.synchronize()
+    ref = ym.copy()
+    if with_k:
+        ref = ring_sub(ref, kc)
+    if R:
+        ref = ring_sub(ref, ring_matmul(q, l.T))
+    assert np.array_equal(y.cpu().numpy(), ref.view(np.int32))
+
+
+def test_unmask_dequantised():
+    rng = _rng_np(5)
+    M, N, R = 40, 90, 64
+    ym = _random_ring(rng, (M, N))
+    q = _random_ring(rng, (M, R))
+    l = _random_ring(rng, (N, R))
+    Q, L = Digits.empty(M, R), Digits.empty(N, R)
+    m.mosaic_mask(to_dev_ring(q), None, None, M, R, out_dig=Q)
+    m.mosaic_mask(to_dev_ring(l), None, None, N, R, out_dig=L)
+    sr = torch.rand(M, device="cuda") * 1e-3
+    sc = torch.rand(N, device="cuda") * 1e-3
+    yf = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    m.mosaic_unmask(to_dev_ring(ym), None, Q, L, M, N, R, s_rows=sr, s_cols=sc, y_f32=yf)
+    torch.cuda.synchronize()
+    yi = ring_sub(ym, ring_matmul(q, l.T)).view(np.int32)
+    ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+    assert np.array_equal(yf.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("rows,n,block", [(3, 16, 16), (5, 64, 64), (4, 1024, 1024), (6, 8192, 8192),
+                                          (2, 32768, 32768), (3, 28672, 4096), (2, 4096, 256)])
+@pytest.mark.parametrize("inverse", [False, True])
+def test_hadamard(rows, n, block, inverse):
+    x = _rng_np(n + rows).standard_normal((rows, n)).astype(np.float32)
+    x[0, 3] *= 50.0
+    signs = smp.sample_signs(n, SEED, 1)
+    xd = torch.from_numpy(x).cuda()
+    y = torch.empty_like(xd)
+    m.mosaic_hadamard_rotate(xd, y, block=block, signs=torch.from_numpy(signs).cuda(), inverse=inverse)
+    torch.cuda.synchronize()
+    ref = ohad.rotate(x.astype(np.float64), signs, block=block, inverse=inverse)
+    err = np.max(np.abs(y.cpu().numpy().astype(np.float64) - ref), axis=1) / np.max(np.abs(ref), axis=1)
+    assert np.all(err <= 1e-5), err.max()
+
+
+def test_hadamard_in_place_roundtrip_and_no_signs():
+    rows, n = 8, 8192
+    x = _rng_np(9).standard_normal((rows, n)).astype(np.float32)
+    xd = torch.from_numpy(x).cuda()
+    signs = torch.from_numpy(smp.sample_signs(n, SEED, 2)).cuda()
+    m.mosaic_hadamard_rotate(xd, xd, signs=signs)
+    m.mosaic_hadamard_rotate(xd, xd, signs=signs, inverse=True)
+    torch.cuda.synchronize()
+    back = xd.cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(back - x) / np.max(np.abs(x), axis=1, keepdims=True)) <= 1e-5
+    y = torch.empty((rows, n), dtype=torch.float32, device="cuda")
+    m.mosaic_hadamard_rotate(torch.from_numpy(x).cuda(), y)
+    torch.cuda.synchronize()
+    ref = ohad.rotate(x.astype(np.float64), np.ones(n, dtype=np.int8))
+    assert np.max(np.abs(y.cpu().numpy() - ref) / np.max(np.abs(ref), axis=1, keepdims=True)) <= 1e-5
+
+
+@pytest.mark.parametrize("rows,n,qmax", [(5, 100, 127), (16, 8192, 1997), (3, 28672, 567), (2, 64, 1)])
+def test_quantize(rows, n, qmax):
+    x = _rng_np(n).standard_normal((rows, n)).astype(np.float32)
+    x[1] = 0.0
+    xd = torch.from_numpy(x).cuda()
+    q = torch.empty((rows, n), dtype=torch.int32, device="cuda")
+    dig = Digits.empty(rows, n)
+    sc = torch.empty(rows, dtype=torch.float32, device="cuda")
+    m.mosaic_quantize_rows(xd, qmax, q=q, q_dig=dig, scale=sc)
+    torch.cuda.synchronize()
+    qr, sr = oquant.quantize_rows(x, qmax)
+    assert np.array_equal(sc.cpu().numpy(), sr)
+    assert np.array_equal(q.cpu().numpy(), qr)
+    assert np.array_equal(unpack_digits(dig), qr.view(np.uint32))
