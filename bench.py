@@ -1,0 +1,242 @@
+"""Benchmark of the MOSAIC hot path on one MI355X.
+
+Workload (prefill-shaped masked products at 70B-layer shapes): M = 2048
+tokens; (K, N) in {(8192, 8192), (8192, 28672), (28672, 8192)}; uniform int8
+plaintext in [-127, 127] (seed 2); depth-1 LWE mask of rank r = 1536 with
+discrete Gaussian error sigma = 0.5, |e| <= 4. Init W runs once per shape,
+outside the timed region.
+
+One step = for every shape, one full call of the protocol: Init X (sample R,
+then [U_a | K_c] in one ring product), the mask pass (A' = A + U_a + E_a, in
+digit layout), the server product ([Y' | Q] = A' Bext^T) and unmasking
+(digits of Q, then Y = Y' - K_c - Q L^T). ``value`` counts the plaintext
+product's ring operations, 2 M K N per shape, over the step time (ring-TOPS).
+
+Printed as one JSON line. ``roofline`` covers the server product kernel
+(per launch: 10 int8 MACs = 20 int8 ops per ring MAC, M K (N + r) ring MACs),
+timed with HIP events on the stream it runs on. ``cpu_baseline`` times the
+CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+INT8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA, TOP/s
+HBM_PEAK_GBS = 8000.0
+
+
+def _events(n):
+    import torch
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def run_gpu(steps: int, warmup: int, extras: bool):
+    import torch
+
+    from paper_2607_29221_amd import mosaic as m
+    from paper_2607_29221_amd import protocol as gp
+    from synthetic_inputs import PARAMS_PAPER_D1, PREFILL_KN, PREFILL_M, PREFILL_SEED, int8_operands
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    params = PARAMS_PAPER_D1
+    M = PREFILL_M
+    seed = 0x6D6F736169630000 | PREFILL_SEED
+    shapes = []
+    for idx, (K, N) in enumerate(PREFILL_KN):
+        A, W = int8_operands(M, K, N, PREFILL_SEED)
+        Ad = torch.from_numpy(A).to(dev)
+        Wd = torch.from_numpy(W).to(dev)
+        w = gp.MaskedWeight(Wd, params, seed, weight_id=idx)
+        del Wd
+        shapes.append((K, N, Ad, w, gp.alloc_call(w, M, dev)))
+    torch.cuda.synchronize()
+
+    phases = ("init_x", "mask", "server", "unmask")
+    ev = {(s, p): [] for s in range(len(shapes)) for p in phases}
+
+    def step(call_id, record):
+        for si, (K, N, Ad, w, buf) in enumerate(shapes):
+            fns = (lambda: gp.init_x(w, M, call_id, buf), lambda: gp.mask(w, Ad, call_id, buf),
+                   lambda: gp.server(w, M, buf), lambda: gp.unmask(w, M, buf))
+            for p, fn in zip(phases, fns):
+                if record:
+                    e0, e1 = _events(2)
+                    e0.record()
+                    fn()
+                    e1.record()
+                    ev[(si, p)].append((e0, e1))
+                else:
+                    fn()
+
+    for i in range(warmup):
+        step(1000 + i, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i, True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    ms = {k: sum(a.elapsed_time(b) for a, b in v) / len(v) for k, v in ev.items()}
+    r = params.ranks[0]
+    ring_ops = sum(2.0 * M * K * N for K, N, *_ in shapes)
+    server_ops = [20.0 * M * K * (N + w.R) for K, N, _, w, _ in shapes]
+    server_ms = [ms[(s, "server")] for s in range(len(shapes))]
+    achieved = sum(server_ops) / (sum(server_ms) * 1e-3) / 1e12
+    per_shape = []
+    for s, (K, N, _, w, _) in enumerate(shapes):
+        per_shape.append({
+            "K": K, "N": N,
+            "ms": {p: round(ms[(s, p)], 4) for p in phases},
+            "server_ring_tops": round(2.0 * M * K * (N + w.R) / (ms[(s, "server")] * 1e-3) / 1e12, 2),
+            "server_int8_tops": round(server_ops[s] / (ms[(s, "server")] * 1e-3) / 1e12, 1),
+            "mask_gbs": round((M * K * 9) / (ms[(s, "mask")] * 1e-3) / 1e9, 1),
+        })
+    out = {
+        "ms_per_step": elapsed / steps * 1e3,
+        "value": ring_ops / (elapsed / steps) / 1e12,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
+                     "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": None,
+                     "kernel": "ring_gemm_kernel<0> (server product [Y'|Q] = A' Bext^T)",
+                     "launch_ms": [round(x, 4) for x in server_ms]},
+        "per_shape": per_shape,
+        "rank": r,
+    }
+    if extras:
+        out["extras"] = run_extras(dev)
+    return out
+
+
+def run_extras(dev):
+    """Stand-alone passes at their own shapes: the rotation of a 4096 x 8192
+    fp32 activation (forward), and the mask pass at the largest prefill shape.
+    Buffers rotate through more than the 256 MB last-level cache."""
+    import torch
+
+    from paper_2607_29221_amd import mosaic as m
+    from paper_2607_29221_amd.mosaic import Digits
+
+    res = {}
+    rows, n = 4096, 8192
+    nbuf = 3
+    xs = [torch.randn(rows, n, device=dev) for _ in range(nbuf)]
+    ys = [torch.empty_like(xs[0]) for _ in range(nbuf)]
+    signs = torch.empty(n, dtype=torch.int8, device=dev)
+    m.mosaic_sample_signs(m.rng(3, 0x70, 0, 0), n, signs)
+    for i in range(3):
+        m.mosaic_hadamard_rotate(xs[i % nbuf], ys[i % nbuf], signs=signs)
+    reps = 30
+    e0, e1 = _events(2)
+    e0.record()
+    for i in range(reps):
+        m.mosaic_hadamard_rotate(xs[i % nbuf], ys[i % nbuf], signs=signs)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps
+    res["fwht_4096x8192_us"] = round(t * 1e3, 2)
+    res["fwht_gbs"] = round(rows * n * 8 / (t * 1e-3) / 1e9, 1)
+    res["fwht_hbm_frac"] = round(res["fwht_gbs"] / HBM_PEAK_GBS, 3)
+    del xs, ys
+
+    M, K = 2048, 28672
+    A = [torch.randint(-127, 128, (M, K), dtype=torch.int8, device=dev) for _ in range(nbuf)]
+    U = [torch.randint(-2 ** 31, 2 ** 31 - 1, (M, K), dtype=torch.int32, device=dev) for _ in range(nbuf)]
+    D = [Digits.empty(M, K, dev) for _ in range(nbuf)]
+    noise = m.rng(2, 0x50, 0, m.DIST_DGAUSS, sigma=0.5, bound=4)
+    for with_noise in (False, True):
+        for i in range(3):
+            m.mosaic_mask(A[i], U[i], noise if with_noise else None, M, K, out_dig=D[i])
+        e0, e1 = _events(2)
+        e0.record()
+        for i in range(reps):
+            m.mosaic_mask(A[i % nbuf], U[i % nbuf], noise if with_noise else None, M, K, out_dig=D[i % nbuf])
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps
+        key = "mask_in_pass_noise" if with_noise else "mask"
+        res[key + "_us"] = round(t * 1e3, 2)
+        res[key + "_gbs"] = round(M * K * 9 / (t * 1e-3) / 1e9, 1)
+        res[key + "_hbm_frac"] = round(res[key + "_gbs"] / HBM_PEAK_GBS, 3)
+    return res
+
+
+def run_cpu_baseline():
+    """The oracle on a bounded sample of the same workload: 64 tokens x 64
+    output columns of the (K, N) = (8192, 8192) shape, full per-call path
+    (Init X, mask, server product incl. Q, unmask); Init W for those 64
+    weight rows is prepared outside the timed region."""
+    import numpy as np
+
+    from oracle import protocol as op
+    from synthetic_inputs import PARAMS_PAPER_D1, PREFILL_SEED, int8_operands
+
+    K, N, Ms, Ns = 8192, 8192, 64, 64
+    A, W = int8_operands(2048, K, N, PREFILL_SEED)
+    seed = 0x6D6F736169630000 | PREFILL_SEED
+    ws = op.init_w(W[:Ns], PARAMS_PAPER_D1, seed, 0)
+    X = A[:Ms].T
+    t0 = time.perf_counter()
+    cs = op.init_x(ws, Ms, PARAMS_PAPER_D1, seed, 0)
+    Xm = op.mask(X, cs)
+    Ym, Q = op.server(ws, Xm)
+    Y = op.unmask(ws, cs, Ym, Q)
+    dt = time.perf_counter() - t0
+    assert Y.shape == (Ns, Ms)
+    ops = 2.0 * Ms * K * Ns
+    return {"value": ops / dt / 1e12, "unit": "ring-TOPS", "cores": 1, "kind": "oracle",
+            "seconds": round(dt, 2),
+            "sample": f"{Ms} tokens x {Ns} output columns of (K, N) = ({K}, {N}), rank 1536, full per-call "
+                      "path (Init X, mask, server incl. Q, unmask); numpy single-threaded"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the masked product is benchmarked on a single MI355X "
+              f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
+        sys.exit(2)
+
+    gpu = run_gpu(args.steps, args.warmup, not args.no_extras)
+    line = {
+        "metric": "masked Z_2^32 matmul ring-TOPS (% int8 MFMA peak) at 70B-layer shapes",
+        "value": round(gpu["value"], 2),
+        "unit": "ring-TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(gpu["ms_per_step"], 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32 ring (i8 MFMA digits)",
+        "data": "synthetic",
+        "config": {"workload": "prefill masked products, 70B-layer shapes, M=2048, "
+                               "(K,N) in {8192x8192, 8192x28672, 28672x8192}, d=1 r=1536 sigma=0.5",
+                   "M": 2048, "shapes": [[8192, 8192], [8192, 28672], [28672, 8192]], "rank": gpu["rank"]},
+        "roofline": gpu["roofline"],
+        "per_shape": gpu["per_shape"],
+    }
+    if "extras" in gpu:
+        line["extras"] = gpu["extras"]
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = run_cpu_baseline()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -13,14 +13,27 @@
 // Accumulator range: a digit product is at most 2^14 in magnitude, so the
 // four-product class acc_3 stays below 2^31 for K < 2^15 (checked by the ABI).
 //
-// Tiling: 256 threads = 4 waves in a 2 x 2 arrangement; block tile 128 x 128,
-// wave tile 64 x 64 as 2 x 2 MFMA tiles of 32 x 32 (v_mfma_i32_32x32x32_i8);
-// BK = 64 columns per stage, i.e. 256 bytes per row (4 groups x 4 digits x 16
-// bytes). Operand tiles are fetched with buffer loads whose descriptor covers
-// only the block's valid rows, so rows past M or N read as zero. In LDS each
-// row is padded to 272 bytes: 16 lanes reading the same 16-byte chunk of 16
-// consecutive rows then touch all 64 banks once, and every fragment address
-// is a per-thread base plus an immediate offset. Double-buffered: 136 KiB.
+// Work decomposition. A block of 512 threads (8 waves, two per SIMD) owns a
+// 128 x 128 output tile; wave w computes rows 64 (w / 4) .. +64 and columns
+// 32 (w % 4) .. +32 as two 32 x 32 tiles of v_mfma_i32_32x32x32_i8, holding
+// 2 tiles x 4 shift classes x 16 = 128 accumulator registers. Two waves per
+// SIMD let one wave's MFMAs run while the other waits at a barrier or on LDS.
+//
+// Pipeline. The K dimension is consumed in stages of 32 columns (128 bytes
+// per row per operand). Four stages live in LDS at once (4 x 32 KiB) and are
+// filled by direct buffer-to-LDS loads issued three stages ahead. Each wave
+// runs a stage as four groups of {5 MFMAs, 1 direct load for stage s+3,
+// 3 LDS reads of stage s+1's fragments}, pinned in that order by scheduling
+// barriers, so load and LDS issue overlap matrix work. The fragments are
+// double-buffered in registers. One barrier per stage publishes stage s+1
+// and retires stage s-1's slot, which the loads of stage s then refill.
+//
+// LDS rows are 128 bytes (8 chunks of 16 bytes); chunk c of row R sits in
+// slot c ^ ((R >> 1) & 7). Sixteen lanes reading one chunk of 16 consecutive
+// rows then cover all 64 banks once. A direct load writes 64 consecutive
+// 16-byte slots (8 rows), so each lane fetches the chunk that belongs to its
+// slot. Operand tiles are addressed through buffer descriptors that cover only
+// the block's valid rows: rows past M or N read as zero and never fault.
 #include "internal.h"
 
 namespace mosaic {
@@ -29,41 +42,79 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128;
-constexpr int BN = 128;
-constexpr int BKB = 256;             // bytes per row per stage (64 columns x 4 digits)
-constexpr int LROW = BKB + 16;       // padded LDS row pitch in bytes
-constexpr int NTHREADS = 256;
-constexpr int LOADS = BM * (BKB / 16) / NTHREADS;   // 16-byte loads per thread per operand (8)
-constexpr int OPB = BM * LROW;       // bytes of one operand stage in LDS
+constexpr int BM = 128;              // block tile rows (A)
+constexpr int BN = 128;              // block tile rows (B) = output columns
+constexpr int NTHREADS = 512;
+constexpr int BK = 32;               // columns per stage
+constexpr int ROWB = BK * 4;         // bytes per row per stage
+constexpr int OPS = BM * ROWB;       // one operand stage in LDS (16 KiB)
+constexpr int STAGE = 2 * OPS;       // A and B (32 KiB)
+constexpr int NSTAGE = 4;            // stages resident in LDS
 constexpr uint32_t kRsrcWord3 = 0x00020000u;
 
 struct Tile {
   int64_t tm, tn;
 };
 
-// Grouped ordering: GROUP_M consecutive row tiles sweep the column tiles
-// together, so blocks that run at the same time share operand rows in L2.
+// Tile order. Workgroups are dispatched to the 8 XCDs round-robin by id, and
+// each XCD has its own L2. The id is first remapped so that XCD x owns a
+// contiguous chunk of the logical order (ids x, x+8, x+16, ... become
+// consecutive), then the logical order is grouped: GROUP_M row tiles sweep
+// the column tiles together. The blocks an XCD runs at once thus cover a
+// compact patch of the output, whose operand slices are shared in that XCD's
+// L2; XCDs that own the same columns for different row groups sweep them at
+// the same pace, so B is shared in the last-level cache as well. The remap is
+// a bijection of [0, tiles); correctness does not depend on dispatch order.
 __device__ __forceinline__ Tile tile_of(int64_t pid, int64_t tiles_m, int64_t tiles_n) {
-  constexpr int64_t GROUP_M = 8;
+  constexpr int64_t NXCD = 8;
+  constexpr int64_t GROUP_M = 4;
+  const int64_t tiles = tiles_m * tiles_n;
+  const int64_t xcd = pid % NXCD;
+  const int64_t local = pid / NXCD;
+  const int64_t q = tiles / NXCD, r = tiles % NXCD;
+  const int64_t lin = xcd * q + (xcd < r ? xcd : r) + local;
   const int64_t per_group = GROUP_M * tiles_n;
-  const int64_t group = pid / per_group;
+  const int64_t group = lin / per_group;
   const int64_t first_m = group * GROUP_M;
   const int64_t gm = (tiles_m - first_m) < GROUP_M ? (tiles_m - first_m) : GROUP_M;
-  const int64_t in_group = pid - group * per_group;
+  const int64_t in_group = lin - group * per_group;
   Tile t;
   t.tm = first_m + in_group % gm;
   t.tn = in_group / gm;
   return t;
 }
 
-__device__ __forceinline__ uint4 lds_read16(const char* lds, int off) {
-  return *(const uint4*)(lds + off);
+// Direct buffer-to-LDS load of 16 bytes per lane: lane l of the wave writes
+// LDS bytes [lds_off + 16 l, lds_off + 16 l + 16). Issued as inline assembly
+// so that the compiler, which cannot tell these writes from later LDS reads,
+// does not drain every outstanding load before each read; completion is
+// tracked by hand with s_waitcnt vmcnt before the barrier that publishes a
+// stage. M0 (the LDS base) is set inside the same statement; nothing else in
+// this kernel uses M0.
+__device__ __forceinline__ void dma16(v4i rs, uint32_t lds_off, int voff, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds_off), "v"(voff), "s"(rs), "s"(soff) : "memory");
 }
+
+// Raw buffer descriptor over [base, base + bytes): out-of-range lanes read 0.
+__device__ __forceinline__ v4i make_rsrc(const void* base, int64_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  return v4i{(int)(uint32_t)b, (int)((uint32_t)(b >> 32) & 0xFFFFu), (int)bytes, (int)kRsrcWord3};
+}
+
+// s_waitcnt with only the vector-memory counter constrained: at most 4 n
+// direct loads of this wave (n stages) may still be in flight.
+__device__ __forceinline__ void wait_loads(int n) {
+  if (n >= 2) __builtin_amdgcn_s_waitcnt(0x0F78);        // vmcnt(8)
+  else if (n == 1) __builtin_amdgcn_s_waitcnt(0x0F74);   // vmcnt(4)
+  else __builtin_amdgcn_s_waitcnt(0x0F70);               // vmcnt(0)
+}
+
+__device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
 
 template <int EPI>
 __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
-  __shared__ __attribute__((aligned(16))) char lds[2 * 2 * OPB];   // [buffer][A/B][row][272 B]
+  __shared__ __attribute__((aligned(1024))) char lds[NSTAGE * STAGE];
 
   const int64_t tiles_m = (g.M + BM - 1) / BM;
   const int64_t tiles_n = (g.N + BN - 1) / BN;
@@ -72,136 +123,157 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   const int64_t n0 = tile.tn * BN;
   const int64_t rows_a = (g.M - m0) < BM ? (g.M - m0) : BM;
   const int64_t rows_b = (g.N - n0) < BN ? (g.N - n0) : BN;
-
-  const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(g.a + m0 * g.a_pitch), (short)0, (int)(rows_a * g.a_pitch), kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(g.b + n0 * g.b_pitch), (short)0, (int)(rows_b * g.b_pitch), kRsrcWord3);
+  const v4i rsa = make_rsrc(g.a + m0 * g.a_pitch, rows_a * g.a_pitch);
+  const v4i rsb = make_rsrc(g.b + n0 * g.b_pitch, rows_b * g.b_pitch);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1;
-  const int wn = wave & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2;
+  const int wn = wave & 3;
 
-  // global -> LDS: thread copies chunk (tid % 16) of rows tid / 16 + 16 p
-  const int lchunk = tid & 15;
-  const int lrow = tid >> 4;
-  const int voff_a = lrow * (int)g.a_pitch + lchunk * 16;
-  const int voff_b = lrow * (int)g.b_pitch + lchunk * 16;
-  const int step_a = 16 * (int)g.a_pitch;
-  const int step_b = 16 * (int)g.b_pitch;
-  const int lds_st = lrow * LROW + lchunk * 16;
+  // direct loads: wave w fills rows 16 w + 8 q .. +8 (q = 0, 1) of A and of B
+  int voff[4];   // A q0, B q0, A q1, B q1
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int R = wave * 16 + q * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((R >> 1) & 7);
+    voff[2 * q] = R * (int)g.a_pitch + c * 16;
+    voff[2 * q + 1] = R * (int)g.b_pitch + c * 16;
+  }
+  const uint32_t lds_wave =
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds + wave * 16 * ROWB;
 
-  // fragment reads: lane reads row (lane % 32) of a 32-row MFMA tile,
-  // column group (lane / 32) of the 32-column k-slice
-  const int frow = lane & 31;
-  const int fgrp = lane >> 5;
-  const int lds_fa = (wm * 64 + frow) * LROW + fgrp * 64;
-  const int lds_fb = (wn * 64 + frow) * LROW + fgrp * 64;
+  // fragment reads: lane reads row (lane % 32) of a 32-row tile, chunk
+  // 4 (lane / 32) + t for digit t
+  const int rr = lane & 31;
+  const int f = (rr >> 1) & 7;
+  int fo[8];     // A digits 0..3, B digits 0..3
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int p = ((lane >> 5) * 4 + t) ^ f;
+    fo[t] = (wm * 64 + rr) * ROWB + p * 16;
+    fo[4 + t] = OPS + (wn * 32 + rr) * ROWB + p * 16;
+  }
 
-  v16i acc[2][2][4];
+  v16i acc[2][4];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+      for (int v = 0; v < 16; ++v) acc[i][s][v] = 0;
+
+  const int stages = (int)(g.Kp / BK);   // even: Kp is a multiple of 64
+  v4i fa[2][2][4], fb[2][4];             // [register set][tile][digit], [register set][digit]
+
+#define MOSAIC_DMA(S, k)                                                                   \
+  dma16(((k) & 1) ? rsb : rsa,                                                            \
+        lds_wave + ((S) % NSTAGE) * STAGE + ((k) & 1) * OPS + ((k) >> 1) * 8 * ROWB, voff[k], \
+        (S) * ROWB)
+
+#define MOSAIC_READ(S, SET, idx)                                                           \
+  do {                                                                                     \
+    const char* base_ = lds + ((S) % NSTAGE) * STAGE;                                      \
+    if ((idx) < 8) {                                                                       \
+      const int i_ = (idx) >> 2, t_ = (idx) & 3;                                           \
+      const uint4 v_ = *(const uint4*)(base_ + i_ * 32 * ROWB + fo[t_]);                   \
+      fa[SET][i_][t_] = v4i{(int)v_.x, (int)v_.y, (int)v_.z, (int)v_.w};                   \
+    } else {                                                                               \
+      const int t_ = (idx) - 8;                                                            \
+      const uint4 v_ = *(const uint4*)(base_ + fo[4 + t_]);                                \
+      fb[SET][t_] = v4i{(int)v_.x, (int)v_.y, (int)v_.z, (int)v_.w};                       \
+    }                                                                                      \
+  } while (0)
+
+  // Keeps fragments in VGPRs (the accumulators own the AGPRs) and makes the
+  // wave wait for its outstanding LDS reads of that set.
+#define MOSAIC_PIN(SET)                                                                    \
+  do {                                                                                     \
+    _Pragma("unroll") for (int i = 0; i < 2; ++i)                                          \
+    _Pragma("unroll") for (int t = 0; t < 4; ++t) asm volatile("" : "+v"(fa[SET][i][t]));  \
+    _Pragma("unroll") for (int t = 0; t < 4; ++t) asm volatile("" : "+v"(fb[SET][t]));     \
+  } while (0)
+
+  // MFMA n (0..19) of a stage: tile n / 10, limb pair n % 10
+#define MOSAIC_MFMA(SET, n)                                                                \
+  do {                                                                                     \
+    constexpr int ta_[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};                                \
+    constexpr int tb_[10] = {0, 1, 2, 3, 0, 1, 2, 0, 1, 0};                                \
+    const int i_ = (n) / 10, a_ = ta_[(n) % 10], b_ = tb_[(n) % 10];                       \
+    acc[i_][a_ + b_] =                                                                     \
+        __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[SET][i_][a_], fb[SET][b_], acc[i_][a_ + b_], 0, 0, 0); \
+  } while (0)
+
+#define MOSAIC_STAGE(CUR, NXT, S)                                                          \
+  do {                                                                                     \
+    const bool refill_ = (S) + NSTAGE - 1 < stages;                                        \
+    const bool next_ = (S) + 1 < stages;                                                   \
+    _Pragma("unroll") for (int gq = 0; gq < 4; ++gq) {                                     \
+      _Pragma("unroll") for (int u = 0; u < 5; ++u) MOSAIC_MFMA(CUR, gq * 5 + u);          \
+      if (refill_) MOSAIC_DMA((S) + NSTAGE - 1, gq);                                       \
+      if (next_) {                                                                         \
+        MOSAIC_READ((S) + 1, NXT, 3 * gq);                                                 \
+        MOSAIC_READ((S) + 1, NXT, 3 * gq + 1);                                             \
+        MOSAIC_READ((S) + 1, NXT, 3 * gq + 2);                                             \
+      }                                                                                    \
+      __builtin_amdgcn_sched_barrier(0);                                                   \
+    }                                                                                      \
+  } while (0)
+
+  // prologue: stages 0..2 in flight, stage 0 published and read
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < stages) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][j][s][v] = 0;
-
-  const int stages = (int)(g.Kp / 64);
-  uint4 sa[LOADS], sb[LOADS];
-
+      for (int k = 0; k < 4; ++k) MOSAIC_DMA(s, k);
+    }
   if (stages > 0) {
+    wait_loads(imin(NSTAGE - 2, stages - 1));
+    __builtin_amdgcn_s_barrier();
 #pragma unroll
-    for (int p = 0; p < LOADS; ++p) {
-      const v4i va = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rsa, voff_a + p * step_a, 0, 0));
-      const v4i vb = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rsb, voff_b + p * step_b, 0, 0));
-      sa[p] = make_uint4(va[0], va[1], va[2], va[3]);
-      sb[p] = make_uint4(vb[0], vb[1], vb[2], vb[3]);
-    }
-#pragma unroll
-    for (int p = 0; p < LOADS; ++p) {
-      *(uint4*)(lds + lds_st + p * 16 * LROW) = sa[p];
-      *(uint4*)(lds + OPB + lds_st + p * 16 * LROW) = sb[p];
-    }
+    for (int k = 0; k < 12; ++k) MOSAIC_READ(0, 0, k);
   }
-  __syncthreads();
 
-  for (int s = 0; s < stages; ++s) {
-    const int cur = (s & 1) * 2 * OPB;
-    const bool more = (s + 1) < stages;
-    if (more) {
-      const int kb = (s + 1) * BKB;
-#pragma unroll
-      for (int p = 0; p < LOADS; ++p) {
-        const v4i va = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rsa, voff_a + p * step_a + kb, 0, 0));
-        const v4i vb = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rsb, voff_b + p * step_b + kb, 0, 0));
-        sa[p] = make_uint4(va[0], va[1], va[2], va[3]);
-        sb[p] = make_uint4(vb[0], vb[1], vb[2], vb[3]);
-      }
-    }
-
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {          // two 32-column k-slices per stage
-      v4i af[2][4], bf[2][4];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int off = i * 32 * LROW + h * 128 + t * 16;
-          const uint4 va = lds_read16(lds + cur, lds_fa + off);
-          const uint4 vb = lds_read16(lds + cur + OPB, lds_fb + off);
-          af[i][t] = v4i{(int)va.x, (int)va.y, (int)va.z, (int)va.w};
-          bf[i][t] = v4i{(int)vb.x, (int)vb.y, (int)vb.z, (int)vb.w};
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int ta = 0; ta < 4; ++ta)
-#pragma unroll
-            for (int tb = 0; tb < 4 - ta; ++tb)
-              acc[i][j][ta + tb] =
-                  __builtin_amdgcn_mfma_i32_32x32x32_i8(af[i][ta], bf[j][tb], acc[i][j][ta + tb], 0, 0, 0);
-    }
-
-    if (more) {
-      const int nxt = ((s + 1) & 1) * 2 * OPB;
-#pragma unroll
-      for (int p = 0; p < LOADS; ++p) {
-        *(uint4*)(lds + nxt + lds_st + p * 16 * LROW) = sa[p];
-        *(uint4*)(lds + nxt + OPB + lds_st + p * 16 * LROW) = sb[p];
-      }
-    }
-    __syncthreads();
+  // Before stage S: this wave's loads of stage S+1 have landed (at most one
+  // later stage in flight) and its reads of stage S have completed (the pin);
+  // the barrier then makes stage S+1 visible to every wave and guarantees
+  // nobody still reads stage S-1's slot, which stage S's loads refill.
+  for (int s = 0; s < stages; s += 2) {
+    wait_loads(imin(NSTAGE - 3, stages - 2 - s));
+    MOSAIC_PIN(0);
+    __builtin_amdgcn_s_barrier();
+    MOSAIC_STAGE(0, 1, s);
+    if (s + 2 < stages) wait_loads(imin(NSTAGE - 3, stages - 3 - s));
+    MOSAIC_PIN(1);
+    if (s + 2 < stages) __builtin_amdgcn_s_barrier();
+    MOSAIC_STAGE(1, 0, s + 1);
   }
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // no direct load outlives the loop
+#undef MOSAIC_DMA
+#undef MOSAIC_READ
+#undef MOSAIC_PIN
+#undef MOSAIC_MFMA
+#undef MOSAIC_STAGE
 
   // epilogue: recombine the shift classes and write. Output layout of the
   // 32 x 32 MFMA: register v of lane l holds row 8 (v / 4) + 4 (l / 32) + v % 4,
   // column l % 32.
+  const int64_t n = n0 + wn * 32 + (lane & 31);
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int64_t m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        if (m < g.M && n < g.N) {
-          const uint32_t val = (uint32_t)acc[i][j][0][v] + ((uint32_t)acc[i][j][1][v] << 8) +
-                               ((uint32_t)acc[i][j][2][v] << 16) + ((uint32_t)acc[i][j][3][v] << 24);
-          if (EPI == EPI_STORE) {
-            g.c[m * g.ldc + n] = val;
-          } else {
-            uint32_t y = g.ym[m * g.ldy + n] - val;
-            if (g.kc != nullptr) y -= g.kc[m * g.ldk + n];
-            if (g.y != nullptr) g.y[m * g.ldo + n] = (int32_t)y;
-            if (g.y_f32 != nullptr) g.y_f32[m * g.ldf + n] = (float)(int32_t)y * g.s_rows[m] * g.s_cols[n];
-          }
+    for (int v = 0; v < 16; ++v) {
+      const int64_t m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+      if (m < g.M && n < g.N) {
+        const uint32_t val = (uint32_t)acc[i][0][v] + ((uint32_t)acc[i][1][v] << 8) +
+                             ((uint32_t)acc[i][2][v] << 16) + ((uint32_t)acc[i][3][v] << 24);
+        if (EPI == EPI_STORE) {
+          g.c[m * g.ldc + n] = val;
+        } else {
+          uint32_t y = g.ym[m * g.ldy + n] - val;
+          if (g.kc != nullptr) y -= g.kc[m * g.ldk + n];
+          if (g.y != nullptr) g.y[m * g.ldo + n] = (int32_t)y;
+          if (g.y_f32 != nullptr) g.y_f32[m * g.ldf + n] = (float)(int32_t)y * g.s_rows[m] * g.s_cols[n];
         }
       }
     }
