@@ -33,6 +33,22 @@ INT8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA, TOP/s
 HBM_PEAK_GBS = 8000.0
 
 
+def _profiled_traffic():
+    """HBM bytes per server launch from the committed byte-counter profile,
+    or None if the kernel source changed since the counters were taken."""
+    import hashlib
+    rec = os.path.join(ROOT, "profiles", "server_gemm_traffic.txt")
+    src = os.path.join(ROOT, "paper_2607_29221_amd", "csrc", "ring_gemm.hip")
+    try:
+        kv = dict(line.split(": ", 1) for line in open(rec).read().splitlines() if ": " in line)
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if kv.get("ring_gemm_source_sha256") != sha:
+        return None
+    return float(kv["server_traffic_bytes_per_launch"])
+
+
 def _events(n):
     import torch
     return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
@@ -105,7 +121,7 @@ def run_gpu(steps: int, warmup: int, extras: bool):
         "ms_per_step": elapsed / steps * 1e3,
         "value": ring_ops / (elapsed / steps) / 1e12,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
-                     "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": None,
+                     "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": _profiled_traffic(),
                      "kernel": "ring_gemm_kernel<0> (server product [Y'|Q] = A' Bext^T)",
                      "launch_ms": [round(x, 4) for x in server_ms]},
         "per_shape": per_shape,
@@ -205,11 +221,24 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy 1 GiB device-to-device three times (scale for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the masked product is benchmarked on a single MI355X "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        import torch
+        src = torch.empty(1 << 28, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_dispatch": 1 << 30, "dispatches": 3}))
+        return
 
     gpu = run_gpu(args.steps, args.warmup, not args.no_extras)
     line = {
