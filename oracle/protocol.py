@@ -184,3 +184,40 @@ def run(A_plain: np.ndarray, W_plain: np.ndarray, params, seed: int, weight_id: 
     Ym, Q = server(ws, Xm)
     Y = unmask(ws, cs, Ym, Q)
     return RunResult(ws=ws, cs=cs, X_masked=Xm, Y_masked=Ym, Q=Q, Y=Y)
+
+
+def sampled_depth1(A_rows: np.ndarray, W_rows: np.ndarray, I, J, K: int, params, seed: int,
+                   weight_id: int, call_id: int) -> dict:
+    """Sampled outputs of the depth-1 protocol (Section 4.1) for token rows I
+    (A_rows = A[I], build orientation) and weight rows J (W_rows = W[J]),
+    computed from the definitions without forming the full matrices:
+
+        W'[J] = W[J] + E_w[J] + L[J] M          (weight mask)
+        X'^T[I] = A[I] + R^T[I] N^T + E_x^T[I]  (activation mask)
+        Y'^T[I, J] = X'^T[I] W'[J]^T,  Q^T[I] = X'^T[I] M^T
+        J_w[J] = (W[J] + E_w[J]) N,   K^T[I, J] = R^T[I] J_w[J]^T
+        Y^T[I, J] = Y'^T[I, J] - K^T[I, J] - Q^T[I] L[J]^T
+
+    M (r x K) and N (K x r) are drawn in full; every other matrix only at
+    the sampled rows."""
+    r = params.ranks[0]
+    nz = params.noise
+    kind = "zero" if nz.kind == "zero" else "dgauss"
+    M_ = smp.sample_matrix("uniform", r, K, seed, smp.STREAM_M + 1, weight_id)
+    N_ = smp.sample_matrix("uniform", K, r, seed, smp.STREAM_N + 1, weight_id)
+    L_J = smp.sample_rows("uniform", J, r, seed, smp.STREAM_L, weight_id)
+    Ew_J = smp.sample_rows(kind, J, K, seed, smp.STREAM_EW, weight_id, sigma=nz.sigma, bound=nz.bound)
+    Rt_I = smp.sample_rows("uniform", I, r, seed, smp.STREAM_R, call_id)
+    Ex_I = smp.sample_rows(kind, I, K, seed, smp.STREAM_EX, call_id, sigma=nz.sigma, bound=nz.bound)
+    WE = ring_add(to_ring(W_rows), Ew_J)
+    Wm = ring_add(WE, ring_matmul(L_J, M_))
+    Ua_noE = ring_matmul(Rt_I, N_.T)
+    Am = ring_add(to_ring(A_rows), Ua_noE, Ex_I)
+    Ym = ring_matmul(Am, Wm.T)
+    Q = ring_matmul(Am, M_.T)
+    Jw = ring_matmul(WE, N_)
+    Kc = ring_matmul(Rt_I, Jw.T)
+    Y = ring_sub(ring_sub(Ym, Kc), ring_matmul(Q, L_J.T))
+    ident = ring_matmul(ring_add(to_ring(A_rows), Ex_I), WE.T)
+    return dict(W_masked=Wm, U_a=Ua_noE, A_masked=Am, Y_masked=Ym, Q=Q, K_c=Kc, Y=Y, identity=ident,
+                E_w=Ew_J, E_x=Ex_I)

@@ -30,6 +30,7 @@ from typing import List
 
 import numpy as np
 
+from . import _cstream
 from .philox import philox4x32_np
 
 # Stream identifiers (counter word 2) of every random matrix of the protocol.
@@ -47,7 +48,18 @@ STREAM_SIGNS = 0x70       # d, Hadamard rotation signs
 
 
 def stream_words(seed: int, stream: int, instance: int, t0: int, count: int) -> np.ndarray:
-    """Words t0 .. t0+count-1 of the stream, as uint32."""
+    """Words t0 .. t0+count-1 of the stream, as uint32 (the C generator of
+    oracle/c for long ranges, the numpy one otherwise; the tests check that
+    both agree with the scalar definition)."""
+    if count <= 0:
+        return np.zeros(0, dtype=np.uint32)
+    if count >= 4096:
+        return _cstream.stream_words(seed, stream, instance, t0, count)
+    return stream_words_np(seed, stream, instance, t0, count)
+
+
+def stream_words_np(seed: int, stream: int, instance: int, t0: int, count: int) -> np.ndarray:
+    """stream_words with the vectorised numpy Philox."""
     if count <= 0:
         return np.zeros(0, dtype=np.uint32)
     t = np.arange(t0, t0 + count, dtype=np.uint64)
@@ -88,29 +100,43 @@ def dgauss_thresholds(sigma: float, bound: int) -> List[int]:
     return out
 
 
-def sample_matrix(kind: str, rows: int, cols: int, seed: int, stream: int, instance: int,
-                  sigma: float = 0.5, bound: int = 4, log2_inv_density: int = 6) -> np.ndarray:
-    """A logical rows x cols matrix over Z_{2^32} (uint32, two's complement)."""
-    n = rows * cols
+def _elements(kind: str, e0: int, count: int, seed: int, stream: int, instance: int,
+              sigma: float, bound: int, log2_inv_density: int) -> np.ndarray:
+    """Elements e0 .. e0+count-1 of a stream matrix (uint32)."""
     if kind == "zero":
-        return np.zeros((rows, cols), dtype=np.uint32)
+        return np.zeros(count, dtype=np.uint32)
     if kind == "uniform":
-        return stream_words(seed, stream, instance, 0, n).reshape(rows, cols)
+        return stream_words(seed, stream, instance, e0, count)
     if kind == "dgauss":
-        u = stream_words(seed, stream, instance, 0, n).astype(np.uint64)
+        u = stream_words(seed, stream, instance, e0, count).astype(np.uint64)
         th = dgauss_thresholds(sigma, bound)
-        v = np.full(n, -bound, dtype=np.int64)
+        v = np.full(count, -bound, dtype=np.int64)
         for t in th:
             v += (u >= np.uint64(t)).astype(np.int64)
-        return v.astype(np.int32).view(np.uint32).reshape(rows, cols)
+        return v.astype(np.int32).view(np.uint32)
     if kind == "sparse":
-        w = stream_words(seed, stream, instance, 0, 2 * n)
+        w = stream_words(seed, stream, instance, 2 * e0, 2 * count)
         gate = w[0::2]
         val = w[1::2]
         s = int(log2_inv_density)
-        keep = (gate >> np.uint32(32 - s)) == 0 if s > 0 else np.ones(n, dtype=bool)
-        return np.where(keep, val, np.uint32(0)).astype(np.uint32).reshape(rows, cols)
+        keep = (gate >> np.uint32(32 - s)) == 0 if s > 0 else np.ones(count, dtype=bool)
+        return np.where(keep, val, np.uint32(0)).astype(np.uint32)
     raise ValueError(f"unknown distribution {kind!r}")
+
+
+def sample_matrix(kind: str, rows: int, cols: int, seed: int, stream: int, instance: int,
+                  sigma: float = 0.5, bound: int = 4, log2_inv_density: int = 6) -> np.ndarray:
+    """A logical rows x cols matrix over Z_{2^32} (uint32, two's complement)."""
+    return _elements(kind, 0, rows * cols, seed, stream, instance, sigma, bound,
+                     log2_inv_density).reshape(rows, cols)
+
+
+def sample_rows(kind: str, row_ids, cols: int, seed: int, stream: int, instance: int,
+                sigma: float = 0.5, bound: int = 4, log2_inv_density: int = 6) -> np.ndarray:
+    """Rows ``row_ids`` of the logical matrix with ``cols`` columns (any row
+    count): row i holds elements i * cols .. i * cols + cols - 1."""
+    return np.stack([_elements(kind, int(i) * cols, cols, seed, stream, instance, sigma, bound,
+                               log2_inv_density) for i in row_ids])
 
 
 def sample_signs(n: int, seed: int, instance: int = 0, stream: int = STREAM_SIGNS) -> np.ndarray:

@@ -126,3 +126,23 @@ def test_chain_shapes():
     assert [q.shape for q in res.Q] == [(24, 3), (16, 3), (8, 3)]
     assert res.ws.L.shape == (12, 8)
     assert res.ws.S[1].shape == (12, 24) and res.ws.S[2].shape == (12, 16)
+
+
+@pytest.mark.parametrize("noise", [SMALL, ZERO])
+def test_sampled_depth1_matches_full_run(noise):
+    """The sampled routine (used at full sizes) restates the depth-1 protocol
+    row by row; it must agree with the full oracle on every sampled output."""
+    rng = np.random.default_rng(8)
+    A = rng.integers(-127, 128, (20, 96), dtype=np.int8)
+    W = rng.integers(-127, 128, (30, 96), dtype=np.int8)
+    p = ProtocolParams(ranks=(64,), noise=noise)
+    full = proto.run(A, W, p, 77, 2, 5)
+    I, J = [0, 7, 19], [1, 29, 11]
+    s = proto.sampled_depth1(A[I], W[J], I, J, 96, p, 77, 2, 5)
+    assert np.array_equal(s["Y"], full.Y.T[np.ix_(I, J)])
+    assert np.array_equal(s["Y_masked"], full.Y_masked.T[np.ix_(I, J)])
+    assert np.array_equal(s["Q"], full.Q[0].T[I])
+    assert np.array_equal(s["W_masked"], full.ws.W_masked[J])
+    assert np.array_equal(s["A_masked"], full.X_masked.T[I])
+    assert np.array_equal(s["K_c"], full.cs.K.T[np.ix_(I, J)])
+    assert np.array_equal(s["Y"], s["identity"])
