@@ -129,6 +129,61 @@ __global__ __launch_bounds__(256) void mask_kernel(MaskLaunch a, int64_t groups)
   }
 }
 
+// Fast path of the mask pass for rows of a multiple of 4 columns with
+// contiguous plaintext: four consecutive lanes share one 16-column digit
+// group, lane q owning columns 4q .. 4q+3. A lane reads 4 plaintext values,
+// one 16-byte word of u and one Philox block of noise, and forms the four
+// digit words of its columns; a transpose across the four lanes (quad
+// shuffles) then hands lane q digit plane q of the whole group, so each lane
+// stores 16 contiguous bytes and a wave stores 1 KiB contiguous per
+// instruction. XT: 0 none, 1 int8, 2 int32 or ring words.
+template <int XT>
+__global__ __launch_bounds__(256) void mask_quad_kernel(MaskLaunch a, int64_t lanes_per_row) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = gid / lanes_per_row;
+  const int64_t l = gid - i * lanes_per_row;       // lane within the row: columns 4 l .. 4 l + 3
+  if (i >= a.rows) return;                          // whole quads leave together (lanes_per_row % 4 == 0)
+  const int64_t j0 = 4 * l;
+  const bool valid = j0 < a.cols;                   // cols % 4 == 0: all four columns valid or all padding
+  uint32_t v[4] = {0u, 0u, 0u, 0u};
+  if (valid) {
+    if (XT == 1) {
+      const uint32_t w = *(const uint32_t*)((const int8_t*)a.x + i * a.x_rs + j0);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) v[b] = (uint32_t)(int32_t)(int8_t)(w >> (8 * b));
+    } else if (XT == 2) {
+      const uint4 w = *(const uint4*)((const uint32_t*)a.x + i * a.x_rs + j0);
+      v[0] = w.x; v[1] = w.y; v[2] = w.z; v[3] = w.w;
+    }
+    if (a.u != nullptr) {
+      const uint4 w = *(const uint4*)(a.u + i * a.ldu + j0);
+      v[0] += w.x; v[1] += w.y; v[2] += w.z; v[3] += w.w;
+    }
+    if (a.has_noise) {
+      uint32_t e[4];
+      sample4_aligned(a.noise, (uint64_t)i * (uint64_t)a.cols + (uint64_t)j0, e);
+      v[0] += e[0]; v[1] += e[1]; v[2] += e[2]; v[3] += e[3];
+    }
+    if (a.out != nullptr) *(uint4*)(a.out + i * a.ldo + j0) = make_uint4(v[0], v[1], v[2], v[3]);
+  }
+  if (a.dig != nullptr) {
+    const uint32_t w[4] = {digit_word(v[0]), digit_word(v[1]), digit_word(v[2]), digit_word(v[3])};
+    uint32_t p[4];                                  // p[t]: digit t of this lane's 4 columns
+    digit_transpose4(w, p);
+    const int q = (int)(l & 3);
+    // lane q collects word q of every lane of its quad
+    uint32_t o[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int src_t = q ^ r;                      // what this lane sends to lane q ^ r
+      const uint32_t send = src_t == 0 ? p[0] : src_t == 1 ? p[1] : src_t == 2 ? p[2] : p[3];
+      const uint32_t got = (r == 0) ? send : (uint32_t)__shfl_xor((int)send, r, 4);
+      o[q ^ r] = got;                               // from lane q ^ r: its digit plane q
+    }
+    *(uint4*)(a.dig + i * a.pitch + 16 * l) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 __global__ __launch_bounds__(256) void signs_kernel(RngArgs r, int64_t n, int8_t* out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t e0 = 4 * i;
@@ -155,6 +210,23 @@ __global__ __launch_bounds__(256) void unmask_elementwise_kernel(GemmLaunch g) {
 }  // namespace
 
 hipError_t launch_mask(const MaskLaunch& a, hipStream_t s) {
+  // fast path: see mask_quad_kernel
+  const bool x_ok = a.x == nullptr ||
+                    (a.x_cs == 1 && a.x_dtype == 0 && a.x_rs % 4 == 0 && ((uintptr_t)a.x & 3) == 0) ||
+                    (a.x_cs == 1 && a.x_dtype >= 2 && a.x_rs % 4 == 0 && ((uintptr_t)a.x & 15) == 0);
+  const bool u_ok = a.u == nullptr || (a.ldu % 4 == 0 && ((uintptr_t)a.u & 15) == 0);
+  const bool o_ok = a.out == nullptr || (a.ldo % 4 == 0 && ((uintptr_t)a.out & 15) == 0);
+  const bool n_ok = !a.has_noise || !a.noise.transposed;
+  if (a.cols % 4 == 0 && x_ok && u_ok && o_ok && n_ok) {
+    const int64_t lanes_per_row = (a.dig != nullptr) ? 64 * ((a.cols + 63) / 64) / 4 : 4 * ((a.cols + 15) / 16);
+    const int64_t threads = a.rows * lanes_per_row;
+    if (threads == 0) return hipSuccess;
+    const dim3 grid((unsigned)((threads + 255) / 256));
+    if (a.x == nullptr) hipLaunchKernelGGL(mask_quad_kernel<0>, grid, dim3(256), 0, s, a, lanes_per_row);
+    else if (a.x_dtype == 0) hipLaunchKernelGGL(mask_quad_kernel<1>, grid, dim3(256), 0, s, a, lanes_per_row);
+    else hipLaunchKernelGGL(mask_quad_kernel<2>, grid, dim3(256), 0, s, a, lanes_per_row);
+    return hipGetLastError();
+  }
   const int64_t groups = (a.dig != nullptr) ? (64 * ((a.cols + 63) / 64)) / 16 : (a.cols + 15) / 16;
   const int64_t threads = a.rows * groups;
   if (threads == 0) return hipSuccess;

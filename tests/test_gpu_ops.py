@@ -62,13 +62,14 @@ def test_signs():
 
 
 @pytest.mark.parametrize("dtype", [torch.int8, torch.int16, torch.int32])
-@pytest.mark.parametrize("rows,cols", [(7, 100), (64, 512), (2, 16)])
-def test_mask(dtype, rows, cols):
+@pytest.mark.parametrize("rows,cols", [(7, 100), (64, 512), (2, 16), (3, 70)])
+@pytest.mark.parametrize("u_pad", [3, 4])
+def test_mask(dtype, rows, cols, u_pad):
     rng = _rng_np(rows * cols)
     info = {torch.int8: (-128, 128), torch.int16: (-32768, 32768), torch.int32: (-2 ** 31, 2 ** 31)}[dtype]
     x = rng.integers(info[0], info[1], (rows, cols)).astype({torch.int8: np.int8, torch.int16: np.int16,
                                                              torch.int32: np.int32}[dtype])
-    u = rng.integers(0, 2 ** 32, (rows, cols + 3), dtype=np.uint64).astype(np.uint32)
+    u = rng.integers(0, 2 ** 32, (rows, cols + u_pad), dtype=np.uint64).astype(np.uint32)
     noise = m.rng(SEED, 0x50, 9, m.DIST_DGAUSS, sigma=0.5, bound=4)
     out = torch.empty((rows, cols), dtype=torch.int32, device="cuda")
     dig = Digits.empty(rows, cols)
