@@ -52,6 +52,26 @@ struct GemmLaunch {
 };
 hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s);
 
+// Products with at most SKINNY_MAX_M rows of A (decode shapes) run on a
+// kernel that streams B once and splits K inside each workgroup.
+constexpr int64_t SKINNY_MAX_M = 64;
+hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStream_t s);
+
+// Writes one recombined ring value of C = A B^T at (m, n) through the
+// epilogue: EPI_STORE stores it; EPI_UNMASK forms y = ym - val - kc and
+// stores it as int32 and/or dequantised fp32.
+template <int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmLaunch& g, int64_t m, int64_t n, uint32_t val) {
+  if (EPI == EPI_STORE) {
+    g.c[m * g.ldc + n] = val;
+  } else {
+    uint32_t y = g.ym[m * g.ldy + n] - val;
+    if (g.kc != nullptr) y -= g.kc[m * g.ldk + n];
+    if (g.y != nullptr) g.y[m * g.ldo + n] = (int32_t)y;
+    if (g.y_f32 != nullptr) g.y_f32[m * g.ldf + n] = (float)(int32_t)y * g.s_rows[m] * g.s_cols[n];
+  }
+}
+
 // Unmask without a product term (R = 0): out = ym - kc.
 hipError_t launch_unmask_elementwise(const GemmLaunch& g, hipStream_t s);
 

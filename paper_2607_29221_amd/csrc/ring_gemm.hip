@@ -270,14 +270,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
       if (m < g.M && n < g.N) {
         const uint32_t val = (uint32_t)acc[i][0][v] + ((uint32_t)acc[i][1][v] << 8) +
                              ((uint32_t)acc[i][2][v] << 16) + ((uint32_t)acc[i][3][v] << 24);
-        if (EPI == EPI_STORE) {
-          g.c[m * g.ldc + n] = val;
-        } else {
-          uint32_t y = g.ym[m * g.ldy + n] - val;
-          if (g.kc != nullptr) y -= g.kc[m * g.ldk + n];
-          if (g.y != nullptr) g.y[m * g.ldo + n] = (int32_t)y;
-          if (g.y_f32 != nullptr) g.y_f32[m * g.ldf + n] = (float)(int32_t)y * g.s_rows[m] * g.s_cols[n];
-        }
+        gemm_epilogue<EPI>(g, m, n, val);
       }
     }
   }
@@ -286,6 +279,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
 }  // namespace
 
 hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
+  if (g.M <= SKINNY_MAX_M) return launch_ring_gemm_skinny(g, epi, s);
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles == 0) return hipSuccess;
   if (epi == EPI_STORE)

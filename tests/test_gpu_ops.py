@@ -125,6 +125,27 @@ def test_masked_matmul(M, N, K):
     assert np.array_equal(got, ring_matmul(a, b.T))
 
 
+@pytest.mark.parametrize("M", [1, 8, 15, 16, 17, 33, 48, 63, 64, 65])
+@pytest.mark.parametrize("N,K", [(33, 64), (100, 576), (16, 1000), (47, 4160)])
+def test_masked_matmul_short_a(M, N, K):
+    """Decode-shaped products (at most 64 rows of A take the K-split kernel):
+    row counts on and around the 16-row tiles, ragged N, and K ranges that
+    leave some of the eight K slices short or empty."""
+    rng = _rng_np(M * 131 + N * 7 + K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
+
+
+@pytest.mark.parametrize("M", [5, 64])
+def test_masked_matmul_accumulator_extreme_short_a(M):
+    N, K = 40, 32767
+    a = np.full((M, K), 0x7F7F7F80, dtype=np.uint32)
+    b = np.full((N, K), 0x7F7F7F80, dtype=np.uint32)
+    got = _gemm(a, b)
+    assert np.all(got == (K * (0x7F7F7F80 ** 2)) % (1 << 32))
+
+
 def test_masked_matmul_accumulator_extreme():
     """All digits -128 (x = 0x7F7F7F80) at the largest supported K: every
     limb product is +2^14, the four-product class reaches 4 K 2^14 < 2^31."""
@@ -155,7 +176,7 @@ def test_masked_matmul_ldc_and_offsets():
     assert np.all(got[:, :5] == 0) and np.all(got[:, 5 + N:] == 0)
 
 
-@pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192)])
+@pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192), (1, 300, 2560), (8, 33, 64)])
 @pytest.mark.parametrize("with_k", [True, False])
 def test_unmask(M, N, R, with_k):
     rng = _rng_np(M + N + R)
@@ -179,9 +200,10 @@ def test_unmask(M, N, R, with_k):
     assert np.array_equal(y.cpu().numpy(), ref.view(np.int32))
 
 
-def test_unmask_dequantised():
-    rng = _rng_np(5)
-    M, N, R = 40, 90, 64
+@pytest.mark.parametrize("M", [40, 150])
+def test_unmask_dequantised(M):
+    rng = _rng_np(5 + M)
+    N, R = 90, 64
     ym = _random_ring(rng, (M, N))
     q = _random_ring(rng, (M, R))
     l = _random_ring(rng, (N, R))
