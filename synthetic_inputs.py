@@ -106,3 +106,58 @@ PREFILL_SEED = 2
 # Random-Hadamard rotation: 4096 x 8192 fp32, signs seed 3.
 HADAMARD_SHAPE = (4096, 8192)
 HADAMARD_SEED = 3
+
+# Synthetic 70B-style decoder stack (end-to-end workload): hidden 8192,
+# 64 query heads and 8 key/value heads of dimension 128, SwiGLU FFN 28672,
+# 4 layers; weights N(0, 0.02^2); input hidden states N(0, 1) for batch 4 x
+# sequence 1024 (seed 4).
+DECODER = dict(hidden=8192, heads=64, kv_heads=8, head_dim=128, ffn=28672, layers=4, batch=4, seq=1024)
+DECODER_SEED = 4
+DECODER_WEIGHT_STD = 0.02
+# linear layers of one block, in evaluation order; q|k|v and gate|up are
+# single fused products (one masked activation per layer input)
+DECODER_LINEARS = ("qkv", "o", "gate_up", "down")
+
+
+def decoder_linear_shape(name: str, cfg: dict = DECODER) -> Tuple[int, int]:
+    """(N, K) = (out features, in features) of one linear layer."""
+    h, hd = cfg["hidden"], cfg["head_dim"]
+    return {
+        "qkv": ((cfg["heads"] + 2 * cfg["kv_heads"]) * hd, h),
+        "o": (h, cfg["heads"] * hd),
+        "gate_up": (2 * cfg["ffn"], h),
+        "down": (h, cfg["ffn"]),
+    }[name]
+
+
+def decoder_weight(layer: int, name: str, device, cfg: dict = DECODER, seed: int = DECODER_SEED):
+    """fp32 weight (N x K) ~ N(0, DECODER_WEIGHT_STD^2), from torch's
+    generator on ``device`` seeded per (seed, layer, linear)."""
+    import torch
+    N, K = decoder_linear_shape(name, cfg)
+    g = torch.Generator(device=device)
+    g.manual_seed(seed * 1_000_003 + layer * 16 + DECODER_LINEARS.index(name))
+    w = torch.randn((N, K), generator=g, device=device, dtype=torch.float32)
+    return w.mul_(DECODER_WEIGHT_STD)
+
+
+def decoder_input(device, cfg: dict = DECODER, seed: int = DECODER_SEED):
+    """Input hidden states, (batch * seq) x hidden fp32 ~ N(0, 1)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed * 1_000_003 + 999)
+    return torch.randn((cfg["batch"] * cfg["seq"], cfg["hidden"]), generator=g, device=device,
+                       dtype=torch.float32)
+
+
+def int_codes(rows: int, cols: int, qmax: int, seed: int) -> np.ndarray:
+    """Uniform integer codes in [-qmax, qmax] (int32)."""
+    rng = np.random.default_rng(seed)
+    return rng.integers(-qmax, qmax + 1, size=(rows, cols), dtype=np.int32)
+
+
+# Ring products of the decoder stack at their own shapes (M = 4096 tokens):
+# (K, N) of the fused QKV, the fused gate|up and the down projection (the
+# output projection is the (8192, 8192) prefill shape).
+DECODER_RING_KN: List[Tuple[int, int]] = [(8192, 10240), (8192, 57344), (28672, 8192)]
+DECODER_RING_SEED = 5
