@@ -129,6 +129,8 @@ def run_gpu(steps: int, warmup: int, extras: bool):
     }
     if extras:
         out["extras"] = run_extras(dev)
+        out["extras"]["decode"] = run_decode(dev)
+        out["extras"]["decoder_stack"] = run_decoder_stack(dev)
     return out
 
 
@@ -183,6 +185,95 @@ def run_extras(dev):
         res[key + "_gbs"] = round(M * K * 9 / (t * 1e-3) / 1e9, 1)
         res[key + "_hbm_frac"] = round(res[key + "_gbs"] / HBM_PEAK_GBS, 3)
     return res
+
+
+def run_decode(dev):
+    """Decode-shaped calls (M in {1, 8, 64} tokens; (K, N) in {4096^2,
+    4096 x 14336, 14336 x 4096}; depth-2 mask of ranks (1536, 1024) with
+    density-1/64 sparse LPN level). Per shape and M: the server product
+    ([Y' | Q], N + 2560 output columns) and the whole call (Init X, mask,
+    server, unmask), HIP-event means over 20 calls; GB/s counts the server
+    product's operand and output bytes once."""
+    import torch
+
+    from paper_2607_29221_amd import protocol as gp
+    from synthetic_inputs import DECODE_KN, DECODE_M, DECODE_SEED, PARAMS_PAPER_D2_SPARSE, int8_operands
+
+    res = []
+    reps = 20
+    for idx, (K, N) in enumerate(DECODE_KN):
+        A, W = int8_operands(max(DECODE_M), K, N, DECODE_SEED)
+        w = gp.MaskedWeight(torch.from_numpy(W).to(dev), PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + idx, weight_id=idx)
+        for M in DECODE_M:
+            Ad = torch.from_numpy(A[:M].copy()).to(dev)
+            buf = gp.alloc_call(w, M, dev)
+            for i in range(3):
+                gp.run_call(w, Ad, 10_000 + i, buf)
+            torch.cuda.synchronize()
+            e = _events(4)
+            e[0].record()
+            for i in range(reps):
+                gp.server(w, M, buf)
+            e[1].record()
+            for i in range(reps):
+                gp.run_call(w, Ad, 20_000 + i, buf)
+            e[2].record()
+            torch.cuda.synchronize()
+            server_ms = e[0].elapsed_time(e[1]) / reps
+            call_ms = e[1].elapsed_time(e[2]) / reps
+            Kp = 64 * ((K + 63) // 64)
+            byts = 4 * Kp * (M + w.n_out) + 4 * M * w.n_out
+            res.append({"K": K, "N": N, "M": M, "server_us": round(server_ms * 1e3, 2),
+                        "server_gbs": round(byts / (server_ms * 1e-3) / 1e9, 1),
+                        "server_hbm_frac": round(byts / (server_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
+                        "call_us": round(call_ms * 1e3, 2)})
+        del w
+    return res
+
+
+def run_decoder_stack(dev):
+    """Secure forward of the synthetic 70B-style stack (hidden 8192, 64/8
+    heads, FFN 28672, 4 layers, 4096 tokens; int8 weights, depth-1 rank-1536
+    mask, sigma = 0.5) against its float32 plaintext forward: per-layer
+    relative l2 error and cosine similarity, and forward times (Init W of the
+    16 weight matrices is outside the timed region)."""
+    import torch
+
+    from paper_2607_29221_amd import decoder as dec
+    from synthetic_inputs import DECODER, DECODER_LINEARS, DECODER_SEED, PARAMS_PAPER_D1, decoder_input, \
+        decoder_weight
+
+    prev = torch.backends.cuda.matmul.allow_tf32
+    torch.backends.cuda.matmul.allow_tf32 = False
+    try:
+        weights = [{n: decoder_weight(l, n, dev) for n in DECODER_LINEARS} for l in range(DECODER["layers"])]
+        x = decoder_input(dev)
+        sd = dec.SecureDecoder(weights, DECODER, PARAMS_PAPER_D1, 0x6D6F736169630000 | DECODER_SEED)
+        sd.forward(x)                                   # warm-up
+        torch.cuda.synchronize()
+        e = _events(3)
+        e[0].record()
+        got = sd.forward(x)
+        e[1].record()
+        ref = dec.plaintext_forward(x, weights, DECODER)
+        e[2].record()
+        torch.cuda.synchronize()
+        errs = [dec.error_metrics(g, r) for g, r in zip(got, ref)]
+    finally:
+        torch.backends.cuda.matmul.allow_tf32 = prev
+    tokens = DECODER["batch"] * DECODER["seq"]
+    macs = sum(a * b for a, b in (_shape(n) for n in DECODER_LINEARS)) * tokens * DECODER["layers"]
+    secure_ms = e[0].elapsed_time(e[1])
+    return {"layers": DECODER["layers"], "tokens": tokens,
+            "secure_forward_ms": round(secure_ms, 2),
+            "plaintext_fp32_forward_ms": round(e[1].elapsed_time(e[2]), 2),
+            "secure_linear_ring_tops": round(2.0 * macs / (secure_ms * 1e-3) / 1e12, 2),
+            "per_layer": [{"rel_l2": round(v["rel_l2"], 5), "cosine": round(v["cosine"], 6)} for v in errs]}
+
+
+def _shape(name):
+    from synthetic_inputs import decoder_linear_shape
+    return decoder_linear_shape(name)
 
 
 def run_cpu_baseline():
