@@ -81,7 +81,16 @@ mosaic_status rng_args(const mosaic_rng* r, RngArgs* a) {
       if (!(r->sigma >= 0.0) || !std::isfinite(r->sigma))
         return fail(MOSAIC_ERR_INVALID_ARG, "dgauss sigma must be finite and >= 0");
       a->bound = r->bound;
-      dgauss_table(r->sigma, r->bound, a->th);
+      {
+        uint64_t t[2 * kMaxDgaussBound];
+        dgauss_table(r->sigma, r->bound, t);
+        a->dg_base = -r->bound;
+        a->dg_count = 0;
+        for (int k = 0; k < 2 * r->bound; ++k) {
+          if (t[k] == 0) ++a->dg_base;
+          else if (t[k] < (1ull << 32)) a->th[a->dg_count++] = (uint32_t)t[k];
+        }
+      }
       break;
     case MOSAIC_DIST_SPARSE:
       if (r->log2_inv_density < 0 || r->log2_inv_density > 31)

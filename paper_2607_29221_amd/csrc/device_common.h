@@ -18,7 +18,13 @@ struct RngArgs {
   int32_t bound;          // DGAUSS support [-bound, bound]
   int32_t sparse_shift;   // SPARSE: 32 - s (gate kept when gate >> shift == 0); 32 keeps all
   int32_t transposed;
-  uint64_t th[2 * kMaxDgaussBound];  // DGAUSS thresholds (33-bit values)
+  // DGAUSS inverse-CDF table. Of the 2 bound thresholds T_k (ascending, in
+  // [0, 2^32]) those equal to 0 count for every word and those equal to 2^32
+  // for none: they are folded into dg_base = -bound + #{T_k = 0}; the
+  // dg_count others lie strictly inside (0, 2^32) and fit in 32 bits.
+  int32_t dg_base;
+  int32_t dg_count;
+  uint32_t th[2 * kMaxDgaussBound];
 };
 
 // Philox-4x32 with 10 rounds (Salmon et al., SC'11): each round multiplies
@@ -52,9 +58,8 @@ __device__ __forceinline__ uint32_t stream_word(const RngArgs& r, uint64_t t) {
 }
 
 __device__ __forceinline__ uint32_t dgauss_from_word(const RngArgs& r, uint32_t u) {
-  int32_t v = -r.bound;
-  const uint64_t uu = u;
-  for (int k = 0; k < 2 * r.bound; ++k) v += (uu >= r.th[k]) ? 1 : 0;
+  int32_t v = r.dg_base;
+  for (int k = 0; k < r.dg_count; ++k) v += (u >= r.th[k]) ? 1 : 0;
   return (uint32_t)v;
 }
 

@@ -139,10 +139,9 @@ __global__ __launch_bounds__(256) void mask_kernel(MaskLaunch a, int64_t groups)
 // instruction. XT: 0 none, 1 int8, 2 int32 or ring words.
 template <int XT>
 __global__ __launch_bounds__(256) void mask_quad_kernel(MaskLaunch a, int64_t lanes_per_row) {
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t i = gid / lanes_per_row;
-  const int64_t l = gid - i * lanes_per_row;       // lane within the row: columns 4 l .. 4 l + 3
-  if (i >= a.rows) return;                          // whole quads leave together (lanes_per_row % 4 == 0)
+  const int64_t i = blockIdx.x;                     // row
+  const int64_t l = (int64_t)blockIdx.y * blockDim.x + threadIdx.x;   // lane: columns 4 l .. 4 l + 3
+  if (l >= lanes_per_row) return;                   // whole quads leave together (lanes_per_row % 4 == 0)
   const int64_t j0 = 4 * l;
   const bool valid = j0 < a.cols;                   // cols % 4 == 0: all four columns valid or all padding
   uint32_t v[4] = {0u, 0u, 0u, 0u};
@@ -217,11 +216,11 @@ hipError_t launch_mask(const MaskLaunch& a, hipStream_t s) {
   const bool u_ok = a.u == nullptr || (a.ldu % 4 == 0 && ((uintptr_t)a.u & 15) == 0);
   const bool o_ok = a.out == nullptr || (a.ldo % 4 == 0 && ((uintptr_t)a.out & 15) == 0);
   const bool n_ok = !a.has_noise || !a.noise.transposed;
-  if (a.cols % 4 == 0 && x_ok && u_ok && o_ok && n_ok) {
-    const int64_t lanes_per_row = (a.dig != nullptr) ? 64 * ((a.cols + 63) / 64) / 4 : 4 * ((a.cols + 15) / 16);
-    const int64_t threads = a.rows * lanes_per_row;
-    if (threads == 0) return hipSuccess;
-    const dim3 grid((unsigned)((threads + 255) / 256));
+  const int64_t lanes_per_row = (a.dig != nullptr) ? 64 * ((a.cols + 63) / 64) / 4 : 4 * ((a.cols + 15) / 16);
+  const int64_t blocks_per_row = (lanes_per_row + 255) / 256;
+  if (a.cols % 4 == 0 && x_ok && u_ok && o_ok && n_ok && blocks_per_row <= 65535 && a.rows <= 0x7FFFFFFF) {
+    if (a.rows == 0 || lanes_per_row == 0) return hipSuccess;
+    const dim3 grid((unsigned)a.rows, (unsigned)blocks_per_row);   // x: row, y: 1024-column slice
     if (a.x == nullptr) hipLaunchKernelGGL(mask_quad_kernel<0>, grid, dim3(256), 0, s, a, lanes_per_row);
     else if (a.x_dtype == 0) hipLaunchKernelGGL(mask_quad_kernel<1>, grid, dim3(256), 0, s, a, lanes_per_row);
     else hipLaunchKernelGGL(mask_quad_kernel<2>, grid, dim3(256), 0, s, a, lanes_per_row);
