@@ -67,11 +67,18 @@ def run_gpu(steps: int, warmup: int, extras: bool):
     M = PREFILL_M
     seed = 0x6D6F736169630000 | PREFILL_SEED
     shapes = []
+    init_w_ms = []
     for idx, (K, N) in enumerate(PREFILL_KN):
         A, W = int8_operands(M, K, N, PREFILL_SEED)
         Ad = torch.from_numpy(A).to(dev)
         Wd = torch.from_numpy(W).to(dev)
+        torch.cuda.synchronize()
+        e0, e1 = _events(2)
+        e0.record()
         w = gp.MaskedWeight(Wd, params, seed, weight_id=idx)
+        e1.record()
+        torch.cuda.synchronize()
+        init_w_ms.append(round(e0.elapsed_time(e1), 3))
         del Wd
         shapes.append((K, N, Ad, w, gp.alloc_call(w, M, dev)))
     torch.cuda.synchronize()
@@ -116,6 +123,7 @@ def run_gpu(steps: int, warmup: int, extras: bool):
             "server_ring_tops": round(2.0 * M * K * (N + w.R) / (ms[(s, "server")] * 1e-3) / 1e12, 2),
             "server_int8_tops": round(server_ops[s] / (ms[(s, "server")] * 1e-3) / 1e12, 1),
             "mask_gbs": round((M * K * 9) / (ms[(s, "mask")] * 1e-3) / 1e9, 1),
+            "init_w_ms_once": init_w_ms[s],
         })
     out = {
         "ms_per_step": elapsed / steps * 1e3,
@@ -136,8 +144,10 @@ def run_gpu(steps: int, warmup: int, extras: bool):
 
 def run_extras(dev):
     """Stand-alone passes at their own shapes: the rotation of a 4096 x 8192
-    fp32 activation (forward), and the mask pass at the largest prefill shape.
-    Buffers rotate through more than the 256 MB last-level cache."""
+    fp32 activation (forward), the mask pass at the largest prefill shape
+    (with and without E_a), the three samplers writing digits at that shape,
+    and the quantisation of a 4096 x 8192 fp32 activation. Buffers rotate
+    through more than the 256 MB last-level cache."""
     import torch
 
     from paper_2607_29221_amd import mosaic as m
@@ -184,6 +194,41 @@ def run_extras(dev):
         res[key + "_us"] = round(t * 1e3, 2)
         res[key + "_gbs"] = round(M * K * 9 / (t * 1e-3) / 1e9, 1)
         res[key + "_hbm_frac"] = round(res[key + "_gbs"] / HBM_PEAK_GBS, 3)
+    del A, U
+
+    # samplers straight to digits (4 B written per element)
+    for name, r in (("uniform", m.rng(2, 0x20, 0, m.DIST_UNIFORM)),
+                    ("dgauss", m.rng(2, 0x50, 0, m.DIST_DGAUSS, sigma=0.5, bound=4)),
+                    ("sparse", m.rng(2, 0x40, 0, m.DIST_SPARSE, log2_inv_density=6))):
+        for i in range(3):
+            m.mosaic_sample(r, M, K, out_dig=D[i])
+        e0, e1 = _events(2)
+        e0.record()
+        for i in range(reps):
+            m.mosaic_sample(r, M, K, out_dig=D[i % nbuf])
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps
+        res[f"sample_{name}_us"] = round(t * 1e3, 2)
+        res[f"sample_{name}_gbs"] = round(M * K * 4 / (t * 1e-3) / 1e9, 1)
+    del D
+
+    # quantisation of rotated activations: 4096 x 8192 fp32 -> int32 codes
+    rows, n = 4096, 8192
+    xs = [torch.randn(rows, n, device=dev) for _ in range(nbuf)]
+    qs = [torch.empty((rows, n), dtype=torch.int32, device=dev) for _ in range(nbuf)]
+    sc = torch.empty(rows, dtype=torch.float32, device=dev)
+    for i in range(3):
+        m.mosaic_quantize_rows(xs[i], 1997, q=qs[i], scale=sc)
+    e0, e1 = _events(2)
+    e0.record()
+    for i in range(reps):
+        m.mosaic_quantize_rows(xs[i % nbuf], 1997, q=qs[i % nbuf], scale=sc)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps
+    res["quantize_4096x8192_us"] = round(t * 1e3, 2)
+    res["quantize_gbs"] = round(rows * n * 8 / (t * 1e-3) / 1e9, 1)
     return res
 
 

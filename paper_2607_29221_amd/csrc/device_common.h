@@ -122,4 +122,22 @@ __device__ __forceinline__ void digit_transpose4(const uint32_t w[4], uint32_t o
   }
 }
 
+// Digit planes of one 16-column group held by four consecutive lanes: lane
+// q of the quad holds ring values v[0..3] of columns 4 q .. 4 q + 3 and
+// receives in o[0..3] the 16 bytes of digit plane q of the whole group
+// (byte 4 r + b = digit q of column 4 r + b), i.e. the 16-byte word it stores
+// at offset 16 q of the group's 64 bytes. Every lane of the quad must call it.
+__device__ __forceinline__ void quad_digit_planes(const uint32_t v[4], int q, uint32_t o[4]) {
+  const uint32_t w[4] = {digit_word(v[0]), digit_word(v[1]), digit_word(v[2]), digit_word(v[3])};
+  uint32_t p[4];                                  // p[t]: digit t of this lane's 4 columns
+  digit_transpose4(w, p);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int src_t = q ^ r;                      // what this lane sends to lane q ^ r
+    const uint32_t send = src_t == 0 ? p[0] : src_t == 1 ? p[1] : src_t == 2 ? p[2] : p[3];
+    const uint32_t got = (r == 0) ? send : (uint32_t)__shfl_xor((int)send, r, 4);
+    o[q ^ r] = got;                               // from lane q ^ r: its digit plane q
+  }
+}
+
 }  // namespace mosaic

@@ -166,19 +166,8 @@ __global__ __launch_bounds__(256) void mask_quad_kernel(MaskLaunch a, int64_t la
     if (a.out != nullptr) *(uint4*)(a.out + i * a.ldo + j0) = make_uint4(v[0], v[1], v[2], v[3]);
   }
   if (a.dig != nullptr) {
-    const uint32_t w[4] = {digit_word(v[0]), digit_word(v[1]), digit_word(v[2]), digit_word(v[3])};
-    uint32_t p[4];                                  // p[t]: digit t of this lane's 4 columns
-    digit_transpose4(w, p);
-    const int q = (int)(l & 3);
-    // lane q collects word q of every lane of its quad
     uint32_t o[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int src_t = q ^ r;                      // what this lane sends to lane q ^ r
-      const uint32_t send = src_t == 0 ? p[0] : src_t == 1 ? p[1] : src_t == 2 ? p[2] : p[3];
-      const uint32_t got = (r == 0) ? send : (uint32_t)__shfl_xor((int)send, r, 4);
-      o[q ^ r] = got;                               // from lane q ^ r: its digit plane q
-    }
+    quad_digit_planes(v, (int)(l & 3), o);
     *(uint4*)(a.dig + i * a.pitch + 16 * l) = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }

@@ -56,13 +56,69 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(const float* __restr
   }
 }
 
+// Fast path for rows of a multiple of 4 elements with 16-byte aligned rows:
+// thread c handles columns 4 c .. 4 c + 3 with one float4 load, so every
+// load and store instruction of a wave covers one contiguous KiB. Pass 1
+// reduces max |x| over the row (wave shuffles, then one LDS word per wave);
+// pass 2 re-reads the row (now in L2), divides by the fp32 scale, rounds half
+// to even and stores int32 codes with int4 stores and/or digit planes: the
+// four lanes of a quad hold one 16-column group, and a quad shuffle hands
+// each lane one 16-byte plane to store. Padding columns up to the next
+// multiple of 64 get zero digits.
+__global__ __launch_bounds__(256) void quantize_rows_vec_kernel(const float* __restrict__ x, int64_t ldx,
+                                                                int64_t n, int32_t qmax, int32_t* q, int64_t ldq,
+                                                                int8_t* q_dig, int64_t q_pitch, float* scale) {
+  __shared__ float red[4];
+  const int64_t row = blockIdx.x;
+  const float4* xr = (const float4*)(x + row * ldx);
+  const int64_t nv = n / 4;
+  float m = 0.0f;
+  for (int64_t c = threadIdx.x; c < nv; c += 256) {
+    const float4 f = xr[c];
+    m = fmaxf(m, fmaxf(fmaxf(fabsf(f.x), fabsf(f.y)), fmaxf(fabsf(f.z), fabsf(f.w))));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
+  if (threadIdx.x == 0 && scale != nullptr) scale[row] = s;
+
+  const int64_t nchunks = q_dig ? 16 * ((n + 63) / 64) : nv;   // a multiple of 4 with digits
+  for (int64_t c = threadIdx.x; c < nchunks; c += 256) {        // quads stay together (256 % 4 == 0)
+    uint32_t v[4] = {0u, 0u, 0u, 0u};
+    if (c < nv) {
+      const float4 f = xr[c];
+      v[0] = (uint32_t)(int32_t)rintf(f.x / s);
+      v[1] = (uint32_t)(int32_t)rintf(f.y / s);
+      v[2] = (uint32_t)(int32_t)rintf(f.z / s);
+      v[3] = (uint32_t)(int32_t)rintf(f.w / s);
+      if (q != nullptr)
+        *(int4*)(q + row * ldq + 4 * c) = make_int4((int)v[0], (int)v[1], (int)v[2], (int)v[3]);
+    }
+    if (q_dig != nullptr) {
+      uint32_t o[4];
+      quad_digit_planes(v, (int)(c & 3), o);
+      *(uint4*)(q_dig + row * q_pitch + 16 * c) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64_t n, int32_t qmax, int32_t* q,
                                 int64_t ldq, int8_t* q_dig, int64_t q_pitch, float* scale, hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)rows), dim3(256), 0, s, x, ldx, n, qmax, q, ldq,
-                     q_dig, q_pitch, scale);
+  const bool vec = n % 4 == 0 && ldx % 4 == 0 && ((uintptr_t)x & 15) == 0 &&
+                   (q == nullptr || (ldq % 4 == 0 && ((uintptr_t)q & 15) == 0)) &&
+                   (q_dig == nullptr || ((uintptr_t)q_dig & 15) == 0);
+  if (vec)
+    hipLaunchKernelGGL(quantize_rows_vec_kernel, dim3((unsigned)rows), dim3(256), 0, s, x, ldx, n, qmax, q, ldq,
+                       q_dig, q_pitch, scale);
+  else
+    hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)rows), dim3(256), 0, s, x, ldx, n, qmax, q, ldq,
+                       q_dig, q_pitch, scale);
   return hipGetLastError();
 }
 

@@ -253,17 +253,44 @@ def test_hadamard_in_place_roundtrip_and_no_signs():
     assert np.max(np.abs(y.cpu().numpy() - ref) / np.max(np.abs(ref), axis=1, keepdims=True)) <= 1e-5
 
 
-@pytest.mark.parametrize("rows,n,qmax", [(5, 100, 127), (16, 8192, 1997), (3, 28672, 567), (2, 64, 1)])
-def test_quantize(rows, n, qmax):
+@pytest.mark.parametrize("rows,n,qmax", [(5, 100, 127), (16, 8192, 1997), (3, 28672, 567), (2, 64, 1),
+                                         (7, 102, 127), (4, 4100, 300)])
+@pytest.mark.parametrize("offset", [0, 1])
+def test_quantize(rows, n, qmax, offset):
+    """offset 1 reads rows that start one float into a wider buffer (not
+    16-byte aligned): the general kernel; offset 0 with n % 4 == 0: the
+    vector kernel."""
     x = _rng_np(n).standard_normal((rows, n)).astype(np.float32)
     x[1] = 0.0
-    xd = torch.from_numpy(x).cuda()
+    wide = torch.zeros((rows, n + 4), dtype=torch.float32, device="cuda")
+    wide[:, offset: offset + n] = torch.from_numpy(x).cuda()
+    xd = wide[:, offset: offset + n]
     q = torch.empty((rows, n), dtype=torch.int32, device="cuda")
     dig = Digits.empty(rows, n)
+    dig.buf.fill_(0x55)
     sc = torch.empty(rows, dtype=torch.float32, device="cuda")
     m.mosaic_quantize_rows(xd, qmax, q=q, q_dig=dig, scale=sc)
     torch.cuda.synchronize()
     qr, sr = oquant.quantize_rows(x, qmax)
     assert np.array_equal(sc.cpu().numpy(), sr)
+    assert np.array_equal(q.cpu().numpy(), qr)
+    assert np.array_equal(unpack_digits(dig), qr.view(np.uint32))
+    assert pad_is_zero(dig)
+
+
+def test_quantize_single_outputs():
+    """Codes only and digits only; a call with neither is rejected."""
+    rows, n, qmax = 6, 1024, 511
+    x = _rng_np(99).standard_normal((rows, n)).astype(np.float32)
+    xd = torch.from_numpy(x).cuda()
+    qr, sr = oquant.quantize_rows(x, qmax)
+    q = torch.empty((rows, n), dtype=torch.int32, device="cuda")
+    m.mosaic_quantize_rows(xd, qmax, q=q)
+    dig = Digits.empty(rows, n)
+    m.mosaic_quantize_rows(xd, qmax, q_dig=dig)
+    sc = torch.empty(rows, dtype=torch.float32, device="cuda")
+    with pytest.raises(m.MosaicError):
+        m.mosaic_quantize_rows(xd, qmax, scale=sc)
+    torch.cuda.synchronize()
     assert np.array_equal(q.cpu().numpy(), qr)
     assert np.array_equal(unpack_digits(dig), qr.view(np.uint32))
