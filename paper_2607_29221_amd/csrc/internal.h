@@ -72,6 +72,87 @@ __device__ __forceinline__ void gemm_epilogue(const GemmLaunch& g, int64_t m, in
   }
 }
 
+// True if the tile epilogue may use 16-byte accesses for every operand:
+// N % 4 == 0 (so a 4-column chunk is wholly inside or outside the matrix),
+// 16-byte aligned base pointers and row pitches that are multiples of 4.
+inline bool gemm_epilogue_vectorizable(const GemmLaunch& g, EpilogueKind epi) {
+  auto ok = [](const void* p, int64_t ld) { return p == nullptr || ((((uintptr_t)p) & 15) == 0 && (ld & 3) == 0); };
+  if (g.N % 4 != 0) return false;
+  if (epi == EPI_STORE) return ok(g.c, g.ldc);
+  return ok(g.ym, g.ldy) && ok(g.kc, g.ldk) && ok(g.y, g.ldo) && ok(g.y_f32, g.ldf) &&
+         (g.y_f32 == nullptr || (((uintptr_t)g.s_cols) & 15) == 0);
+}
+
+// Epilogue of a TM x TN output tile held in LDS (row pitch TROW words) by a
+// workgroup of NT threads: chunks of 4 consecutive columns, thread t taking
+// chunks t, t + NT, .... VEC (see gemm_epilogue_vectorizable): 16-byte
+// accesses, and the unmask inputs of all of a thread's chunks are loaded
+// first, from addresses clamped into the matrix so that the loads need no
+// branches (values of chunks outside the matrix are discarded). Otherwise one
+// word at a time through gemm_epilogue.
+template <int EPI, int VEC, int TM, int TN, int NT, int TROW>
+__device__ __forceinline__ void gemm_tile_epilogue(const GemmLaunch& g, const uint32_t* tile, int64_t m0,
+                                                   int64_t n0, int tid) {
+  constexpr int CPR = TN / 4;                     // chunks per tile row
+  constexpr int PER = TM * CPR / NT;              // chunks per thread
+  static_assert(TM * CPR % NT == 0, "tile must split evenly");
+  if (!VEC) {
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + NT * k;
+      const int r = c / CPR;
+      const int64_t m = m0 + r;
+      const int64_t n = n0 + 4 * (c % CPR);
+      for (int e = 0; e < 4; ++e)
+        if (m < g.M && n + e < g.N) gemm_epilogue<EPI>(g, m, n + e, tile[r * TROW + 4 * (c % CPR) + e]);
+    }
+    return;
+  }
+  if (EPI == EPI_STORE) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + NT * k;
+      const int r = c / CPR;
+      const int64_t m = m0 + r;
+      const int64_t n = n0 + 4 * (c % CPR);
+      if (m < g.M && n < g.N)
+        *(uint4*)(g.c + m * g.ldc + n) = *(const uint4*)(tile + r * TROW + 4 * (c % CPR));
+    }
+    return;
+  }
+  const bool dq = g.y_f32 != nullptr;
+  uint4 ymv[PER], kcv[PER];
+  float4 scv[PER];
+  float srv[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + NT * k;
+    const int64_t m = min(m0 + c / CPR, g.M - 1);
+    const int64_t n = min(n0 + 4 * (c % CPR), g.N - 4);
+    ymv[k] = *(const uint4*)(g.ym + m * g.ldy + n);
+    kcv[k] = g.kc != nullptr ? *(const uint4*)(g.kc + m * g.ldk + n) : make_uint4(0u, 0u, 0u, 0u);
+    if (dq) {
+      scv[k] = *(const float4*)(g.s_cols + n);
+      srv[k] = g.s_rows[m];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + NT * k;
+    const int r = c / CPR;
+    const int64_t m = m0 + r;
+    const int64_t n = n0 + 4 * (c % CPR);
+    if (m >= g.M || n >= g.N) continue;
+    const uint4 a = *(const uint4*)(tile + r * TROW + 4 * (c % CPR));
+    const uint32_t o0 = ymv[k].x - kcv[k].x - a.x, o1 = ymv[k].y - kcv[k].y - a.y;
+    const uint32_t o2 = ymv[k].z - kcv[k].z - a.z, o3 = ymv[k].w - kcv[k].w - a.w;
+    if (g.y != nullptr) *(int4*)(g.y + m * g.ldo + n) = make_int4((int)o0, (int)o1, (int)o2, (int)o3);
+    if (dq)
+      *(float4*)(g.y_f32 + m * g.ldf + n) =
+          make_float4((float)(int32_t)o0 * srv[k] * scv[k].x, (float)(int32_t)o1 * srv[k] * scv[k].y,
+                      (float)(int32_t)o2 * srv[k] * scv[k].z, (float)(int32_t)o3 * srv[k] * scv[k].w);
+  }
+}
+
 // Unmask without a product term (R = 0): out = ym - kc.
 hipError_t launch_unmask_elementwise(const GemmLaunch& g, hipStream_t s);
 

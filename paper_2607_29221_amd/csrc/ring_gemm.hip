@@ -112,7 +112,7 @@ __device__ __forceinline__ void wait_loads(int n) {
 
 __device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
 
-template <int EPI>
+template <int EPI, int VEC>
 __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   __shared__ __attribute__((aligned(1024))) char lds[NSTAGE * STAGE];
 
@@ -261,19 +261,27 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   // epilogue: recombine the shift classes and write. Output layout of the
   // 32 x 32 MFMA: register v of lane l holds row 8 (v / 4) + 4 (l / 32) + v % 4,
   // column l % 32.
-  const int64_t n = n0 + wn * 32 + (lane & 31);
+  // Recombine the shift classes and stage the 128 x 128 tile in LDS (rows
+  // padded to 132 words so the two rows a wave writes per instruction fall in
+  // different banks), then write it out in 16-byte chunks along rows: thread
+  // t takes chunks t + 512 k (row c / 32, columns 4 (c % 32) .. + 3), so each
+  // wave instruction covers two whole 512-byte tile rows. All loads of the
+  // unmask epilogue (Y', K_c, scales) are issued before its first store.
+  __builtin_amdgcn_s_barrier();                 // every wave is done reading stage data
+  uint32_t* ctile = (uint32_t*)lds;
+  constexpr int TROW = BN + 4;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int64_t m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-      if (m < g.M && n < g.N) {
-        const uint32_t val = (uint32_t)acc[i][0][v] + ((uint32_t)acc[i][1][v] << 8) +
-                             ((uint32_t)acc[i][2][v] << 16) + ((uint32_t)acc[i][3][v] << 24);
-        gemm_epilogue<EPI>(g, m, n, val);
-      }
+      const int r = wm * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+      const int c = wn * 32 + (lane & 31);
+      ctile[r * TROW + c] = (uint32_t)acc[i][0][v] + ((uint32_t)acc[i][1][v] << 8) +
+                           ((uint32_t)acc[i][2][v] << 16) + ((uint32_t)acc[i][3][v] << 24);
     }
   }
+  __syncthreads();
+  gemm_tile_epilogue<EPI, VEC, BM, BN, NTHREADS, TROW>(g, ctile, m0, n0, tid);
 }
 
 }  // namespace
@@ -282,10 +290,15 @@ hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s
   if (g.M <= SKINNY_MAX_M) return launch_ring_gemm_skinny(g, epi, s);
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles == 0) return hipSuccess;
-  if (epi == EPI_STORE)
-    hipLaunchKernelGGL(ring_gemm_kernel<EPI_STORE>, dim3((unsigned)tiles), dim3(NTHREADS), 0, s, g);
-  else
-    hipLaunchKernelGGL(ring_gemm_kernel<EPI_UNMASK>, dim3((unsigned)tiles), dim3(NTHREADS), 0, s, g);
+  const dim3 grid((unsigned)tiles);
+  const bool vec = gemm_epilogue_vectorizable(g, epi);
+  if (epi == EPI_STORE) {
+    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 1>), grid, dim3(NTHREADS), 0, s, g);
+    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 0>), grid, dim3(NTHREADS), 0, s, g);
+  } else {
+    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 1>), grid, dim3(NTHREADS), 0, s, g);
+    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 0>), grid, dim3(NTHREADS), 0, s, g);
+  }
   return hipGetLastError();
 }
 

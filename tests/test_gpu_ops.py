@@ -176,7 +176,8 @@ def test_masked_matmul_ldc_and_offsets():
     assert np.all(got[:, :5] == 0) and np.all(got[:, 5 + N:] == 0)
 
 
-@pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192), (1, 300, 2560), (8, 33, 64)])
+@pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192), (1, 300, 2560), (8, 33, 64),
+                                   (200, 132, 192), (130, 256, 64), (257, 4, 128)])
 @pytest.mark.parametrize("with_k", [True, False])
 def test_unmask(M, N, R, with_k):
     rng = _rng_np(M + N + R)
@@ -200,10 +201,10 @@ def test_unmask(M, N, R, with_k):
     assert np.array_equal(y.cpu().numpy(), ref.view(np.int32))
 
 
-@pytest.mark.parametrize("M", [40, 150])
-def test_unmask_dequantised(M):
-    rng = _rng_np(5 + M)
-    N, R = 90, 64
+@pytest.mark.parametrize("M,N", [(40, 90), (150, 90), (150, 92), (300, 260)])
+def test_unmask_dequantised(M, N):
+    rng = _rng_np(5 + M + N)
+    R = 64
     ym = _random_ring(rng, (M, N))
     q = _random_ring(rng, (M, R))
     l = _random_ring(rng, (N, R))
