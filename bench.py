@@ -322,16 +322,19 @@ def _shape(name):
 
 
 def run_cpu_baseline():
-    """The oracle on a bounded sample of the same workload: 64 tokens x 64
+    """The oracle on a bounded sample of the same workload: 512 tokens x 128
     output columns of the (K, N) = (8192, 8192) shape, full per-call path
-    (Init X, mask, server product incl. Q, unmask); Init W for those 64
-    weight rows is prepared outside the timed region."""
+    (Init X, mask, server product incl. Q, unmask; 10-20 s of CPU work);
+    Init W for those 128 weight rows is prepared outside the timed region.
+    At this output width the rank-1536 mask products (U_a and Q, M K r ring
+    MACs each) dominate the oracle's work, so its rate per plaintext ring op
+    is lower than it would be at the full width."""
     import numpy as np
 
     from oracle import protocol as op
     from synthetic_inputs import PARAMS_PAPER_D1, PREFILL_SEED, int8_operands
 
-    K, N, Ms, Ns = 8192, 8192, 64, 64
+    K, N, Ms, Ns = 8192, 8192, 512, 128
     A, W = int8_operands(2048, K, N, PREFILL_SEED)
     seed = 0x6D6F736169630000 | PREFILL_SEED
     ws = op.init_w(W[:Ns], PARAMS_PAPER_D1, seed, 0)
@@ -347,7 +350,7 @@ def run_cpu_baseline():
     return {"value": ops / dt / 1e12, "unit": "ring-TOPS", "cores": 1, "kind": "oracle",
             "seconds": round(dt, 2),
             "sample": f"{Ms} tokens x {Ns} output columns of (K, N) = ({K}, {N}), rank 1536, full per-call "
-                      "path (Init X, mask, server incl. Q, unmask); numpy single-threaded"}
+                      "path (Init X, mask, server incl. Q, unmask); numpy integer matmul, single-threaded"}
 
 
 def main():
