@@ -139,6 +139,7 @@ def run_gpu(steps: int, warmup: int, extras: bool):
         out["extras"] = run_extras(dev)
         out["extras"]["decode"] = run_decode(dev)
         out["extras"]["decoder_stack"] = run_decoder_stack(dev)
+        out["extras"]["integrity_check"] = run_integrity(dev)
     return out
 
 
@@ -230,6 +231,40 @@ def run_extras(dev):
     res["quantize_4096x8192_us"] = round(t * 1e3, 2)
     res["quantize_gbs"] = round(rows * n * 8 / (t * 1e-3) / 1e9, 1)
     return res
+
+
+def run_integrity(dev):
+    """Cost of the integrity check (Freivalds' test, 32 check vectors) per
+    prefill call: Init W with the check key (once, untimed), one honest call,
+    then the check timed with HIP events (mean over 10) and compared with the
+    call's server product."""
+    import torch
+
+    from paper_2607_29221_amd import protocol as gp
+    from synthetic_inputs import PARAMS_PAPER_D1, PREFILL_KN, PREFILL_M, PREFILL_SEED, int8_operands
+
+    M, t, reps = PREFILL_M, 32, 10
+    out = []
+    for idx, (K, N) in enumerate(PREFILL_KN):
+        A, W = int8_operands(M, K, N, PREFILL_SEED)
+        w = gp.MaskedWeight(torch.from_numpy(W).to(dev), PARAMS_PAPER_D1, 0x6D6F736169630000 | PREFILL_SEED,
+                            weight_id=idx, check_vectors=t)
+        buf = gp.run_call(w, torch.from_numpy(A).to(dev), call_id=1)
+        ok = int(gp.verify(w, M, buf).item()) == 0
+        e = _events(4)
+        e[0].record()
+        for _ in range(reps):
+            gp.server(w, M, buf)
+        e[1].record()
+        for _ in range(reps):
+            gp.verify(w, M, buf)
+        e[2].record()
+        torch.cuda.synchronize()
+        sv, ck = e[0].elapsed_time(e[1]) / reps, e[1].elapsed_time(e[2]) / reps
+        out.append({"K": K, "N": N, "vectors": t, "honest_call_accepted": ok, "check_ms": round(ck, 4),
+                    "server_ms": round(sv, 4), "check_over_server": round(ck / sv, 4)})
+        del w, buf
+    return out
 
 
 def run_decode(dev):

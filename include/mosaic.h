@@ -169,6 +169,19 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy,
                             const float* s_rows, const float* s_cols,
                             float* y_f32, int64_t ldf, void* stream);
 
+/* Integrity check (Freivalds' test; Appendix "Computational integrity" and
+ * online step 4 of the Section 4.2 protocol box): the client compares two
+ * short products that agree whenever the server's product was computed
+ * honestly. This call counts the entries where two uint32 matrices differ:
+ *     *count = #{(i, j) : a(i, j) != b(i, j)},  0 <= i < rows, 0 <= j < cols
+ * a and b are device matrices with leading dimensions lda, ldb >= cols;
+ * ``count`` is a device int64 written by the call (0 for an empty matrix).
+ * One workgroup does the whole count, so the call is meant for the check's
+ * small matrices (t x M). Fails with MOSAIC_ERR_INVALID_ARG for NULL
+ * pointers or leading dimensions < cols. */
+mosaic_status mosaic_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb,
+                                      int64_t rows, int64_t cols, int64_t* count, void* stream);
+
 /* a1 (signs). Random sign vector of the rotation (Section 5: d drawn
  * uniformly from {+1, -1}^n): out[j] = +1 if bit 31 of word j of the stream
  * (rng->seed, rng->stream, rng->instance) is 0, else -1. ``out`` is a device

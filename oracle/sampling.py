@@ -45,6 +45,8 @@ STREAM_EX = 0x50          # E_x, full-rank LWE error on the activations
 STREAM_R = 0x51           # R, secret right factor
 STREAM_T = 0x60           # + i: T_i, sparse LPN mask on the activations
 STREAM_SIGNS = 0x70       # d, Hadamard rotation signs
+STREAM_CHECK_W = 0x80     # integrity check vectors for the Y' outputs (t x m)
+STREAM_CHECK_Q = 0x90     # + i: integrity check vectors for the Q_i outputs (t x r_i)
 
 
 def stream_words(seed: int, stream: int, instance: int, t0: int, count: int) -> np.ndarray:

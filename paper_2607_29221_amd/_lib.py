@@ -44,6 +44,7 @@ _SIGNATURES = {
     "mosaic_unmask": ([c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64,
                        c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
     "mosaic_sample_signs": ([ctypes.POINTER(MosaicRng), c_i64, c_ptr, c_ptr], c_i32),
+    "mosaic_count_mismatches": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_hadamard_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
     "mosaic_quantize_rows": ([c_ptr, c_i64, c_i64, c_i64, c_i32, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_ptr],
                              c_i32),

@@ -219,6 +219,18 @@ mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch, const i
   return hip_status(launch_ring_gemm(g, EPI_STORE, (hipStream_t)stream), "ring product launch");
 }
 
+mosaic_status mosaic_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb,
+                                      int64_t rows, int64_t cols, int64_t* count, void* stream) {
+  if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (count == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "count is NULL");
+  if (rows > 0 && cols > 0) {
+    if (a == nullptr || b == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "a or b is NULL");
+    if (lda < cols || ldb < cols) return fail(MOSAIC_ERR_INVALID_ARG, "leading dimension < cols");
+  }
+  return hip_status(launch_count_mismatches(a, lda, b, ldb, rows, cols, count, (hipStream_t)stream),
+                    "mismatch count launch");
+}
+
 mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy, const uint32_t* kc, int64_t ldk, const int8_t* q_dig,
                             int64_t q_pitch, const int8_t* l_dig, int64_t l_pitch, int64_t M, int64_t N, int64_t R,
                             int32_t* y, int64_t ldo, const float* s_rows, const float* s_cols, float* y_f32,

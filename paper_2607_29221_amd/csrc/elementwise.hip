@@ -183,6 +183,30 @@ __global__ __launch_bounds__(256) void signs_kernel(RngArgs r, int64_t n, int8_t
     if (e0 + q < n) out[e0 + q] = (ww[q] >> 31) ? (int8_t)-1 : (int8_t)1;
 }
 
+// One workgroup of 1024 threads counts differing entries: each thread scans
+// a strided share of the elements, then wave shuffles and one LDS word per
+// wave reduce the counts, and thread 0 writes the total.
+__global__ __launch_bounds__(1024) void count_mismatches_kernel(const uint32_t* a, int64_t lda, const uint32_t* b,
+                                                                int64_t ldb, int64_t rows, int64_t cols,
+                                                                int64_t* count) {
+  __shared__ unsigned long long part[16];
+  unsigned long long n = 0;
+  const int64_t total = rows * cols;
+  for (int64_t e = threadIdx.x; e < total; e += 1024) {
+    const int64_t i = e / cols, j = e - i * cols;
+    n += (a[i * lda + j] != b[i * ldb + j]) ? 1ull : 0ull;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) n += __shfl_xor(n, off);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = n;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long t = 0;
+    for (int w = 0; w < 16; ++w) t += part[w];
+    *count = (int64_t)t;
+  }
+}
+
 __global__ __launch_bounds__(256) void unmask_elementwise_kernel(GemmLaunch g) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t i = gid / g.N;
@@ -227,6 +251,12 @@ hipError_t launch_signs(const RngArgs& r, int64_t n, int8_t* out, hipStream_t s)
   const int64_t threads = (n + 3) / 4;
   if (threads == 0) return hipSuccess;
   hipLaunchKernelGGL(signs_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, r, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb, int64_t rows,
+                                   int64_t cols, int64_t* count, hipStream_t s) {
+  hipLaunchKernelGGL(count_mismatches_kernel, dim3(1), dim3(1024), 0, s, a, lda, b, ldb, rows, cols, count);
   return hipGetLastError();
 }
 

@@ -27,6 +27,9 @@ hipError_t launch_mask(const MaskLaunch& a, hipStream_t s);
 
 hipError_t launch_signs(const RngArgs& r, int64_t n, int8_t* out, hipStream_t s);
 
+hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb, int64_t rows,
+                                   int64_t cols, int64_t* count, hipStream_t s);
+
 // Ring product C = A B^T with an epilogue.
 enum EpilogueKind { EPI_STORE = 0, EPI_UNMASK = 1 };
 struct GemmLaunch {

@@ -148,6 +148,18 @@ def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digi
                                      y_f32.stride(0) if y_f32 is not None else 0, _stream()), "mosaic_unmask")
 
 
+def mosaic_count_mismatches(a: torch.Tensor, b: torch.Tensor, count: torch.Tensor) -> None:
+    """count[0] = number of entries where the int32 matrices a and b differ
+    (same shape; count is a one-element int64 device tensor)."""
+    if a.shape != b.shape or a.dim() != 2:
+        raise ValueError("a and b must be matrices of the same shape")
+    if count.dtype != torch.int64 or count.numel() < 1:
+        raise ValueError("count must be an int64 tensor")
+    rows, cols = a.shape
+    _check(_lib.load().mosaic_count_mismatches(a.data_ptr(), a.stride(0), b.data_ptr(), b.stride(0), rows, cols,
+                                               count.data_ptr(), _stream()), "mosaic_count_mismatches")
+
+
 def mosaic_sample_signs(r: _lib.MosaicRng, n: int, out: torch.Tensor) -> None:
     _check(_lib.load().mosaic_sample_signs(ctypes.byref(r), n, out.data_ptr(), _stream()), "mosaic_sample_signs")
 

@@ -41,6 +41,8 @@ STREAM_EX = 0x50
 STREAM_R = 0x51
 STREAM_T = 0x60     # + i
 STREAM_SIGNS = 0x70
+STREAM_CHECK_W = 0x80   # integrity check vectors for the Y' columns
+STREAM_CHECK_Q = 0x90   # + i: integrity check vectors for the Q_i columns
 
 
 def _noise_rng(params, seed: int, stream: int, instance: int):
@@ -59,9 +61,16 @@ def _ring_empty(rows: int, cols: int, device) -> torch.Tensor:
 class MaskedWeight:
     """Init W of the protocol box for one plaintext weight matrix W (N x K,
     int8/int16/int32 on the GPU). Holds the server's Bext and the client's
-    unmasking material."""
+    unmasking material.
 
-    def __init__(self, W: torch.Tensor, params, seed: int, weight_id: int = 0):
+    With ``check_vectors`` = t > 0 it also prepares the integrity check of
+    the server's outputs (Freivalds' test; box Init W step 3): check vectors
+    a_W (t x N, uniform) for the Y' columns and a_i (t x r_i) for each Q_i,
+    and the key c^T = a_W W' + sum_i a_i (M_i ... M_1) (t x K), all held in
+    digit layout by the client. One vector misses an error in the top bit
+    with probability 1/2 over Z_{2^32}; t vectors bound that by 2^-t."""
+
+    def __init__(self, W: torch.Tensor, params, seed: int, weight_id: int = 0, check_vectors: int = 0):
         dev = W.device
         N, K = W.shape
         r = list(params.ranks)
@@ -128,13 +137,37 @@ class MaskedWeight:
                                   log2_inv_density=params.sparse_log2_inv_density),
                             N, r[lv - 1], out_dig=self.Lcat[slot])
 
+        # integrity check vectors (slots of a_Q in the order of Q's columns)
+        self.t = int(check_vectors)
+        if self.t > 0:
+            t = self.t
+            self.aW = Digits.empty(t, N, dev)
+            m.mosaic_sample(m.rng(s, STREAM_CHECK_W, weight_id, U), t, N, out_dig=self.aW)
+            self.aQ = Digits.concat(t, self.slot_ranks, dev)
+            for slot, lv in enumerate(self.slot_levels):
+                m.mosaic_sample(m.rng(s, STREAM_CHECK_Q + lv, weight_id, U), t, r[lv - 1], out_dig=self.aQ[slot])
+            key_q = _ring_empty(t, K, dev)          # sum_i a_i Mc_i = aQcat McTcat^T
+            m.mosaic_masked_matmul(self.aQ[0].whole(self.R), McTcat[0].whole(self.R), t, K, self.R, key_q)
+
         # U_w = Lcat McTcat^T (= L Mc_d + sum S_{i+1} Mc_i); W' = W + U_w + E_w
         U_w = _ring_empty(N, K, dev)
         m.mosaic_masked_matmul(self.Lcat[0].whole(self.R), McTcat[0].whole(self.R), N, K, self.R, U_w)
         del McTcat
         ew = _noise_rng(params, s, STREAM_EW, weight_id)
-        m.mosaic_mask(W, U_w, ew, N, K, out_dig=Digits(self.Bext.buf[:N], K))
+        Wm = _ring_empty(N, K, dev) if self.t > 0 else None
+        m.mosaic_mask(W, U_w, ew, N, K, out=Wm, out_dig=Digits(self.Bext.buf[:N], K))
         del U_w
+        if self.t > 0:
+            # key: c^T = a_W W' + key_q, with W'^T in digit layout for the product
+            WmT = Digits.empty(K, N, dev)
+            m.mosaic_mask(Wm, None, None, K, N, out_dig=WmT, x_transposed=True)
+            del Wm
+            key_w = _ring_empty(self.t, K, dev)
+            m.mosaic_masked_matmul(self.aW, WmT, self.t, K, N, key_w)
+            del WmT
+            self.cT = Digits.empty(self.t, K, dev)
+            m.mosaic_mask(key_w, key_q, None, self.t, K, out_dig=self.cT)
+            del key_w, key_q
 
         # client: J_i = (W + E_w) Nc_i, stored in the lower rows of Bx
         WE = Digits.empty(N, K, dev)
@@ -161,6 +194,7 @@ class CallBuffers:
     YQ: torch.Tensor           # [Y' | Q], M x (N + R)
     Qdig: List[Digits]         # Q slots in digit layout, M x R
     Y: torch.Tensor            # unmasked output, M x N int32
+    check: Optional[tuple] = None   # (lhs, rhs) of the last integrity check
 
 
 def alloc_call(w: MaskedWeight, M: int, device="cuda") -> CallBuffers:
@@ -207,6 +241,36 @@ def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tens
         m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
     m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
                     M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
+
+
+def verify(w: MaskedWeight, M: int, buf: CallBuffers) -> torch.Tensor:
+    """Online step 4 (Freivalds' test) on the server's [Y' | Q]: forms
+    lhs = c^T A'^T and rhs = a_W Y'^T^T + a_Q Q^T^T (both t x M, on the masked
+    activations A' the server multiplied) and returns a one-element int64
+    device tensor with the number of entries where they differ: 0 accepts
+    the call. Work O((K + N + R) M t), against M K (N + R) for the product."""
+    if w.t <= 0:
+        raise ValueError("the weight was prepared without check vectors")
+    dev = buf.YQ.device
+    t = w.t
+    Ydig = Digits.empty(M, w.N, dev)
+    m.mosaic_mask(None, buf.YQ[:, : w.N], None, M, w.N, out_dig=Ydig)
+    r = list(w.params.ranks)
+    for slot, lv in enumerate(w.slot_levels):
+        c0 = w.q_cols[slot]
+        m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
+    lhs = _ring_empty(t, M, dev)
+    m.mosaic_masked_matmul(w.cT, buf.A_masked, t, M, w.K, lhs)
+    ry = _ring_empty(t, M, dev)
+    m.mosaic_masked_matmul(w.aW, Ydig, t, M, w.N, ry)
+    rq = _ring_empty(t, M, dev)
+    m.mosaic_masked_matmul(w.aQ[0].whole(w.R), buf.Qdig[0].whole(w.R), t, M, w.R, rq)
+    rhs = _ring_empty(t, M, dev)
+    m.mosaic_mask(ry, rq, None, t, M, out=rhs)
+    count = torch.empty(1, dtype=torch.int64, device=dev)
+    m.mosaic_count_mismatches(lhs, rhs, count)
+    buf.check = (lhs, rhs)
+    return count
 
 
 def run_call(w: MaskedWeight, A: torch.Tensor, call_id: int, buf: Optional[CallBuffers] = None) -> CallBuffers:

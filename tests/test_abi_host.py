@@ -107,6 +107,14 @@ def test_unmask_validation(lib):
     assert call(R=40000, qp=4 * 40000 + 64, lp=4 * 40000 + 64) == UNSUPPORTED
 
 
+def test_count_mismatches_validation(lib):
+    assert lib.mosaic_count_mismatches(FAKE, 4, FAKE, 4, 2, 4, None, None) == INVALID      # no count
+    assert lib.mosaic_count_mismatches(None, 4, FAKE, 4, 2, 4, FAKE, None) == INVALID
+    assert lib.mosaic_count_mismatches(FAKE, 3, FAKE, 4, 2, 4, FAKE, None) == INVALID      # lda < cols
+    assert lib.mosaic_count_mismatches(FAKE, 4, FAKE, 3, 2, 4, FAKE, None) == INVALID
+    assert lib.mosaic_count_mismatches(FAKE, 4, FAKE, 4, -1, 4, FAKE, None) == INVALID
+
+
 def test_hadamard_validation(lib):
     def call(x=FAKE, ldx=64, y=FAKE + (1 << 24), ldy=64, rows=2, n=64, block=64, signs=None, inv=0):
         return lib.mosaic_hadamard_rotate(x, ldx, y, ldy, rows, n, block, signs, inv, None)
