@@ -283,12 +283,18 @@ def run_decode(dev):
     reps = 20
     for idx, (K, N) in enumerate(DECODE_KN):
         A, W = int8_operands(max(DECODE_M), K, N, DECODE_SEED)
-        w = gp.MaskedWeight(torch.from_numpy(W).to(dev), PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + idx, weight_id=idx)
+        Wd = torch.from_numpy(W).to(dev)
+        w = gp.MaskedWeight(Wd, PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + idx, weight_id=idx)
+        ws = gp.MaskedWeight(Wd, PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + idx, weight_id=idx, sparse_lpn=True)
         for M in DECODE_M:
             Ad = torch.from_numpy(A[:M].copy()).to(dev)
             buf = gp.alloc_call(w, M, dev)
             for i in range(3):
                 gp.run_call(w, Ad, 10_000 + i, buf)
+            torch.cuda.synchronize()
+            bufs = gp.alloc_call(ws, M, dev)
+            for i in range(3):
+                gp.run_call(ws, Ad, 10_000 + i, bufs)
             torch.cuda.synchronize()
             e = _events(4)
             e[0].record()
@@ -298,16 +304,21 @@ def run_decode(dev):
             for i in range(reps):
                 gp.run_call(w, Ad, 20_000 + i, buf)
             e[2].record()
+            for i in range(reps):
+                gp.run_call(ws, Ad, 20_000 + i, bufs)
+            e[3].record()
             torch.cuda.synchronize()
             server_ms = e[0].elapsed_time(e[1]) / reps
             call_ms = e[1].elapsed_time(e[2]) / reps
+            call_sparse_ms = e[2].elapsed_time(e[3]) / reps
             Kp = 64 * ((K + 63) // 64)
             byts = 4 * Kp * (M + w.n_out) + 4 * M * w.n_out
             res.append({"K": K, "N": N, "M": M, "server_us": round(server_ms * 1e3, 2),
                         "server_gbs": round(byts / (server_ms * 1e-3) / 1e9, 1),
                         "server_hbm_frac": round(byts / (server_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
-                        "call_us": round(call_ms * 1e3, 2)})
-        del w
+                        "call_us": round(call_ms * 1e3, 2),
+                        "call_us_sparse_lpn": round(call_sparse_ms * 1e3, 2)})
+        del w, ws
     return res
 
 

@@ -169,6 +169,52 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy,
                             const float* s_rows, const float* s_cols,
                             float* y_f32, int64_t ldf, void* stream);
 
+/* Sparse LPN matrices in compressed-row form (Section 4.2 protocol box:
+ * S_{i+1} and T_{i+1} are sparse with noise rate 2^-s; the client's products
+ * with them then cost O(nonzeros) per output row, Section 4.2 cost analysis
+ * and Table "lpn-tradeoff").
+ *
+ * The matrix is the rows x cols SPARSE stream matrix of ``rng`` (rng->dist
+ * must be MOSAIC_DIST_SPARSE, rng->transposed 0). Its compressed rows are
+ *   row_ptr[0 .. rows]     int64, row_ptr[0] = 0, row i owns
+ *                          entries row_ptr[i] .. row_ptr[i+1]-1;
+ *   col_idx[nnz], values[nnz]  column (int32, increasing within a row) and
+ *                          ring value (uint32) of each nonzero.
+ * mosaic_sparse_csr_count writes row_ptr (rows + 1 entries); the caller
+ * then sizes col_idx / values to at least row_ptr[rows] entries (reading it
+ * back, or using the bound rows * cols) and calls mosaic_sparse_csr_fill. */
+mosaic_status mosaic_sparse_csr_count(const mosaic_rng* rng, int64_t rows, int64_t cols, int64_t* row_ptr,
+                                      void* stream);
+mosaic_status mosaic_sparse_csr_fill(const mosaic_rng* rng, int64_t rows, int64_t cols, const int64_t* row_ptr,
+                                     int32_t* col_idx, uint32_t* values, void* stream);
+
+/* Products with a compressed-row sparse matrix P (rows of P given by
+ * row_ptr / col_idx / values as above), over Z_{2^32}; ``subtract`` selects
+ * c -= ... instead of c += ....
+ *
+ * mosaic_sparse_gather_rows: c(i, k) +-= sum_j P(i, j) d(j, k) for
+ *   0 <= i < rows, 0 <= k < ncols: P is rows x r, d is a dense r x ncols
+ *   uint32 matrix (ldd), c is rows x ncols (ldc). Used for T_{i+1} terms of
+ *   U_x and K (Init X) and for S_{i+1} (M_i ... M_1) in U_w (Init W).
+ * mosaic_sparse_gather_cols: c(m, n) +-= sum_j d(m, j) P(n, j) for
+ *   0 <= m < M, 0 <= n < N: P is N x r, d is a dense M x r uint32 matrix
+ *   (ldd), c is M x N (ldc). Used for the S_{i+1} Q_i terms of unmasking.
+ * c must not overlap d or the sparse arrays. */
+mosaic_status mosaic_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const int32_t* col_idx,
+                                        const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
+                                        uint32_t* c, int64_t ldc, int32_t subtract, void* stream);
+/* mosaic_sparse_stream_gather_rows: as mosaic_sparse_gather_rows with P the
+ *   rows x rcols SPARSE stream matrix of ``rng`` itself (same validity rules
+ *   as mosaic_sparse_csr_count): each row's nonzeros are drawn inside the
+ *   call, so no compressed form is stored (T_{i+1} of Init X, drawn afresh
+ *   for every call). */
+mosaic_status mosaic_sparse_stream_gather_rows(const mosaic_rng* rng, int64_t rows, int64_t rcols, const uint32_t* d,
+                                               int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc,
+                                               int32_t subtract, void* stream);
+mosaic_status mosaic_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
+                                        const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
+                                        int64_t ldc, int32_t subtract, void* stream);
+
 /* Integrity check (Freivalds' test; Appendix "Computational integrity" and
  * online step 4 of the Section 4.2 protocol box): the client compares two
  * short products that agree whenever the server's product was computed

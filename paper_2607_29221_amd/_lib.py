@@ -45,6 +45,14 @@ _SIGNATURES = {
                        c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
     "mosaic_sample_signs": ([ctypes.POINTER(MosaicRng), c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_count_mismatches": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_ptr, c_ptr], c_i32),
+    "mosaic_sparse_csr_count": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_ptr], c_i32),
+    "mosaic_sparse_csr_fill": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_ptr, c_ptr, c_ptr], c_i32),
+    "mosaic_sparse_gather_rows": ([c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_i64, c_ptr, c_i64, c_i32, c_ptr],
+                                  c_i32),
+    "mosaic_sparse_stream_gather_rows": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_i64, c_i64, c_ptr, c_i64,
+                                          c_i32, c_ptr], c_i32),
+    "mosaic_sparse_gather_cols": ([c_i64, c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr, c_i64, c_i32, c_ptr],
+                                  c_i32),
     "mosaic_hadamard_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
     "mosaic_quantize_rows": ([c_ptr, c_i64, c_i64, c_i64, c_i32, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_ptr],
                              c_i32),

@@ -219,6 +219,80 @@ mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch, const i
   return hip_status(launch_ring_gemm(g, EPI_STORE, (hipStream_t)stream), "ring product launch");
 }
 
+mosaic_status mosaic_sparse_csr_count(const mosaic_rng* rng, int64_t rows, int64_t cols, int64_t* row_ptr,
+                                      void* stream) {
+  if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (cols > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "cols must fit int32");
+  if (row_ptr == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "row_ptr is NULL");
+  if (rng == nullptr || rng->dist != MOSAIC_DIST_SPARSE || rng->transposed)
+    return fail(MOSAIC_ERR_INVALID_ARG, "rng must be a non-transposed SPARSE stream");
+  RngArgs a{};
+  mosaic_status st = rng_args(rng, &a);
+  if (st != MOSAIC_OK) return st;
+  if (rows > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  return hip_status(launch_sparse_csr_count(a, rows, cols, row_ptr, (hipStream_t)stream), "sparse count launch");
+}
+
+mosaic_status mosaic_sparse_csr_fill(const mosaic_rng* rng, int64_t rows, int64_t cols, const int64_t* row_ptr,
+                                     int32_t* col_idx, uint32_t* values, void* stream) {
+  if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (cols > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "cols must fit int32");
+  if (rows == 0 || cols == 0) return MOSAIC_OK;
+  if (row_ptr == nullptr || col_idx == nullptr || values == nullptr)
+    return fail(MOSAIC_ERR_INVALID_ARG, "row_ptr, col_idx or values is NULL");
+  if (rng == nullptr || rng->dist != MOSAIC_DIST_SPARSE || rng->transposed)
+    return fail(MOSAIC_ERR_INVALID_ARG, "rng must be a non-transposed SPARSE stream");
+  RngArgs a{};
+  mosaic_status st = rng_args(rng, &a);
+  if (st != MOSAIC_OK) return st;
+  if (rows > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  return hip_status(launch_sparse_csr_fill(a, rows, cols, row_ptr, col_idx, values, (hipStream_t)stream),
+                    "sparse fill launch");
+}
+
+mosaic_status mosaic_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const int32_t* col_idx,
+                                        const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
+                                        uint32_t* c, int64_t ldc, int32_t subtract, void* stream) {
+  if (rows < 0 || ncols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || ncols == 0) return MOSAIC_OK;
+  if (row_ptr == nullptr || col_idx == nullptr || values == nullptr || d == nullptr || c == nullptr)
+    return fail(MOSAIC_ERR_INVALID_ARG, "NULL operand");
+  if (ldd < ncols || ldc < ncols) return fail(MOSAIC_ERR_INVALID_ARG, "leading dimension < ncols");
+  if (rows > 0x7FFFFFFF || (ncols + 255) / 256 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
+  return hip_status(launch_sparse_gather_rows(rows, row_ptr, col_idx, values, d, ldd, ncols, c, ldc, subtract != 0,
+                                              (hipStream_t)stream), "sparse gather launch");
+}
+
+mosaic_status mosaic_sparse_stream_gather_rows(const mosaic_rng* rng, int64_t rows, int64_t rcols, const uint32_t* d,
+                                               int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc, int32_t subtract,
+                                               void* stream) {
+  if (rows < 0 || rcols < 0 || ncols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || ncols == 0) return MOSAIC_OK;
+  if (c == nullptr || (rcols > 0 && d == nullptr)) return fail(MOSAIC_ERR_INVALID_ARG, "NULL operand");
+  if (ldd < ncols || ldc < ncols) return fail(MOSAIC_ERR_INVALID_ARG, "leading dimension < ncols");
+  if (rng == nullptr || rng->dist != MOSAIC_DIST_SPARSE || rng->transposed)
+    return fail(MOSAIC_ERR_INVALID_ARG, "rng must be a non-transposed SPARSE stream");
+  RngArgs a{};
+  mosaic_status st = rng_args(rng, &a);
+  if (st != MOSAIC_OK) return st;
+  if (rows > 0x7FFFFFFF || (ncols + 255) / 256 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
+  return hip_status(launch_sparse_stream_gather_rows(a, rows, rcols, d, ldd, ncols, c, ldc, subtract != 0,
+                                                     (hipStream_t)stream), "sparse gather launch");
+}
+
+mosaic_status mosaic_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
+                                        const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
+                                        int64_t ldc, int32_t subtract, void* stream) {
+  if (M < 0 || N < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (M == 0 || N == 0) return MOSAIC_OK;
+  if (row_ptr == nullptr || col_idx == nullptr || values == nullptr || d == nullptr || c == nullptr)
+    return fail(MOSAIC_ERR_INVALID_ARG, "NULL operand");
+  if (ldc < N || ldd < 0) return fail(MOSAIC_ERR_INVALID_ARG, "ldc < N");
+  if (M > 0x7FFFFFFF || (N + 31) / 32 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
+  return hip_status(launch_sparse_gather_cols(M, N, row_ptr, col_idx, values, d, ldd, c, ldc, subtract != 0,
+                                              (hipStream_t)stream), "sparse gather launch");
+}
+
 mosaic_status mosaic_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb,
                                       int64_t rows, int64_t cols, int64_t* count, void* stream) {
   if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");

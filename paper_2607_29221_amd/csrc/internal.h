@@ -27,6 +27,19 @@ hipError_t launch_mask(const MaskLaunch& a, hipStream_t s);
 
 hipError_t launch_signs(const RngArgs& r, int64_t n, int8_t* out, hipStream_t s);
 
+hipError_t launch_sparse_csr_count(const RngArgs& r, int64_t rows, int64_t cols, int64_t* row_ptr, hipStream_t s);
+hipError_t launch_sparse_csr_fill(const RngArgs& r, int64_t rows, int64_t cols, const int64_t* row_ptr,
+                                  int32_t* col_idx, uint32_t* values, hipStream_t s);
+hipError_t launch_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const int32_t* col_idx,
+                                     const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
+                                     uint32_t* c, int64_t ldc, int subtract, hipStream_t s);
+hipError_t launch_sparse_stream_gather_rows(const RngArgs& r, int64_t rows, int64_t rcols, const uint32_t* d,
+                                            int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc, int subtract,
+                                            hipStream_t s);
+hipError_t launch_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
+                                     const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
+                                     int64_t ldc, int subtract, hipStream_t s);
+
 hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb, int64_t rows,
                                    int64_t cols, int64_t* count, hipStream_t s);
 

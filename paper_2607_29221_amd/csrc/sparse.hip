@@ -1,0 +1,231 @@
+// Sparse LPN matrices of the nested mask (Section 4.2 protocol box: S_{i+1}
+// on the weight side, T_{i+1} on the activation side; LPN noise of rate
+// 2^-s, Section 3) handled in compressed-row form, so that the client's
+// products with them cost O(nonzeros) instead of the dense O(r_i) per output
+// (the client-cost argument of Section 4.2 with Table "lpn-tradeoff").
+//
+// The matrices are the SPARSE streams of mosaic.h: element (i, j) of a
+// rows x cols matrix is e = i cols + j, nonzero iff the top s bits of word 2e
+// are zero, and then equal to word 2e + 1. Compressed rows list the nonzeros
+// of each row in increasing column order.
+#include "internal.h"
+
+namespace mosaic {
+namespace {
+
+// gate and value of element e (words 2e and 2e + 1 share a Philox block)
+__device__ __forceinline__ bool sparse_elem(const RngArgs& r, uint64_t e, uint32_t* val) {
+  const uint4 blk = philox_block(r, e >> 1);
+  const bool hi = (e & 1) != 0;
+  const uint32_t gate = hi ? blk.z : blk.x;
+  *val = hi ? blk.w : blk.y;
+  return (r.sparse_shift >= 32) ? true : ((gate >> r.sparse_shift) == 0u);
+}
+
+// One wave per row: nonzero count of the row.
+__global__ __launch_bounds__(256) void sparse_count_kernel(RngArgs r, int64_t rows, int64_t cols, int64_t* counts) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  uint32_t n = 0, v;
+  for (int64_t j = lane; j < cols; j += 64) n += sparse_elem(r, (uint64_t)row * cols + j, &v) ? 1u : 0u;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) n += __shfl_xor(n, off);
+  if (lane == 0) counts[row] = n;
+}
+
+// One workgroup: row_ptr[i] = sum of counts[0 .. i-1], row_ptr[rows] = total.
+// counts and row_ptr may be the same array shifted by one (counts = row_ptr + 1).
+__global__ __launch_bounds__(1024) void exclusive_scan_kernel(const int64_t* counts, int64_t rows, int64_t* row_ptr) {
+  __shared__ int64_t part[1024];
+  const int t = threadIdx.x;
+  const int64_t per = (rows + 1023) / 1024;
+  const int64_t b = t * per, e = (b + per < rows) ? b + per : rows;
+  int64_t s = 0;
+  for (int64_t i = b; i < e; ++i) s += counts[i];
+  // When counts aliases row_ptr + 1, the neighbour's write of row_ptr[e]
+  // overwrites counts[e - 1]: keep this chunk's last count in a register.
+  const int64_t last = (e > b) ? counts[e - 1] : 0;
+  part[t] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {       // inclusive Hillis-Steele scan of the chunk sums
+    const int64_t add = (t >= off) ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += add;
+    __syncthreads();
+  }
+  int64_t run = (t > 0) ? part[t - 1] : 0;
+  for (int64_t i = b; i < e; ++i) {                  // counts[i] is read before row_ptr[i] (= counts[i-1]) moves
+    const int64_t c = (i == e - 1) ? last : counts[i];
+    row_ptr[i] = run;
+    run += c;
+  }
+  if (t == 1023) row_ptr[rows] = part[1023];
+}
+
+// One wave per row: nonzeros written in column order (ballot + prefix count).
+__global__ __launch_bounds__(256) void sparse_fill_kernel(RngArgs r, int64_t rows, int64_t cols,
+                                                          const int64_t* row_ptr, int32_t* col_idx, uint32_t* values) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  int64_t base = row_ptr[row];
+  for (int64_t j0 = 0; j0 < cols; j0 += 64) {
+    const int64_t j = j0 + lane;
+    uint32_t v = 0;
+    const bool nz = (j < cols) && sparse_elem(r, (uint64_t)row * cols + j, &v);
+    const uint64_t mask = __ballot(nz);
+    if (nz) {
+      const int64_t pos = base + __popcll(mask & ((1ull << lane) - 1ull));
+      col_idx[pos] = (int32_t)j;
+      values[pos] = v;
+    }
+    base += __popcll(mask);
+  }
+}
+
+// c[i][k] +-= sum_j P(i, j) d[j][k] for k < ncols. A workgroup owns 256
+// consecutive k of one row i. The row's nonzeros are staged in LDS in chunks
+// of CH entries -- copied from compressed rows (STREAM = 0) or drawn from the
+// SPARSE stream of rng over the row's rcols columns (STREAM = 1: each wave
+// appends its nonzeros through an LDS counter; the ring sum does not depend
+// on their order) -- and every thread then runs over the staged entries,
+// which are LDS broadcasts, with several independent loads of d in flight.
+template <int STREAM>
+__global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rcols, const int64_t* row_ptr,
+                                                          const int32_t* col_idx, const uint32_t* values,
+                                                          const uint32_t* d, int64_t ldd, int64_t ncols,
+                                                          uint32_t* c, int64_t ldc, int subtract) {
+  constexpr int CH = 2048;
+  __shared__ int32_t scol[CH];
+  __shared__ uint32_t sval[CH];
+  __shared__ int scount;
+  const int tid = threadIdx.x;
+  const int64_t i = blockIdx.x;
+  const int64_t k = (int64_t)blockIdx.y * 256 + tid;
+  const bool active = k < ncols;
+  const uint32_t* dk = d + (active ? k : 0);
+  const int64_t lo = STREAM ? 0 : row_ptr[i];
+  const int64_t hi = STREAM ? rcols : row_ptr[i + 1];
+  uint32_t acc = 0;
+  for (int64_t base = lo; base < hi; base += CH) {
+    const int64_t end = (base + CH < hi) ? base + CH : hi;
+    int n;
+    if (STREAM) {
+      if (tid == 0) scount = 0;
+      __syncthreads();
+      for (int64_t j0 = base; j0 < end; j0 += 256) {
+        const int64_t j = j0 + tid;
+        uint32_t v = 0;
+        const bool nz = (j < end) && sparse_elem(r, (uint64_t)i * rcols + j, &v);
+        const uint64_t mask = __ballot(nz);
+        const int lane = tid & 63;
+        int wbase = 0;
+        if (lane == 0 && mask) wbase = atomicAdd(&scount, __popcll(mask));
+        wbase = __shfl(wbase, 0);
+        if (nz) {
+          const int pos = wbase + __popcll(mask & ((1ull << lane) - 1ull));
+          scol[pos] = (int32_t)j;
+          sval[pos] = v;
+        }
+      }
+      __syncthreads();
+      n = scount;
+    } else {
+      for (int64_t p = base + tid; p < end; p += 256) {
+        scol[p - base] = col_idx[p];
+        sval[p - base] = values[p];
+      }
+      __syncthreads();
+      n = (int)(end - base);
+    }
+    if (active) {
+      int q = 0;
+      for (; q + 4 <= n; q += 4) {
+        const uint32_t a0 = dk[(int64_t)scol[q] * ldd], a1 = dk[(int64_t)scol[q + 1] * ldd];
+        const uint32_t a2 = dk[(int64_t)scol[q + 2] * ldd], a3 = dk[(int64_t)scol[q + 3] * ldd];
+        acc += sval[q] * a0 + sval[q + 1] * a1 + sval[q + 2] * a2 + sval[q + 3] * a3;
+      }
+      for (; q < n; ++q) acc += sval[q] * dk[(int64_t)scol[q] * ldd];
+    }
+    __syncthreads();                                   // before the next chunk overwrites the staging
+  }
+  if (active) {
+    uint32_t* out = c + i * ldc + k;
+    *out = subtract ? *out - acc : *out + acc;
+  }
+}
+
+// c[m][n] +-= sum_{p in row n} values[p] * d[m][col_idx[p]]. A workgroup owns
+// 32 consecutive n of one row m; eight lanes share each n and split its
+// nonzeros, so a row's entries are read in a few coalesced rounds, then the
+// eight partial sums are combined with lane shuffles.
+__global__ __launch_bounds__(256) void gather_cols_kernel(int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
+                                                          const uint32_t* values, const uint32_t* d, int64_t ldd,
+                                                          uint32_t* c, int64_t ldc, int subtract) {
+  const int64_t m = blockIdx.x;
+  const int sub = threadIdx.x & 7;
+  const int64_t n = (int64_t)blockIdx.y * 32 + (threadIdx.x >> 3);
+  uint32_t acc = 0;
+  if (n < N) {
+    const int64_t p0 = row_ptr[n], p1 = row_ptr[n + 1];
+    const uint32_t* dr = d + m * ldd;
+    for (int64_t p = p0 + sub; p < p1; p += 8) acc += values[p] * dr[col_idx[p]];
+  }
+  acc += __shfl_xor(acc, 4, 8);
+  acc += __shfl_xor(acc, 2, 8);
+  acc += __shfl_xor(acc, 1, 8);
+  if (n < N && sub == 0) {
+    uint32_t* out = c + m * ldc + n;
+    *out = subtract ? *out - acc : *out + acc;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sparse_csr_count(const RngArgs& r, int64_t rows, int64_t cols, int64_t* row_ptr, hipStream_t s) {
+  // per-row counts land in row_ptr[1 ..], then the scan rewrites the array
+  if (rows > 0)
+    hipLaunchKernelGGL(sparse_count_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, r, rows, cols,
+                       row_ptr + 1);
+  hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, row_ptr + 1, rows, row_ptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_csr_fill(const RngArgs& r, int64_t rows, int64_t cols, const int64_t* row_ptr,
+                                  int32_t* col_idx, uint32_t* values, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(sparse_fill_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, r, rows, cols, row_ptr,
+                     col_idx, values);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const int32_t* col_idx,
+                                     const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
+                                     uint32_t* c, int64_t ldc, int subtract, hipStream_t s) {
+  if (rows == 0 || ncols == 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_kernel<0>, dim3((unsigned)rows, (unsigned)((ncols + 255) / 256)), dim3(256), 0, s,
+                     RngArgs{}, (int64_t)0, row_ptr, col_idx, values, d, ldd, ncols, c, ldc, subtract);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_stream_gather_rows(const RngArgs& r, int64_t rows, int64_t rcols, const uint32_t* d,
+                                            int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc, int subtract,
+                                            hipStream_t s) {
+  if (rows == 0 || ncols == 0 || rcols == 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_kernel<1>, dim3((unsigned)rows, (unsigned)((ncols + 255) / 256)), dim3(256), 0, s,
+                     r, rcols, (const int64_t*)nullptr, (const int32_t*)nullptr, (const uint32_t*)nullptr, d, ldd,
+                     ncols, c, ldc, subtract);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
+                                     const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
+                                     int64_t ldc, int subtract, hipStream_t s) {
+  if (M == 0 || N == 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_cols_kernel, dim3((unsigned)M, (unsigned)((N + 31) / 32)), dim3(256), 0, s, N,
+                     row_ptr, col_idx, values, d, ldd, c, ldc, subtract);
+  return hipGetLastError();
+}
+
+}  // namespace mosaic

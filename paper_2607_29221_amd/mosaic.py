@@ -148,6 +148,58 @@ def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digi
                                      y_f32.stride(0) if y_f32 is not None else 0, _stream()), "mosaic_unmask")
 
 
+@dataclass
+class SparseRows:
+    """Compressed rows of a sparse ring matrix (rows x cols) on the device."""
+    row_ptr: torch.Tensor      # int64, rows + 1
+    col_idx: torch.Tensor      # int32, capacity >= nnz
+    values: torch.Tensor       # int32 holding uint32 ring values
+    rows: int
+    cols: int
+
+
+def mosaic_sparse_csr(r: _lib.MosaicRng, rows: int, cols: int, exact: bool = True, device="cuda") -> SparseRows:
+    """Compressed rows of the SPARSE stream matrix of ``r``. With ``exact``
+    the arrays are sized to the nonzero count (one device-to-host read);
+    otherwise to the bound rows * cols (no synchronisation)."""
+    row_ptr = torch.empty(rows + 1, dtype=torch.int64, device=device)
+    _check(_lib.load().mosaic_sparse_csr_count(ctypes.byref(r), rows, cols, row_ptr.data_ptr(), _stream()),
+           "mosaic_sparse_csr_count")
+    cap = int(row_ptr[rows].item()) if exact else rows * cols
+    col_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
+    values = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
+    _check(_lib.load().mosaic_sparse_csr_fill(ctypes.byref(r), rows, cols, row_ptr.data_ptr(), col_idx.data_ptr(),
+                                              values.data_ptr(), _stream()), "mosaic_sparse_csr_fill")
+    return SparseRows(row_ptr, col_idx, values, rows, cols)
+
+
+def mosaic_sparse_gather_rows(p: SparseRows, d: torch.Tensor, ncols: int, c: torch.Tensor,
+                              subtract: bool = False) -> None:
+    """c[i, :ncols] +-= sum_j P[i, j] d[j, :ncols] (P: rows x r sparse)."""
+    _check(_lib.load().mosaic_sparse_gather_rows(p.rows, p.row_ptr.data_ptr(), p.col_idx.data_ptr(),
+                                                 p.values.data_ptr(), d.data_ptr(), d.stride(0), ncols,
+                                                 c.data_ptr(), c.stride(0), 1 if subtract else 0, _stream()),
+           "mosaic_sparse_gather_rows")
+
+
+def mosaic_sparse_stream_gather_rows(r: _lib.MosaicRng, rows: int, rcols: int, d: torch.Tensor, ncols: int,
+                                     c: torch.Tensor, subtract: bool = False) -> None:
+    """c[i, :ncols] +-= sum_j P[i, j] d[j, :ncols], P the rows x rcols SPARSE
+    stream matrix of ``r`` (drawn inside the call)."""
+    _check(_lib.load().mosaic_sparse_stream_gather_rows(ctypes.byref(r), rows, rcols, d.data_ptr(), d.stride(0), ncols,
+                                                        c.data_ptr(), c.stride(0), 1 if subtract else 0, _stream()),
+           "mosaic_sparse_stream_gather_rows")
+
+
+def mosaic_sparse_gather_cols(p: SparseRows, d: torch.Tensor, M: int, c: torch.Tensor,
+                              subtract: bool = False) -> None:
+    """c[m, n] +-= sum_j d[m, j] P[n, j] for m < M, n < P.rows."""
+    _check(_lib.load().mosaic_sparse_gather_cols(M, p.rows, p.row_ptr.data_ptr(), p.col_idx.data_ptr(),
+                                                 p.values.data_ptr(), d.data_ptr(), d.stride(0), c.data_ptr(),
+                                                 c.stride(0), 1 if subtract else 0, _stream()),
+           "mosaic_sparse_gather_cols")
+
+
 def mosaic_count_mismatches(a: torch.Tensor, b: torch.Tensor, count: torch.Tensor) -> None:
     """count[0] = number of entries where the int32 matrices a and b differ
     (same shape; count is a one-element int64 device tensor)."""

@@ -68,9 +68,17 @@ class MaskedWeight:
     a_W (t x N, uniform) for the Y' columns and a_i (t x r_i) for each Q_i,
     and the key c^T = a_W W' + sum_i a_i (M_i ... M_1) (t x K), all held in
     digit layout by the client. One vector misses an error in the top bit
-    with probability 1/2 over Z_{2^32}; t vectors bound that by 2^-t."""
+    with probability 1/2 over Z_{2^32}; t vectors bound that by 2^-t.
 
-    def __init__(self, W: torch.Tensor, params, seed: int, weight_id: int = 0, check_vectors: int = 0):
+    With ``sparse_lpn`` (the default at depth >= 2) the LPN matrices stay sparse on the
+    client: S_{i+1} is kept in compressed rows and multiplied by gathering
+    (U_w at Init W, S_{i+1} Q_i at unmasking), T_{i+1} is compressed per
+    call and gathered into U_a and K_c, so their cost per output follows the
+    nonzero count instead of r_i. The dense products then run over the
+    level-d slot only. Results are identical to the dense path."""
+
+    def __init__(self, W: torch.Tensor, params, seed: int, weight_id: int = 0, check_vectors: int = 0,
+                 sparse_lpn: Optional[bool] = None):
         dev = W.device
         N, K = W.shape
         r = list(params.ranks)
@@ -80,6 +88,8 @@ class MaskedWeight:
         self.slot_levels = [d] + list(range(1, d))            # level of each slot
         self.slot_ranks = [r[lv - 1] for lv in self.slot_levels]
         self.R = sum(padded_k(c) for c in self.slot_ranks)    # padded inner width
+        self.sparse = (True if sparse_lpn is None else bool(sparse_lpn)) and d >= 2
+        self.Rd = padded_k(r[d - 1]) if self.sparse else self.R   # width of the dense products
         U = m.DIST_UNIFORM
         s = seed
 
@@ -108,34 +118,54 @@ class MaskedWeight:
         def nc_dst(i):    # N_1 ... N_i (K x r_i): upper rows of Bx
             return Digits(bx[:K], r[i - 1], slot_col[slot_of[i]])
 
+        # sparse mode: ring words of M_i..M_1 (r_i x K, partner of S_{i+1} in U_w)
+        # and D_i = [(N_1..N_i)^T | J_i^T] (r_i x (K + N), partner of T_{i+1})
+        # for the levels i < d that meet a sparse matrix
+        self.D: dict = {}
+        Mc32: dict = {}
+        if self.sparse:
+            for i in range(1, d):
+                self.D[i] = _ring_empty(r[i - 1], K + N, dev)
+                Mc32[i] = _ring_empty(r[i - 1], K, dev)
+
         NcT: List[Digits] = []                # (N_1 ... N_i)^T (r_i x K)
         for i in range(1, d + 1):
             ri = r[i - 1]
             nct = Digits.empty(ri, K, dev)
+            keep = i in self.D
             if i == 1:
-                m.mosaic_sample(m.rng(s, STREAM_M + 1, weight_id, U), ri, K, out_dig=mc_dst(1))
+                m.mosaic_sample(m.rng(s, STREAM_M + 1, weight_id, U), ri, K, out_dig=mc_dst(1),
+                                out=Mc32[1] if keep else None)
                 m.mosaic_sample(m.rng(s, STREAM_M + 1, weight_id, U, transposed=True), K, ri, out_dig=mct_dst(1))
                 m.mosaic_sample(m.rng(s, STREAM_N + 1, weight_id, U), K, ri, out_dig=nc_dst(1))
-                m.mosaic_sample(m.rng(s, STREAM_N + 1, weight_id, U, transposed=True), ri, K, out_dig=nct)
+                m.mosaic_sample(m.rng(s, STREAM_N + 1, weight_id, U, transposed=True), ri, K, out_dig=nct,
+                                out=self.D[1][:, :K] if keep else None)
             else:
                 rp = r[i - 2]
                 Mi = Digits.empty(ri, rp, dev)                  # M_i (r_i x r_{i-1})
                 NiT = Digits.empty(ri, rp, dev)                 # N_i^T
                 m.mosaic_sample(m.rng(s, STREAM_M + i, weight_id, U), ri, rp, out_dig=Mi)
                 m.mosaic_sample(m.rng(s, STREAM_N + i, weight_id, U, transposed=True), ri, rp, out_dig=NiT)
-                self._product_to_digits(Mi, mct_dst(i - 1), ri, K, rp, mc_dst(i))    # M_i Mc_{i-1}
+                self._product_to_digits(Mi, mct_dst(i - 1), ri, K, rp, mc_dst(i),
+                                        Mc32[i] if keep else None)                      # M_i Mc_{i-1}
                 self._product_to_digits(mct_dst(i - 1), Mi, K, ri, rp, mct_dst(i))   # McT_{i-1} M_i^T
                 self._product_to_digits(nc_dst(i - 1), NiT, K, ri, rp, nc_dst(i))    # Nc_{i-1} N_i
-                self._product_to_digits(NiT, nc_dst(i - 1), ri, K, rp, nct)          # N_i^T Nc_{i-1}^T
+                self._product_to_digits(NiT, nc_dst(i - 1), ri, K, rp, nct,
+                                        self.D[i][:, :K] if keep else None)            # N_i^T Nc_{i-1}^T
             NcT.append(nct)
 
-        # client: Lcat = [L | S_2 | ... | S_d]
-        self.Lcat = Digits.concat(N, self.slot_ranks, dev)
+        # client: Lcat = [L | S_2 | ... | S_d] (sparse mode: L only, S_{i+1} as
+        # compressed rows)
+        self.Lcat = Digits.concat(N, self.slot_ranks[:1] if self.sparse else self.slot_ranks, dev)
         m.mosaic_sample(m.rng(s, STREAM_L, weight_id, U), N, r[d - 1], out_dig=self.Lcat[0])
+        self.S: dict = {}
         for slot, lv in enumerate(self.slot_levels[1:], start=1):
-            m.mosaic_sample(m.rng(s, STREAM_S + lv + 1, weight_id, m.DIST_SPARSE,
-                                  log2_inv_density=params.sparse_log2_inv_density),
-                            N, r[lv - 1], out_dig=self.Lcat[slot])
+            srng = m.rng(s, STREAM_S + lv + 1, weight_id, m.DIST_SPARSE,
+                         log2_inv_density=params.sparse_log2_inv_density)
+            if self.sparse:
+                self.S[lv] = m.mosaic_sparse_csr(srng, N, r[lv - 1], exact=True, device=dev)
+            else:
+                m.mosaic_sample(srng, N, r[lv - 1], out_dig=self.Lcat[slot])
 
         # integrity check vectors (slots of a_Q in the order of Q's columns)
         self.t = int(check_vectors)
@@ -151,8 +181,10 @@ class MaskedWeight:
 
         # U_w = Lcat McTcat^T (= L Mc_d + sum S_{i+1} Mc_i); W' = W + U_w + E_w
         U_w = _ring_empty(N, K, dev)
-        m.mosaic_masked_matmul(self.Lcat[0].whole(self.R), McTcat[0].whole(self.R), N, K, self.R, U_w)
-        del McTcat
+        m.mosaic_masked_matmul(self.Lcat[0].whole(self.Rd), McTcat[0].whole(self.Rd), N, K, self.Rd, U_w)
+        for lv, S in self.S.items():
+            m.mosaic_sparse_gather_rows(S, Mc32[lv], K, U_w)
+        del McTcat, Mc32
         ew = _noise_rng(params, s, STREAM_EW, weight_id)
         Wm = _ring_empty(N, K, dev) if self.t > 0 else None
         m.mosaic_mask(W, U_w, ew, N, K, out=Wm, out_dig=Digits(self.Bext.buf[:N], K))
@@ -177,11 +209,16 @@ class MaskedWeight:
             J = _ring_empty(N, ri, dev)
             m.mosaic_masked_matmul(WE, NcT[lv - 1], N, ri, K, J)
             m.mosaic_mask(None, J, None, N, ri, out_dig=Digits(bx[K:], ri, slot_col[slot_of[lv]]))
+            if lv in self.D:                                  # J_i^T next to (N_1..N_i)^T
+                m.mosaic_masked_matmul(NcT[lv - 1], WE, ri, N, K, self.D[lv][:, K:])
         del WE, NcT
+        self.Bx_dense = Digits(bx, r[d - 1]) if self.sparse else self.Bx
 
     @staticmethod
-    def _product_to_digits(a: Digits, b: Digits, rows: int, cols: int, inner: int, out: Digits) -> None:
-        tmp = _ring_empty(rows, cols, a.buf.device)
+    def _product_to_digits(a: Digits, b: Digits, rows: int, cols: int, inner: int, out: Digits,
+                           words: Optional[torch.Tensor] = None) -> None:
+        """out = digits of a b^T; ``words`` (optional) receives the ring words."""
+        tmp = _ring_empty(rows, cols, a.buf.device) if words is None else words
         m.mosaic_masked_matmul(a, b, rows, cols, inner, tmp)
         m.mosaic_mask(None, tmp, None, rows, cols, out_dig=out)
 
@@ -213,11 +250,21 @@ def init_x(w: MaskedWeight, M: int, call_id: int, buf: CallBuffers) -> None:
     product (E_x is drawn later, inside the mask pass)."""
     p, s, r = w.params, w.seed, list(w.params.ranks)
     m.mosaic_sample(m.rng(s, STREAM_R, call_id, m.DIST_UNIFORM), M, r[w.d - 1], out_dig=buf.rho[0])
-    for slot, lv in enumerate(w.slot_levels[1:], start=1):
-        m.mosaic_sample(m.rng(s, STREAM_T + lv + 1, call_id, m.DIST_SPARSE,
-                              log2_inv_density=p.sparse_log2_inv_density),
-                        M, r[lv - 1], out_dig=buf.rho[slot])
-    m.mosaic_masked_matmul(buf.rho[0].whole(w.R), w.Bx, M, w.K + w.N, w.R, buf.UK)
+    if not w.sparse:
+        for slot, lv in enumerate(w.slot_levels[1:], start=1):
+            m.mosaic_sample(m.rng(s, STREAM_T + lv + 1, call_id, m.DIST_SPARSE,
+                                  log2_inv_density=p.sparse_log2_inv_density),
+                            M, r[lv - 1], out_dig=buf.rho[slot])
+        m.mosaic_masked_matmul(buf.rho[0].whole(w.R), w.Bx, M, w.K + w.N, w.R, buf.UK)
+        return
+    # sparse mode: the level-d slot as a product, then each T_{i+1}^T (M x r_i,
+    # a few nonzeros per token, drawn inside the gather) against
+    # D_i = [(N_1..N_i)^T | J_i^T]
+    m.mosaic_masked_matmul(buf.rho[0].whole(w.Rd), w.Bx_dense.whole(w.Rd), M, w.K + w.N, w.Rd, buf.UK)
+    for lv, D in w.D.items():
+        m.mosaic_sparse_stream_gather_rows(m.rng(s, STREAM_T + lv + 1, call_id, m.DIST_SPARSE,
+                                                 log2_inv_density=p.sparse_log2_inv_density),
+                                           M, r[lv - 1], D, w.K + w.N, buf.UK)
 
 
 def mask(w: MaskedWeight, A: torch.Tensor, call_id: int, buf: CallBuffers) -> None:
@@ -234,13 +281,26 @@ def server(w: MaskedWeight, M: int, buf: CallBuffers) -> None:
 
 def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tensor] = None,
            s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None) -> None:
-    """Online step 5: Y = Y' - K_c - Q Lcat^T (digits of Q first)."""
+    """Online step 5: Y = Y' - K_c - Q Lcat^T (digits of Q first). In sparse
+    mode the product covers the level-d slot (L Q_d) and each S_{i+1} Q_i is
+    subtracted by gathering from Q_i's ring words."""
     r = list(w.params.ranks)
-    for slot, lv in enumerate(w.slot_levels):
+    slots = w.slot_levels[:1] if w.sparse else w.slot_levels
+    for slot, lv in enumerate(slots):
         c0 = w.q_cols[slot]
         m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
-    m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
-                    M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
+    if not w.sparse:
+        m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
+                        M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
+        return
+    m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.Rd), w.Lcat[0].whole(w.Rd),
+                    M, w.N, w.Rd, y=buf.Y)
+    for slot, lv in enumerate(w.slot_levels):
+        if lv in w.S:
+            c0 = w.q_cols[slot]
+            m.mosaic_sparse_gather_cols(w.S[lv], buf.YQ[:, c0: c0 + r[lv - 1]], M, buf.Y, subtract=True)
+    if y_f32 is not None:                    # dequantise the finished result (no product term)
+        m.mosaic_unmask(buf.Y, None, None, None, M, w.N, 0, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
 
 
 def verify(w: MaskedWeight, M: int, buf: CallBuffers) -> torch.Tensor:

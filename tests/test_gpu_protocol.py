@@ -21,7 +21,7 @@ def _check_run(A, W, params, seed, weight_id=1, call_id=2):
     ref = oproto.run(A, W, params, seed, weight_id, call_id)
     Wd = torch.from_numpy(W).cuda()
     Ad = torch.from_numpy(A).cuda()
-    w = gproto.MaskedWeight(Wd, params, seed, weight_id)
+    w = gproto.MaskedWeight(Wd, params, seed, weight_id, sparse_lpn=False)     # dense layout: every factor in Lcat/Bx
     buf = gproto.run_call(w, Ad, call_id)
     torch.cuda.synchronize()
     N, K = W.shape

@@ -1,0 +1,159 @@
+"""Sparse LPN matrices in compressed rows, through the C ABI: the compressed
+form equals the oracle's SPARSE stream matrix exactly, the two gather
+products equal ring products with that matrix, and the protocol in sparse
+mode gives every output of the oracle (and of the dense mode) bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import protocol as oproto
+from oracle import sampling as smp
+from oracle.ring import lift, ring_add, ring_matmul, ring_sub
+from paper_2607_29221_amd import mosaic as m
+from paper_2607_29221_amd import protocol as gproto
+from synthetic_inputs import (PARAMS_D2_SPARSE, PARAMS_D3_SPARSE_SMALL, PARAMS_PAPER_D2_SPARSE, DECODE_KN,
+                              DECODE_M, DECODE_SEED, NoiseSpec, ProtocolParams, int8_operands)
+from tests.gpu_util import to_dev_ring, to_np_u32
+
+pytestmark = pytest.mark.gpu
+
+
+def _dense_from_csr(p: m.SparseRows) -> np.ndarray:
+    rp = p.row_ptr.cpu().numpy()
+    nnz = int(rp[-1])
+    ci = p.col_idx.cpu().numpy()[:nnz]
+    va = p.values.cpu().numpy().view(np.uint32)[:nnz]
+    out = np.zeros((p.rows, p.cols), dtype=np.uint32)
+    for i in range(p.rows):
+        cols = ci[rp[i]:rp[i + 1]]
+        assert np.all(np.diff(cols) > 0)                  # increasing within a row
+        out[i, cols] = va[rp[i]:rp[i + 1]]
+    return out
+
+
+@pytest.mark.parametrize("rows,cols,s", [(5, 1536, 6), (300, 70, 2), (5000, 8, 4), (3, 33, 0), (40, 100, 31),
+                                         (0, 10, 6), (7, 0, 6), (1, 1, 0)])
+@pytest.mark.parametrize("exact", [True, False])
+def test_csr_matches_oracle(rows, cols, s, exact):
+    seed, stream, inst = 99, 0x41, 3
+    p = m.mosaic_sparse_csr(m.rng(seed, stream, inst, m.DIST_SPARSE, log2_inv_density=s), rows, cols, exact=exact)
+    ref = smp.sample_matrix("sparse", rows, cols, seed, stream, inst, log2_inv_density=s)
+    if rows and cols:
+        assert np.array_equal(_dense_from_csr(p), ref)
+    rp = p.row_ptr.cpu().numpy()
+    assert rp[0] == 0 and rp[-1] == np.count_nonzero(ref) if rows else rp[-1] == 0
+    assert np.array_equal(np.diff(rp), np.count_nonzero(ref, axis=1)) if rows else True
+
+
+@pytest.mark.parametrize("subtract", [False, True])
+def test_gather_rows_and_cols(subtract):
+    rng = np.random.default_rng(7)
+    rows, r, ncols, M = 37, 300, 517, 19
+    p = m.mosaic_sparse_csr(m.rng(5, 0x42, 0, m.DIST_SPARSE, log2_inv_density=3), rows, r)
+    P = smp.sample_matrix("sparse", rows, r, 5, 0x42, 0, log2_inv_density=3)
+    D = rng.integers(0, 2 ** 32, (r, ncols), dtype=np.uint32)
+    C0 = rng.integers(0, 2 ** 32, (rows, ncols + 3), dtype=np.uint32)
+    c = to_dev_ring(C0)
+    m.mosaic_sparse_gather_rows(p, to_dev_ring(D), ncols, c, subtract=subtract)
+    prod = ring_matmul(P, D)
+    want = C0.copy()
+    want[:, :ncols] = ring_sub(C0[:, :ncols], prod) if subtract else ring_add(C0[:, :ncols], prod)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_u32(c), want)
+
+    Dm = rng.integers(0, 2 ** 32, (M, r + 5), dtype=np.uint32)       # M x r with ld > r
+    C1 = rng.integers(0, 2 ** 32, (M, rows), dtype=np.uint32)
+    c1 = to_dev_ring(C1)
+    dm = to_dev_ring(Dm)
+    m.mosaic_sparse_gather_cols(p, dm[:, :r], M, c1, subtract=subtract)
+    prod = ring_matmul(Dm[:, :r], P.T)
+    want = ring_sub(C1, prod) if subtract else ring_add(C1, prod)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_u32(c1), want)
+
+
+@pytest.mark.parametrize("rows,r,ncols,s", [(9, 300, 517, 3), (3, 5000, 70, 0), (4, 5000, 300, 6), (1, 1, 1, 0),
+                                            (2, 64, 4096, 31)])
+@pytest.mark.parametrize("subtract", [False, True])
+def test_stream_gather_rows_and_long_rows(rows, r, ncols, s, subtract):
+    """Rows drawn inside the gather, and compressed rows longer than one LDS
+    staging chunk (density 1 over 5000 columns)."""
+    rng = np.random.default_rng(rows * r + ncols)
+    seed, stream, inst = 12, 0x43, 5
+    P = smp.sample_matrix("sparse", rows, r, seed, stream, inst, log2_inv_density=s)
+    D = rng.integers(0, 2 ** 32, (r, ncols), dtype=np.uint32)
+    C0 = rng.integers(0, 2 ** 32, (rows, ncols), dtype=np.uint32)
+    prod = ring_matmul(P, D)
+    want = ring_sub(C0, prod) if subtract else ring_add(C0, prod)
+    rr = m.rng(seed, stream, inst, m.DIST_SPARSE, log2_inv_density=s)
+    c = to_dev_ring(C0)
+    m.mosaic_sparse_stream_gather_rows(rr, rows, r, to_dev_ring(D), ncols, c, subtract=subtract)
+    c2 = to_dev_ring(C0)
+    m.mosaic_sparse_gather_rows(m.mosaic_sparse_csr(rr, rows, r), to_dev_ring(D), ncols, c2, subtract=subtract)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_u32(c), want)
+    assert np.array_equal(to_np_u32(c2), want)
+
+
+@pytest.mark.parametrize("params", [PARAMS_D2_SPARSE, PARAMS_D3_SPARSE_SMALL,
+                                    ProtocolParams(ranks=(128, 64), noise=NoiseSpec("dgauss", 0.5, 4),
+                                                   sparse_log2_inv_density=2)],
+                         ids=["d2", "d3", "d2-dense-lpn-noise"])
+@pytest.mark.parametrize("shape", [(64, 512, 512), (70, 130, 200)], ids=["small", "ragged"])
+def test_sparse_mode_protocol(params, shape):
+    M, K, N = shape
+    A, W = int8_operands(M, K, N, 0)
+    seed = 31337
+    ref = oproto.run(A, W, params, seed, weight_id=1, call_id=2)
+    outs = {}
+    for sparse in (False, True):
+        w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), params, seed, 1, sparse_lpn=sparse)
+        buf = gproto.run_call(w, torch.from_numpy(A).cuda(), 2)
+        torch.cuda.synchronize()
+        outs[sparse] = (to_np_u32(buf.UK), to_np_u32(buf.YQ), buf.Y.cpu().numpy())
+    UK, YQ, Y = outs[True]
+    cs = ref.cs
+    assert np.array_equal(UK[:, :K], ring_sub(cs.U_x, cs.E_x).T)
+    assert np.array_equal(UK[:, K:], cs.K.T)
+    assert np.array_equal(YQ[:, :N], ref.Y_masked.T)
+    assert np.array_equal(Y, lift(ref.Y).T)
+    for a, b in zip(outs[False], outs[True]):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("shape_id", range(len(DECODE_KN)), ids=[f"{k}x{n}" for k, n in DECODE_KN])
+def test_sparse_mode_decode_exact(shape_id):
+    """Decode shapes, depth 2 with ranks (1536, 1024), E = 0, sparse mode:
+    Y equals A W^T exactly for every token count."""
+    K, N = DECODE_KN[shape_id]
+    A, W = int8_operands(max(DECODE_M), K, N, DECODE_SEED)
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + shape_id, shape_id,
+                            sparse_lpn=True)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    for Mi in DECODE_M:
+        buf = gproto.run_call(w, torch.from_numpy(np.ascontiguousarray(A[:Mi])).cuda(), call_id=Mi)
+        torch.cuda.synchronize()
+        assert np.array_equal(buf.Y.cpu().numpy().astype(np.float64), ref[:Mi])
+
+
+def test_sparse_mode_dequantised_output():
+    """Unmasking with dequantisation in sparse mode (gathers, then an
+    elementwise dequantisation) equals the dense mode's fused epilogue."""
+    M, K, N = 40, 256, 200
+    A, W = int8_operands(M, K, N, 3)
+    p = PARAMS_D3_SPARSE_SMALL
+    sr = torch.rand(M, device="cuda") * 1e-3
+    sc = torch.rand(N, device="cuda") * 1e-3
+    outs = []
+    for sparse in (False, True):
+        w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), p, 5, 1, sparse_lpn=sparse)
+        buf = gproto.alloc_call(w, M)
+        gproto.init_x(w, M, 4, buf)
+        gproto.mask(w, torch.from_numpy(A).cuda(), 4, buf)
+        gproto.server(w, M, buf)
+        yf = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        gproto.unmask(w, M, buf, y_f32=yf, s_rows=sr, s_cols=sc)
+        torch.cuda.synchronize()
+        outs.append((buf.Y.cpu().numpy(), yf.cpu().numpy()))
+    assert np.array_equal(outs[0][0], outs[1][0])
+    assert np.array_equal(outs[0][1], outs[1][1])
