@@ -367,6 +367,39 @@ def _shape(name):
     return decoder_linear_shape(name)
 
 
+def run_product_only():
+    """The server product alone (mosaic_masked_matmul) at the prefill server
+    shapes, M = 2048, (N + 1536, K), on uniformly sampled digit operands:
+    the kernel the roofline covers, without the rest of the call (used for
+    counter runs)."""
+    import torch
+
+    from paper_2607_29221_amd import mosaic as m
+    from paper_2607_29221_amd.mosaic import Digits
+    from synthetic_inputs import PREFILL_KN, PREFILL_M
+
+    dev = torch.device("cuda", 0)
+    M, out = PREFILL_M, []
+    for K, N in PREFILL_KN:
+        Np = N + 1536
+        A, B = Digits.empty(M, K, dev), Digits.empty(Np, K, dev)
+        m.mosaic_sample(m.rng(1, 1, 0, m.DIST_UNIFORM), M, K, out_dig=A)
+        m.mosaic_sample(m.rng(1, 2, 0, m.DIST_UNIFORM), Np, K, out_dig=B)
+        C = torch.empty((M, Np), dtype=torch.int32, device=dev)
+        for _ in range(2):
+            m.mosaic_masked_matmul(A, B, M, Np, K, C)
+        e0, e1 = _events(2)
+        e0.record()
+        for _ in range(5):
+            m.mosaic_masked_matmul(A, B, M, Np, K, C)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 5
+        out.append({"K": K, "N_plus_r": Np, "ms": round(ms, 4), "int8_tops": round(20.0 * M * K * Np / ms / 1e9, 1)})
+        del A, B, C
+    return out
+
+
 def run_cpu_baseline():
     """The oracle on a bounded sample of the same workload: 512 tokens x 128
     output columns of the (K, N) = (8192, 8192) shape, full per-call path
@@ -406,6 +439,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--product-only", action="store_true",
+                    help="only time the server ring product on uniform digits (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device three times (scale for HBM byte counters)")
     args = ap.parse_args()
@@ -413,6 +448,10 @@ def main():
         print(f"bench.py measures one GPU: the masked product is benchmarked on a single MI355X "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
+
+    if args.product_only:
+        print(json.dumps({"product_only": run_product_only()}))
+        return
 
     if args.copy_calibration:
         import torch
