@@ -307,17 +307,33 @@ def run_decode(dev):
             for i in range(reps):
                 gp.run_call(ws, Ad, 20_000 + i, bufs)
             e[3].record()
+            # phases of the sparse-mode call: Init X is input independent (it
+            # can run ahead of the token); mask, server and unmask are online
+            ph = _events(4)
+            ph[0].record()
+            for i in range(reps):
+                gp.init_x(ws, M, 30_000 + i, bufs)
+            ph[1].record()
+            for i in range(reps):
+                gp.mask(ws, Ad, 30_000 + i, bufs)
+                gp.server(ws, M, bufs)
+                gp.unmask(ws, M, bufs)
+            ph[2].record()
             torch.cuda.synchronize()
             server_ms = e[0].elapsed_time(e[1]) / reps
             call_ms = e[1].elapsed_time(e[2]) / reps
             call_sparse_ms = e[2].elapsed_time(e[3]) / reps
+            init_x_ms = ph[0].elapsed_time(ph[1]) / reps
+            online_ms = ph[1].elapsed_time(ph[2]) / reps
             Kp = 64 * ((K + 63) // 64)
             byts = 4 * Kp * (M + w.n_out) + 4 * M * w.n_out
             res.append({"K": K, "N": N, "M": M, "server_us": round(server_ms * 1e3, 2),
                         "server_gbs": round(byts / (server_ms * 1e-3) / 1e9, 1),
                         "server_hbm_frac": round(byts / (server_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
                         "call_us": round(call_ms * 1e3, 2),
-                        "call_us_sparse_lpn": round(call_sparse_ms * 1e3, 2)})
+                        "call_us_sparse_lpn": round(call_sparse_ms * 1e3, 2),
+                        "init_x_us_sparse_lpn": round(init_x_ms * 1e3, 2),
+                        "online_us_sparse_lpn": round(online_ms * 1e3, 2)})
         del w, ws
     return res
 
