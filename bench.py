@@ -230,6 +230,44 @@ def run_extras(dev):
     t = e0.elapsed_time(e1) / reps
     res["quantize_4096x8192_us"] = round(t * 1e3, 2)
     res["quantize_gbs"] = round(rows * n * 8 / (t * 1e-3) / 1e9, 1)
+
+    # Pi_Sec-Linear input pass at the decoder shapes: rotation + quantisation
+    # + mask (E_a drawn) as three passes and fused (12 algorithmic bytes per
+    # element: x and U in, digits out)
+    res["secure_input"] = []
+    for n, block, qx in ((8192, 8192, 1997), (28672, 4096, 567)):
+        xs = [torch.randn(rows, n, device=dev) for _ in range(2)]
+        U = torch.randint(-2 ** 31, 2 ** 31 - 1, (rows, n), dtype=torch.int32, device=dev)
+        Dg = Digits.empty(rows, n, dev)
+        y = torch.empty_like(xs[0])
+        q = torch.empty((rows, n), dtype=torch.int32, device=dev)
+        sg = torch.empty(n, dtype=torch.int8, device=dev)
+        m.mosaic_sample_signs(m.rng(3, 0x70, 0, 0), n, sg)
+        nz = m.rng(2, 0x50, 0, m.DIST_DGAUSS, sigma=0.5, bound=4)
+
+        def separate(i):
+            m.mosaic_hadamard_rotate(xs[i % 2], y, block=block, signs=sg)
+            m.mosaic_quantize_rows(y, qx, q=q, scale=sc)
+            m.mosaic_mask(q, U, nz, rows, n, out_dig=Dg)
+
+        def fused(i):
+            m.mosaic_rotate_quantize_mask(xs[i % 2], qx, Dg, block=block, signs=sg, u=U, noise=nz, scale=sc)
+
+        ts = []
+        for fn in (separate, fused):
+            for i in range(2):
+                fn(i)
+            e0, e1 = _events(2)
+            e0.record()
+            for i in range(10):
+                fn(i)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / 10)
+        res["secure_input"].append({"rows": rows, "n": n, "block": block, "separate_us": round(ts[0] * 1e3, 1),
+                                    "fused_us": round(ts[1] * 1e3, 1),
+                                    "fused_gbs": round(rows * n * 12 / (ts[1] * 1e-3) / 1e9, 1)})
+        del xs, U, Dg, y, q
     return res
 
 

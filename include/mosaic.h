@@ -169,6 +169,25 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy,
                             const float* s_rows, const float* s_cols,
                             float* y_f32, int64_t ldf, void* stream);
 
+/* Fused client input pass of Pi_Sec-Linear (Section 5 protocol box, online
+ * step 1, then the mask of the Section 4.2 box, online step 2): for every row
+ * of x (rows x n fp32, ldx), in one pass,
+ *     y = forward rotation of mosaic_hadamard_rotate (block, signs),
+ *     s = max_j |y_j| / qmax (1 for an all-zero row), q = round-half-even(y / s),
+ *     A' = q + u + noise (mod 2^32), written as digits (out_dig, dig_pitch),
+ * and scale[i] = s (scale is required; it also holds max |y| between the
+ * call's two launches). The result is bit-identical to
+ * mosaic_hadamard_rotate, mosaic_quantize_rows (int32 codes) and mosaic_mask
+ * (x = the codes, u, noise) called in sequence. u (rows x n uint32, ldu) and
+ * noise may be NULL. Requirements: block = 2^k with 10 <= k <= 14, n a
+ * multiple of block, x and u 16-byte aligned with ldx, ldu multiples of 4,
+ * noise not transposed; otherwise MOSAIC_ERR_UNSUPPORTED (the three calls
+ * above remain available). */
+mosaic_status mosaic_rotate_quantize_mask(const float* x, int64_t ldx, int64_t rows, int64_t n, int64_t block,
+                                          const int8_t* signs, int32_t qmax, const uint32_t* u, int64_t ldu,
+                                          const mosaic_rng* noise, int8_t* out_dig, int64_t dig_pitch,
+                                          float* scale, void* stream);
+
 /* Sparse LPN matrices in compressed-row form (Section 4.2 protocol box:
  * S_{i+1} and T_{i+1} are sparse with noise rate 2^-s; the client's products
  * with them then cost O(nonzeros) per output row, Section 4.2 cost analysis

@@ -44,6 +44,8 @@ _SIGNATURES = {
     "mosaic_unmask": ([c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64,
                        c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
     "mosaic_sample_signs": ([ctypes.POINTER(MosaicRng), c_i64, c_ptr, c_ptr], c_i32),
+    "mosaic_rotate_quantize_mask": ([c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr, c_i64,
+                                     ctypes.POINTER(MosaicRng), c_ptr, c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_count_mismatches": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_sparse_csr_count": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_sparse_csr_fill": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_ptr, c_ptr, c_ptr], c_i32),

@@ -219,6 +219,39 @@ mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch, const i
   return hip_status(launch_ring_gemm(g, EPI_STORE, (hipStream_t)stream), "ring product launch");
 }
 
+mosaic_status mosaic_rotate_quantize_mask(const float* x, int64_t ldx, int64_t rows, int64_t n, int64_t block,
+                                          const int8_t* signs, int32_t qmax, const uint32_t* u, int64_t ldu,
+                                          const mosaic_rng* noise, int8_t* out_dig, int64_t dig_pitch,
+                                          float* scale, void* stream) {
+  if (rows < 0 || n < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || n == 0) return MOSAIC_OK;
+  if (qmax < 1) return fail(MOSAIC_ERR_INVALID_ARG, "qmax must be >= 1");
+  if (x == nullptr || out_dig == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "x or out_dig is NULL");
+  int lg = 0;
+  while (lg < 62 && (int64_t(1) << lg) < block) ++lg;
+  if (block <= 0 || (int64_t(1) << lg) != block) return fail(MOSAIC_ERR_INVALID_ARG, "block must be a power of two");
+  if (n % block != 0) return fail(MOSAIC_ERR_INVALID_ARG, "n must be a multiple of block");
+  if (!rotate_quantize_mask_supported(lg)) return fail(MOSAIC_ERR_UNSUPPORTED, "block outside [2^10, 2^14]");
+  if (scale == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "scale is NULL");
+  if (ldx < n || (ldx & 3) != 0 || ((uintptr_t)x & 15) != 0)
+    return fail(MOSAIC_ERR_UNSUPPORTED, "x must be 16-byte aligned with ldx >= n, a multiple of 4");
+  if (u != nullptr && (ldu < n || (ldu & 3) != 0 || ((uintptr_t)u & 15) != 0))
+    return fail(MOSAIC_ERR_UNSUPPORTED, "u must be 16-byte aligned with ldu >= n, a multiple of 4");
+  mosaic_status st = check_digits(out_dig, dig_pitch, rows, n, "out_dig");
+  if (st != MOSAIC_OK) return st;
+  if (((uintptr_t)out_dig & 15) != 0) return fail(MOSAIC_ERR_UNSUPPORTED, "out_dig must be 16-byte aligned");
+  RngArgs na{};
+  if (noise != nullptr) {
+    if (noise->transposed) return fail(MOSAIC_ERR_UNSUPPORTED, "transposed noise");
+    st = rng_args(noise, &na);
+    if (st != MOSAIC_OK) return st;
+  }
+  if (rows > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  return hip_status(launch_rotate_quantize_mask(x, ldx, rows, n, lg, signs, qmax, u, ldu,
+                                                noise != nullptr ? &na : nullptr, out_dig, dig_pitch, scale,
+                                                (hipStream_t)stream), "rotate-quantize-mask launch");
+}
+
 mosaic_status mosaic_sparse_csr_count(const mosaic_rng* rng, int64_t rows, int64_t cols, int64_t* row_ptr,
                                       void* stream) {
   if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");

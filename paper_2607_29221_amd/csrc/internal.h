@@ -176,6 +176,13 @@ hipError_t launch_hadamard(const float* x, int64_t ldx, float* y, int64_t ldy, i
                            int64_t n, int log2_block, const int8_t* signs, int inverse,
                            hipStream_t s);
 
+// Fused rotate + quantise + mask of Pi_Sec-Linear's input (secure_input.hip).
+bool rotate_quantize_mask_supported(int log2_block);
+hipError_t launch_rotate_quantize_mask(const float* x, int64_t ldx, int64_t rows, int64_t n, int log2_block,
+                                       const int8_t* signs, int32_t qmax, const uint32_t* u, int64_t ldu,
+                                       const RngArgs* noise, int8_t* out_dig, int64_t pitch, float* scale,
+                                       hipStream_t s);
+
 hipError_t launch_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64_t n, int32_t qmax,
                                 int32_t* q, int64_t ldq, int8_t* q_dig, int64_t q_pitch,
                                 float* scale, hipStream_t s);

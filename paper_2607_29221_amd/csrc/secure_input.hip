@@ -1,0 +1,137 @@
+// Client input pass of Pi_Sec-Linear (Section 5 protocol box, online step 1,
+// followed by the mask of the Section 4.2 protocol box, online step 2) fused
+// into one kernel: for every token row x (n floats)
+//   1. rotate blockwise, y = H_b (d * x) / sqrt(b)   (b = 2^LOGB, n = k b);
+//   2. quantise, s = max_j |y_j| / q_max (1 for an all-zero row),
+//      q_j = round-half-even(y_j / s);
+//   3. mask, A'_j = q_j + U_j + E_j over Z_{2^32}, E drawn in the pass;
+//   4. write A' as digits, and s.
+// It performs exactly the arithmetic of mosaic_hadamard_rotate,
+// mosaic_quantize_rows and mosaic_mask in sequence (same butterfly order,
+// same fp32 scale and division, same noise element indices), so the digits
+// are bit-identical to that sequence, with 16 bytes of HBM traffic per
+// element instead of 28 for the three passes.
+//
+// Two launches, one workgroup per row each, with only the block transform's
+// scratch in LDS (so occupancy is that of the plain rotation): the first
+// rotates the row block by block and keeps only max |y| (written to
+// scale[row]); the second rotates again -- the butterflies are cheap next to
+// the memory traffic -- quantises with s = max / q_max, adds u and the noise
+// and writes the digits, then replaces scale[row] by s. HBM traffic: x twice,
+// u once, digits once (16 bytes per element).
+#include "fwht_block.h"
+
+namespace mosaic {
+namespace {
+
+template <int LOGB>
+__device__ __forceinline__ float block_max(float m, float* red) {
+  constexpr int T = FwhtShape<LOGB>::T;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int w = 1; w < T / 64; ++w) r = fmaxf(r, red[w]);
+  return r;
+}
+
+template <int LOGB>
+__global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float* __restrict__ x, int64_t ldx,
+                                                                     int64_t n, const int8_t* __restrict__ signs,
+                                                                     float scale_b, float* amax_out) {
+  using S = FwhtShape<LOGB>;
+  constexpr int E = S::E, B = S::B;
+  static_assert(S::T == 256, "four full waves per workgroup");
+  __shared__ float sm[S::SM];
+  __shared__ float red[S::T / 64];
+  const int64_t row = blockIdx.x;
+  const float* xr = x + row * ldx;
+  float m = 0.0f;
+  for (int64_t blk = 0; blk < n / B; ++blk) {
+    float v[E];
+    fwht_block<LOGB>(xr + blk * B, signs ? signs + blk * B : nullptr, true, sm, v);
+#pragma unroll
+    for (int r = 0; r < E; ++r) m = fmaxf(m, fabsf(v[r] * scale_b));
+    __syncthreads();                // the next block reuses the scratch
+  }
+  const float amax = block_max<LOGB>(m, red);
+  if (threadIdx.x == 0) amax_out[row] = amax;
+}
+
+template <int LOGB>
+__global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_mask_kernel(
+    const float* __restrict__ x, int64_t ldx, int64_t n, const int8_t* __restrict__ signs, float scale_b,
+    int32_t qmax, const uint32_t* __restrict__ u, int64_t ldu, int32_t has_noise, RngArgs noise, int8_t* out_dig,
+    int64_t pitch, float* scale) {
+  using S = FwhtShape<LOGB>;
+  constexpr int T = S::T, E = S::E, NV = S::NV, B = S::B;
+  __shared__ float sm[S::SM];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const float* xr = x + row * ldx;
+  const float amax = scale[row];    // written by rqm_max_kernel
+  const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
+  for (int64_t blk = 0; blk < n / B; ++blk) {
+    float v[E];
+    fwht_block<LOGB>(xr + blk * B, signs ? signs + blk * B : nullptr, true, sm, v);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      // columns 4 c .. 4 c + 3 of the row; lanes t .. t + 3 hold one 16-column group
+      const int64_t c = blk * (B / 4) + t + T * k;
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)(int32_t)rintf((v[4 * k + q] * scale_b) / s);
+      if (u != nullptr) {
+        const uint4 uu = *(const uint4*)(u + row * ldu + 4 * c);
+        w[0] += uu.x; w[1] += uu.y; w[2] += uu.z; w[3] += uu.w;
+      }
+      if (has_noise) {
+        uint32_t e[4];
+        sample4_aligned(noise, (uint64_t)row * (uint64_t)n + (uint64_t)(4 * c), e);
+        w[0] += e[0]; w[1] += e[1]; w[2] += e[2]; w[3] += e[3];
+      }
+      uint32_t o[4];
+      quad_digit_planes(w, t & 3, o);
+      *(uint4*)(out_dig + row * pitch + 16 * c) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+    __syncthreads();                // the next block reuses the scratch
+  }
+  if (t == 0) scale[row] = s;       // every thread read the maximum before the first barrier
+}
+
+template <int LOGB>
+hipError_t launch_rqm(const float* x, int64_t ldx, int64_t rows, int64_t n, const int8_t* signs, int32_t qmax,
+                      const uint32_t* u, int64_t ldu, const RngArgs* noise, int8_t* out_dig, int64_t pitch,
+                      float* scale, hipStream_t s) {
+  using S = FwhtShape<LOGB>;
+  const float scale_b = (float)(1.0 / sqrt((double)S::B));
+  hipLaunchKernelGGL(rqm_max_kernel<LOGB>, dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, n, signs, scale_b,
+                     scale);
+  hipLaunchKernelGGL(rqm_mask_kernel<LOGB>, dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, n, signs, scale_b,
+                     qmax, u, ldu, noise != nullptr ? 1 : 0, noise != nullptr ? *noise : RngArgs{}, out_dig, pitch,
+                     scale);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool rotate_quantize_mask_supported(int log2_block) { return log2_block >= 10 && log2_block <= 14; }
+
+hipError_t launch_rotate_quantize_mask(const float* x, int64_t ldx, int64_t rows, int64_t n, int log2_block,
+                                       const int8_t* signs, int32_t qmax, const uint32_t* u, int64_t ldu,
+                                       const RngArgs* noise, int8_t* out_dig, int64_t pitch, float* scale,
+                                       hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  switch (log2_block) {
+    case 10: return launch_rqm<10>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+    case 11: return launch_rqm<11>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+    case 12: return launch_rqm<12>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+    case 13: return launch_rqm<13>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+    case 14: return launch_rqm<14>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace mosaic

@@ -21,6 +21,7 @@ from . import _lib
 
 DIST_ZERO, DIST_UNIFORM, DIST_DGAUSS, DIST_SPARSE = 0, 1, 2, 3
 DT_I8, DT_I16, DT_I32, DT_U32 = 0, 1, 2, 3
+STATUS_OK, STATUS_INVALID_ARG, STATUS_UNSUPPORTED, STATUS_HIP = 0, -1, -2, -3
 _TORCH_DT = {torch.int8: DT_I8, torch.int16: DT_I16, torch.int32: DT_I32}
 
 
@@ -146,6 +147,20 @@ def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digi
                                      _ptr(y), y.stride(0) if y is not None else 0,
                                      _ptr(s_rows), _ptr(s_cols), _ptr(y_f32),
                                      y_f32.stride(0) if y_f32 is not None else 0, _stream()), "mosaic_unmask")
+
+
+def mosaic_rotate_quantize_mask(x: torch.Tensor, qmax: int, out_dig: Digits, block: Optional[int] = None,
+                                signs: Optional[torch.Tensor] = None, u: Optional[torch.Tensor] = None,
+                                noise: Optional[_lib.MosaicRng] = None,
+                                scale: Optional[torch.Tensor] = None) -> None:
+    """Fused rotate + quantise + mask of Pi_Sec-Linear's input: digits of
+    round(R x / s) + u + noise for every row of x, and the row scales."""
+    rows, n = x.shape
+    _check(_lib.load().mosaic_rotate_quantize_mask(x.data_ptr(), x.stride(0), rows, n, n if block is None else block,
+                                                   _ptr(signs), qmax, _ptr(u), u.stride(0) if u is not None else 0,
+                                                   ctypes.byref(noise) if noise is not None else None,
+                                                   out_dig.ptr, out_dig.pitch, _ptr(scale), _stream()),
+           "mosaic_rotate_quantize_mask")
 
 
 @dataclass

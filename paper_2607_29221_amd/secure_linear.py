@@ -77,6 +77,7 @@ class SecureLinear:
         self.last_codes: Optional[torch.Tensor] = None
         self.last_scales: Optional[torch.Tensor] = None
         self.last_buf: Optional[gp.CallBuffers] = None
+        self.fused = True                   # fused input pass when the shape allows
 
     def quantize_activations(self, x: torch.Tensor):
         """Rotated, quantised activations: (codes int32 M x K, scales M)."""
@@ -89,13 +90,31 @@ class SecureLinear:
         return codes, s_x
 
     def __call__(self, x: torch.Tensor, call_id: int, keep_codes: bool = False) -> torch.Tensor:
+        """Online phase. The rotation, quantisation and mask run as one fused
+        pass (mosaic_rotate_quantize_mask) unless the codes are to be kept or
+        the shape is outside what the fused kernel takes, in which case the
+        three passes run in sequence; both give the same bits."""
         if x.dtype != torch.float32 or x.dim() != 2 or x.shape[1] != self.K or not x.is_contiguous():
             raise ValueError("x must be a contiguous float32 tensor (M x K)")
         M = x.shape[0]
-        codes, s_x = self.quantize_activations(x)
         buf = gp.alloc_call(self.w, M, x.device)
         gp.init_x(self.w, M, call_id, buf)
-        gp.mask(self.w, codes, call_id, buf)
+        codes = None
+        done = False
+        if self.fused and not keep_codes:
+            s_x = torch.empty(M, dtype=torch.float32, device=x.device)
+            try:
+                m.mosaic_rotate_quantize_mask(x, self.q_x, buf.A_masked, block=self.block, signs=self.signs,
+                                              u=buf.UK[:, : self.K],
+                                              noise=gp._noise_rng(self.w.params, self.w.seed, gp.STREAM_EX, call_id),
+                                              scale=s_x)
+                done = True
+            except m.MosaicError as err:
+                if err.status != m.STATUS_UNSUPPORTED:
+                    raise
+        if not done:
+            codes, s_x = self.quantize_activations(x)
+            gp.mask(self.w, codes, call_id, buf)
         gp.server(self.w, M, buf)
         y = torch.empty((M, self.N), dtype=torch.float32, device=x.device)
         gp.unmask(self.w, M, buf, y_f32=y, s_rows=s_x, s_cols=self.s_w)

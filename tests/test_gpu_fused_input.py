@@ -1,0 +1,76 @@
+"""Fused rotate + quantise + mask of Pi_Sec-Linear's input against the
+three separate passes (rotation, quantisation, mask) through the C ABI:
+digits and scales are bit-identical, and shapes outside the fused kernel's
+limits are refused with MOSAIC_ERR_UNSUPPORTED."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_29221_amd import mosaic as m
+from paper_2607_29221_amd import protocol as gproto
+from paper_2607_29221_amd.mosaic import Digits
+from paper_2607_29221_amd.secure_linear import SecureLinear
+from synthetic_inputs import PARAMS_PAPER_D1, decoder_weight, outlier_activations
+from tests.gpu_util import digits_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _separate(x, block, signs, qmax, u, noise):
+    rows, n = x.shape
+    y = torch.empty_like(x)
+    m.mosaic_hadamard_rotate(x, y, block=block, signs=signs)
+    q = torch.empty((rows, n), dtype=torch.int32, device="cuda")
+    sc = torch.empty(rows, dtype=torch.float32, device="cuda")
+    m.mosaic_quantize_rows(y, qmax, q=q, scale=sc)
+    d = Digits.empty(rows, n)
+    m.mosaic_mask(q, u, noise, rows, n, out_dig=d)
+    return d, sc
+
+
+@pytest.mark.parametrize("rows,n,block,qmax", [(5, 8192, 8192, 1997), (3, 28672, 4096, 567), (4, 1024, 1024, 300),
+                                               (2, 16384, 16384, 1000), (3, 3072, 1024, 127), (2, 32768, 4096, 511),
+                                               (2, 36864, 4096, 400)])
+@pytest.mark.parametrize("with_u,with_noise", [(True, True), (False, False), (True, False)])
+def test_fused_matches_separate_passes(rows, n, block, qmax, with_u, with_noise):
+    x = torch.from_numpy(outlier_activations(rows, n, rows + n)).cuda()
+    x[1] = 0.0                                                     # all-zero row: scale 1
+    signs = torch.empty(n, dtype=torch.int8, device="cuda")
+    m.mosaic_sample_signs(m.rng(17, gproto.STREAM_SIGNS, 2, 0), n, signs)
+    u = None
+    if with_u:
+        u = torch.empty((rows, n + 4), dtype=torch.int32, device="cuda")[:, :n]
+        m.mosaic_sample(m.rng(18, 0x51, 0, m.DIST_UNIFORM), rows, n, out=u)
+    noise = m.rng(19, gproto.STREAM_EX, 4, m.DIST_DGAUSS, sigma=0.5, bound=4) if with_noise else None
+    d_ref, s_ref = _separate(x, block, signs, qmax, u, noise)
+    d = Digits.empty(rows, n)
+    d.buf.fill_(0x33)
+    sc = torch.empty(rows, dtype=torch.float32, device="cuda")
+    m.mosaic_rotate_quantize_mask(x, qmax, d, block=block, signs=signs, u=u, noise=noise, scale=sc)
+    torch.cuda.synchronize()
+    assert np.array_equal(sc.cpu().numpy(), s_ref.cpu().numpy())
+    assert np.array_equal(digits_np(d), digits_np(d_ref))
+
+
+@pytest.mark.parametrize("n,block", [(1024, 512), (4096, 256), (32768, 32768)])
+def test_fused_refuses_unsupported_shapes(n, block):
+    x = torch.zeros((2, n), dtype=torch.float32, device="cuda")
+    d = Digits.empty(2, n)
+    with pytest.raises(m.MosaicError) as e:
+        m.mosaic_rotate_quantize_mask(x, 127, d, block=block)
+    assert e.value.status == m.STATUS_UNSUPPORTED
+
+
+def test_secure_linear_fused_equals_separate():
+    """A Pi_Sec-Linear call (fused QKV of the decoder stack, 512 tokens) gives
+    the same output bits with the fused input pass and with the three
+    separate passes."""
+    dev = torch.device("cuda", 0)
+    W = decoder_weight(0, "qkv", dev)
+    lin = SecureLinear(W, PARAMS_PAPER_D1, 0x5EC, weight_id=0)
+    x = torch.randn((512, W.shape[1]), generator=torch.Generator(device=dev).manual_seed(3), device=dev)
+    y_fused = lin(x, call_id=5)
+    lin.fused = False
+    y_sep = lin(x, call_id=5)
+    torch.cuda.synchronize()
+    assert np.array_equal(y_fused.cpu().numpy(), y_sep.cpu().numpy())
