@@ -140,6 +140,7 @@ def run_gpu(steps: int, warmup: int, extras: bool):
         out["extras"]["decode"] = run_decode(dev)
         out["extras"]["decoder_stack"] = run_decoder_stack(dev)
         out["extras"]["integrity_check"] = run_integrity(dev)
+        out["extras"]["matvec_sweep"] = run_matvec_sweep(dev)
     return out
 
 
@@ -301,6 +302,53 @@ def run_integrity(dev):
         sv, ck = e[0].elapsed_time(e[1]) / reps, e[1].elapsed_time(e[2]) / reps
         out.append({"K": K, "N": N, "vectors": t, "honest_call_accepted": ok, "check_ms": round(ck, 4),
                     "server_ms": round(sv, 4), "check_over_server": round(ck / sv, 4)})
+        del w, buf
+    return out
+
+
+def run_matvec_sweep(dev):
+    """One secure matrix-vector product (one token, W' n x n) for
+    n in {4096, 8192, 16384, 36864}, depth-1 mask of rank 1536 with sigma =
+    0.5: the server product ([Y' | Q]), the client's online steps (mask and
+    unmask) and the input-independent Init X, HIP-event means over 20 calls.
+    The paper reports the same split for its own implementation (context
+    only: other hardware and design)."""
+    import torch
+
+    from paper_2607_29221_amd import protocol as gp
+    from synthetic_inputs import MATVEC_N, MATVEC_SEED, PARAMS_PAPER_D1, int8_matrix_device
+
+    out, reps = [], 20
+    for n in MATVEC_N:
+        W = int8_matrix_device(n, n, MATVEC_SEED, dev)
+        A = int8_matrix_device(1, n, MATVEC_SEED + 1, dev)
+        w = gp.MaskedWeight(W, PARAMS_PAPER_D1, 0x6D6F736169630000 | MATVEC_SEED, weight_id=0)
+        del W
+        buf = gp.alloc_call(w, 1, dev)
+        for i in range(3):
+            gp.run_call(w, A, 100 + i, buf)
+        torch.cuda.synchronize()
+        e = _events(5)
+        e[0].record()
+        for i in range(reps):
+            gp.init_x(w, 1, 200 + i, buf)
+        e[1].record()
+        for i in range(reps):
+            gp.mask(w, A, 200 + i, buf)
+        e[2].record()
+        for i in range(reps):
+            gp.server(w, 1, buf)
+        e[3].record()
+        for i in range(reps):
+            gp.unmask(w, 1, buf)
+        e[4].record()
+        torch.cuda.synchronize()
+        t = [e[k].elapsed_time(e[k + 1]) / reps for k in range(4)]
+        Kp = 64 * ((n + 63) // 64)
+        byts = 4 * Kp * (1 + w.n_out) + 4 * w.n_out
+        out.append({"n": n, "server_ms": round(t[2], 4), "server_gbs": round(byts / (t[2] * 1e-3) / 1e9, 1),
+                    "client_online_ms": round(t[1] + t[3], 4), "init_x_ms": round(t[0], 4),
+                    "total_ms": round(sum(t), 4)})
         del w, buf
     return out
 

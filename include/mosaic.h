@@ -145,7 +145,9 @@ mosaic_status mosaic_mask(const void* x, int32_t x_dtype, int64_t x_rs, int64_t 
  * limbs): C = A B^T over Z_{2^32}.
  * A: M x K digits (pitch a_pitch); B: N x K digits (pitch b_pitch);
  * C: M x N uint32, leading dimension ldc >= N. Stacking the rows of
- * M_i ... M_1 under W' in B returns [Y' | Q] from one call. */
+ * M_i ... M_1 under W' in B returns [Y' | Q] from one call. Any K: inner
+ * dimensions of 2^15 and more run as chunks whose partial products are
+ * added into C (each chunk keeps the int32 shift-class sums exact). */
 mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch,
                                    const int8_t* b_dig, int64_t b_pitch,
                                    int64_t M, int64_t N, int64_t K,

@@ -196,7 +196,6 @@ mosaic_status mosaic_sample_signs(const mosaic_rng* rng, int64_t n, int8_t* out,
 mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch, const int8_t* b_dig, int64_t b_pitch,
                                    int64_t M, int64_t N, int64_t K, uint32_t* c, int64_t ldc, void* stream) {
   if (M < 0 || N < 0 || K < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
-  if (K >= 32768) return fail(MOSAIC_ERR_UNSUPPORTED, "K = %lld: the int32 shift-class accumulators need K < 32768", (long long)K);
   if (M == 0 || N == 0) return MOSAIC_OK;
   if (c == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "c is NULL");
   if (ldc < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldc < N");
@@ -213,10 +212,24 @@ mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch, const i
   g.b_pitch = b_pitch;
   g.M = M;
   g.N = N;
-  g.Kp = padded_k(K);
   g.c = c;
   g.ldc = ldc;
-  return hip_status(launch_ring_gemm(g, EPI_STORE, (hipStream_t)stream), "ring product launch");
+  // Inner chunks of at most MAX_K_CHUNK columns (digit columns are contiguous
+  // along a row, so a chunk at column k0 starts 4 k0 bytes in): the first
+  // stores, the others add.
+  const int64_t Kp = padded_k(K);
+  int64_t k0 = 0;
+  do {
+    const int64_t kc = (Kp - k0 < MAX_K_CHUNK) ? Kp - k0 : MAX_K_CHUNK;
+    g.a = a_dig + 4 * k0;
+    g.b = b_dig + 4 * k0;
+    g.Kp = kc;
+    const mosaic_status ls = hip_status(launch_ring_gemm(g, k0 == 0 ? EPI_STORE : EPI_ACCUM, (hipStream_t)stream),
+                                        "ring product launch");
+    if (ls != MOSAIC_OK) return ls;
+    k0 += kc;
+  } while (k0 < Kp);
+  return MOSAIC_OK;
 }
 
 mosaic_status mosaic_rotate_quantize_mask(const float* x, int64_t ldx, int64_t rows, int64_t n, int64_t block,

@@ -44,7 +44,13 @@ hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_
                                    int64_t cols, int64_t* count, hipStream_t s);
 
 // Ring product C = A B^T with an epilogue.
-enum EpilogueKind { EPI_STORE = 0, EPI_UNMASK = 1 };
+// EPI_ACCUM adds the product to c (c += A B^T over the ring): long inner
+// dimensions are split into chunks that each fit the int32 accumulators.
+enum EpilogueKind { EPI_STORE = 0, EPI_UNMASK = 1, EPI_ACCUM = 2 };
+
+// Inner-dimension chunk of one launch: the four-product shift class
+// accumulates 4 K 2^14 < 2^31 only for K < 2^15; a multiple of 64.
+constexpr int64_t MAX_K_CHUNK = 32704;
 struct GemmLaunch {
   const int8_t* a;
   int64_t a_pitch;
@@ -80,6 +86,8 @@ template <int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmLaunch& g, int64_t m, int64_t n, uint32_t val) {
   if (EPI == EPI_STORE) {
     g.c[m * g.ldc + n] = val;
+  } else if (EPI == EPI_ACCUM) {
+    g.c[m * g.ldc + n] += val;
   } else {
     uint32_t y = g.ym[m * g.ldy + n] - val;
     if (g.kc != nullptr) y -= g.kc[m * g.ldk + n];
@@ -94,7 +102,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmLaunch& g, int64_t m, in
 inline bool gemm_epilogue_vectorizable(const GemmLaunch& g, EpilogueKind epi) {
   auto ok = [](const void* p, int64_t ld) { return p == nullptr || ((((uintptr_t)p) & 15) == 0 && (ld & 3) == 0); };
   if (g.N % 4 != 0) return false;
-  if (epi == EPI_STORE) return ok(g.c, g.ldc);
+  if (epi == EPI_STORE || epi == EPI_ACCUM) return ok(g.c, g.ldc);
   return ok(g.ym, g.ldy) && ok(g.kc, g.ldk) && ok(g.y, g.ldo) && ok(g.y_f32, g.ldf) &&
          (g.y_f32 == nullptr || (((uintptr_t)g.s_cols) & 15) == 0);
 }
@@ -132,6 +140,27 @@ __device__ __forceinline__ void gemm_tile_epilogue(const GemmLaunch& g, const ui
       const int64_t n = n0 + 4 * (c % CPR);
       if (m < g.M && n < g.N)
         *(uint4*)(g.c + m * g.ldc + n) = *(const uint4*)(tile + r * TROW + 4 * (c % CPR));
+    }
+    return;
+  }
+  if (EPI == EPI_ACCUM) {
+    uint4 cv[PER];                                  // every c chunk is read before the first store
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + NT * k;
+      const int64_t m = min(m0 + c / CPR, g.M - 1);
+      const int64_t n = min(n0 + 4 * (c % CPR), g.N - 4);
+      cv[k] = *(const uint4*)(g.c + m * g.ldc + n);
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + NT * k;
+      const int r = c / CPR;
+      const int64_t m = m0 + r;
+      const int64_t n = n0 + 4 * (c % CPR);
+      if (m >= g.M || n >= g.N) continue;
+      const uint4 a = *(const uint4*)(tile + r * TROW + 4 * (c % CPR));
+      *(uint4*)(g.c + m * g.ldc + n) = make_uint4(cv[k].x + a.x, cv[k].y + a.y, cv[k].z + a.z, cv[k].w + a.w);
     }
     return;
   }

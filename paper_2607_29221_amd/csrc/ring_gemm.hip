@@ -295,6 +295,9 @@ hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s
   if (epi == EPI_STORE) {
     if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 1>), grid, dim3(NTHREADS), 0, s, g);
     else hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 0>), grid, dim3(NTHREADS), 0, s, g);
+  } else if (epi == EPI_ACCUM) {
+    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 1>), grid, dim3(NTHREADS), 0, s, g);
+    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 0>), grid, dim3(NTHREADS), 0, s, g);
   } else {
     if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 1>), grid, dim3(NTHREADS), 0, s, g);
     else hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 0>), grid, dim3(NTHREADS), 0, s, g);

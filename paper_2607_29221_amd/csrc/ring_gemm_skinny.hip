@@ -215,7 +215,9 @@ hipError_t launch_epi(const GemmLaunch& g, hipStream_t s) {
 
 hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  return epi == EPI_STORE ? launch_epi<EPI_STORE>(g, s) : launch_epi<EPI_UNMASK>(g, s);
+  if (epi == EPI_STORE) return launch_epi<EPI_STORE>(g, s);
+  if (epi == EPI_ACCUM) return launch_epi<EPI_ACCUM>(g, s);
+  return launch_epi<EPI_UNMASK>(g, s);
 }
 
 }  // namespace mosaic

@@ -161,3 +161,17 @@ def int_codes(rows: int, cols: int, qmax: int, seed: int) -> np.ndarray:
 # output projection is the (8192, 8192) prefill shape).
 DECODER_RING_KN: List[Tuple[int, int]] = [(8192, 10240), (8192, 57344), (28672, 8192)]
 DECODER_RING_SEED = 5
+
+
+# Secure mat-vec sweep (one token, square weights), seed 6.
+MATVEC_N = (4096, 8192, 16384, 36864)
+MATVEC_SEED = 6
+
+
+def int8_matrix_device(rows: int, cols: int, seed: int, device):
+    """Uniform int8 in [-127, 127] drawn by torch's generator on ``device``
+    (for matrices too large to draw on the host quickly)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    return torch.randint(-127, 128, (rows, cols), generator=g, device=device, dtype=torch.int8)

@@ -80,8 +80,8 @@ def test_mask_validation(lib):
 
 
 def test_matmul_validation(lib):
-    # K at the accumulator limit
-    assert lib.mosaic_masked_matmul(FAKE, 4 * 32768, FAKE, 4 * 32768, 1, 1, 32768, FAKE, 1, None) == UNSUPPORTED
+    # a pitch too small for K (long K itself is accepted: it runs in chunks)
+    assert lib.mosaic_masked_matmul(FAKE, 4 * 32768 - 64, FAKE, 4 * 32768, 1, 1, 32768, FAKE, 1, None) == INVALID
     assert lib.mosaic_masked_matmul(FAKE, 256, FAKE, 256, 1, 1, 64, None, 1, None) == INVALID
     assert lib.mosaic_masked_matmul(FAKE, 256, FAKE, 256, 1, 2, 64, FAKE, 1, None) == INVALID   # ldc < N
     assert lib.mosaic_masked_matmul(FAKE, 192, FAKE, 256, 1, 1, 64, FAKE, 1, None) == INVALID   # pitch

@@ -146,6 +146,27 @@ def test_masked_matmul_accumulator_extreme_short_a(M):
     assert np.all(got == (K * (0x7F7F7F80 ** 2)) % (1 << 32))
 
 
+@pytest.mark.parametrize("M,N,K", [(70, 50, 40000), (130, 132, 33000), (3, 37, 65600)])
+def test_masked_matmul_long_inner_dimension(M, N, K):
+    """K >= 2^15 runs as chunks added into C (tiled kernel, per-word and
+    16-byte epilogues, and the K-split kernel)."""
+    rng = _rng_np(M + N + K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
+
+
+@pytest.mark.parametrize("M", [5, 130])
+def test_masked_matmul_accumulator_extreme_long_k(M):
+    """All digits -128 at K = 70000: one launch would overflow the
+    four-product class (4 K 2^14 > 2^31); the chunks keep it exact."""
+    N, K = 36, 70000
+    a = np.full((M, K), 0x7F7F7F80, dtype=np.uint32)
+    b = np.full((N, K), 0x7F7F7F80, dtype=np.uint32)
+    got = _gemm(a, b)
+    assert np.all(got == (K * (0x7F7F7F80 ** 2)) % (1 << 32))
+
+
 def test_masked_matmul_accumulator_extreme():
     """All digits -128 (x = 0x7F7F7F80) at the largest supported K: every
     limb product is +2^14, the four-product class reaches 4 K 2^14 < 2^31."""
