@@ -11,7 +11,9 @@
 // operands does the work of the paper's ten INT8 GEMM launches.
 //
 // Accumulator range: a digit product is at most 2^14 in magnitude, so the
-// four-product class acc_3 stays below 2^31 for K < 2^15 (checked by the ABI).
+// four-product class acc_3 stays below 2^31 for K < 2^15; the ABI splits
+// longer inner dimensions into chunks whose products are added into C
+// (EPI_ACCUM).
 //
 // Work decomposition. A block of 512 threads (8 waves, two per SIMD) owns a
 // 128 x 128 output tile; wave w computes rows 64 (w / 4) .. +64 and columns
@@ -34,6 +36,11 @@
 // 16-byte slots (8 rows), so each lane fetches the chunk that belongs to its
 // slot. Operand tiles are addressed through buffer descriptors that cover only
 // the block's valid rows: rows past M or N read as zero and never fault.
+//
+// Epilogue. The recombined tile is staged in the (then idle) LDS and written
+// in 16-byte chunks along rows (gemm_tile_epilogue): EPI_STORE writes C,
+// EPI_ACCUM adds to C, EPI_UNMASK forms Y = Y' - K_c - C and optionally the
+// dequantised fp32 result.
 #include "internal.h"
 
 namespace mosaic {
