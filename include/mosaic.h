@@ -7,7 +7,9 @@
  * to a small error; a random Hadamard rotation (Section 5) keeps the
  * fixed-point error small. This library implements the data-parallel steps:
  * sampling of the mask material, the mask pass, the server's ring product,
- * unmasking and the rotation.
+ * unmasking, the rotation and fixed-point quantisation (also fused into one
+ * client input pass), the client's products with the sparse LPN matrices,
+ * and the comparison of Freivalds' integrity check.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
