@@ -9,8 +9,9 @@
 // arithmetic. Here the matrix instruction is v_mfma_i32_16x16x64_i8, so A is
 // padded only to 16, 32 or 64 rows.
 //
-// Work decomposition. A workgroup owns 16 rows of B (output columns) and
-// every row of A. Its 8 waves split K into 8 contiguous ranges; each wave
+// Work decomposition. A workgroup owns 16 NT rows of B (output columns; NT
+// is 1, or 2 for A of more than 32 rows, where each B fragment then feeds
+// twice as many MFMAs per A fragment) and every row of A. Its 8 waves split K into 8 contiguous ranges; each wave
 // streams its part of B straight from memory into registers (no reuse, so no
 // LDS staging), reads the matching part of A (shared by all workgroups, so it
 // is served by the caches), and multiplies. The eight partial products are
@@ -30,8 +31,10 @@
 // sixteen k-slots of column group h. A and B use the same k-slot assignment,
 // which is all the product needs.
 //
-// Pipelining. Each wave keeps two stages of loads in flight (the fragments of
-// the next stage load while the current one multiplies). Prefetches past the
+// Pipelining. For A of up to 32 rows each wave keeps two stages of loads in
+// flight (the fragments of the next stage load while the current one
+// multiplies); with 64 rows the accumulators leave no registers for a second
+// set of fragments, and the hardware overlaps the waves instead. Prefetches past the
 // wave's last stage are clamped to that stage: the duplicate request hits in
 // cache and the loop needs no branches around loads.
 #include "internal.h"
