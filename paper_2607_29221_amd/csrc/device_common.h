@@ -9,6 +9,11 @@ namespace mosaic {
 
 constexpr int kMaxDgaussBound = 15;
 
+// 16-byte vectors for __builtin_nontemporal_load/store, which stream data
+// that a kernel reads or writes once.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 // Parameters of one random stream as the kernels see them (passed by value).
 struct RngArgs {
   uint32_t k0, k1;        // Philox key: seed low / high word

@@ -136,40 +136,70 @@ __global__ __launch_bounds__(256) void mask_kernel(MaskLaunch a, int64_t groups)
 // digit words of its columns; a transpose across the four lanes (quad
 // shuffles) then hands lane q digit plane q of the whole group, so each lane
 // stores 16 contiguous bytes and a wave stores 1 KiB contiguous per
-// instruction. XT: 0 none, 1 int8, 2 int32 or ring words.
-template <int XT>
-__global__ __launch_bounds__(256) void mask_quad_kernel(MaskLaunch a, int64_t lanes_per_row) {
-  const int64_t i = blockIdx.x;                     // row
-  const int64_t l = (int64_t)blockIdx.y * blockDim.x + threadIdx.x;   // lane: columns 4 l .. 4 l + 3
+// instruction. Every input is read once and every output written once, so
+// all accesses are non-temporal (they do not displace cached data).
+// XT: 0 none, 1 int8, 2 int32 or ring words. F: which of u, noise, out and
+// digits are present (MQ_* bits). Presence is a compile-time choice: with
+// run-time tests the loads of x and u were issued one round trip apart.
+enum { MQ_U = 1, MQ_NOISE = 2, MQ_OUT = 4, MQ_DIG = 8 };
+// Workgroup b covers 1024-column slice b % slices of row b / slices, so
+// consecutive workgroups stream consecutive memory (79% of the HBM peak
+// measured for the int8 mask pass, against 67% with rows varying fastest).
+template <int XT, int F>
+__global__ __launch_bounds__(256) void mask_quad_kernel(MaskLaunch a, int64_t lanes_per_row, uint32_t slices) {
+  const uint32_t b = blockIdx.x;
+  const int64_t i = b / slices;                     // row
+  const int64_t l = (int64_t)(b - (uint32_t)i * slices) * 256 + threadIdx.x;   // lane: columns 4 l .. 4 l + 3
   if (l >= lanes_per_row) return;                   // whole quads leave together (lanes_per_row % 4 == 0)
   const int64_t j0 = 4 * l;
   const bool valid = j0 < a.cols;                   // cols % 4 == 0: all four columns valid or all padding
   uint32_t v[4] = {0u, 0u, 0u, 0u};
   if (valid) {
+    u32x4 xw = {0u, 0u, 0u, 0u}, uw = {0u, 0u, 0u, 0u};
     if (XT == 1) {
-      const uint32_t w = *(const uint32_t*)((const int8_t*)a.x + i * a.x_rs + j0);
+      const uint32_t w = __builtin_nontemporal_load((const uint32_t*)((const int8_t*)a.x + i * a.x_rs + j0));
 #pragma unroll
-      for (int b = 0; b < 4; ++b) v[b] = (uint32_t)(int32_t)(int8_t)(w >> (8 * b));
+      for (int b = 0; b < 4; ++b) xw[b] = (uint32_t)(int32_t)(int8_t)(w >> (8 * b));
     } else if (XT == 2) {
-      const uint4 w = *(const uint4*)((const uint32_t*)a.x + i * a.x_rs + j0);
-      v[0] = w.x; v[1] = w.y; v[2] = w.z; v[3] = w.w;
+      xw = __builtin_nontemporal_load((const u32x4*)((const uint32_t*)a.x + i * a.x_rs + j0));
     }
-    if (a.u != nullptr) {
-      const uint4 w = *(const uint4*)(a.u + i * a.ldu + j0);
-      v[0] += w.x; v[1] += w.y; v[2] += w.z; v[3] += w.w;
-    }
-    if (a.has_noise) {
+    if (F & MQ_U) uw = __builtin_nontemporal_load((const u32x4*)(a.u + i * a.ldu + j0));
+#pragma unroll
+    for (int b = 0; b < 4; ++b) v[b] = xw[b] + uw[b];
+    if (F & MQ_NOISE) {
       uint32_t e[4];
       sample4_aligned(a.noise, (uint64_t)i * (uint64_t)a.cols + (uint64_t)j0, e);
       v[0] += e[0]; v[1] += e[1]; v[2] += e[2]; v[3] += e[3];
     }
-    if (a.out != nullptr) *(uint4*)(a.out + i * a.ldo + j0) = make_uint4(v[0], v[1], v[2], v[3]);
+    if (F & MQ_OUT) {
+      const u32x4 ov = {v[0], v[1], v[2], v[3]};
+      __builtin_nontemporal_store(ov, (u32x4*)(a.out + i * a.ldo + j0));
+    }
   }
-  if (a.dig != nullptr) {
+  if (F & MQ_DIG) {
     uint32_t o[4];
     quad_digit_planes(v, (int)(l & 3), o);
-    *(uint4*)(a.dig + i * a.pitch + 16 * l) = make_uint4(o[0], o[1], o[2], o[3]);
+    const u32x4 ov = {o[0], o[1], o[2], o[3]};
+    __builtin_nontemporal_store(ov, (u32x4*)(a.dig + i * a.pitch + 16 * l));
   }
+}
+
+template <int XT, int F>
+void launch_mask_quad(uint32_t slices, const MaskLaunch& a, int64_t lanes_per_row, hipStream_t s) {
+  hipLaunchKernelGGL((mask_quad_kernel<XT, F>), dim3((unsigned)(a.rows * slices)), dim3(256), 0, s, a,
+                     lanes_per_row, slices);
+}
+
+typedef void (*MaskQuadLaunch)(uint32_t, const MaskLaunch&, int64_t, hipStream_t);
+
+template <int XT>
+MaskQuadLaunch mask_quad_for(int f) {
+  static const MaskQuadLaunch table[16] = {
+      launch_mask_quad<XT, 0>,  launch_mask_quad<XT, 1>,  launch_mask_quad<XT, 2>,  launch_mask_quad<XT, 3>,
+      launch_mask_quad<XT, 4>,  launch_mask_quad<XT, 5>,  launch_mask_quad<XT, 6>,  launch_mask_quad<XT, 7>,
+      launch_mask_quad<XT, 8>,  launch_mask_quad<XT, 9>,  launch_mask_quad<XT, 10>, launch_mask_quad<XT, 11>,
+      launch_mask_quad<XT, 12>, launch_mask_quad<XT, 13>, launch_mask_quad<XT, 14>, launch_mask_quad<XT, 15>};
+  return table[f & 15];
 }
 
 __global__ __launch_bounds__(256) void signs_kernel(RngArgs r, int64_t n, int8_t* out) {
@@ -231,12 +261,14 @@ hipError_t launch_mask(const MaskLaunch& a, hipStream_t s) {
   const bool n_ok = !a.has_noise || !a.noise.transposed;
   const int64_t lanes_per_row = (a.dig != nullptr) ? 64 * ((a.cols + 63) / 64) / 4 : 4 * ((a.cols + 15) / 16);
   const int64_t blocks_per_row = (lanes_per_row + 255) / 256;
-  if (a.cols % 4 == 0 && x_ok && u_ok && o_ok && n_ok && blocks_per_row <= 65535 && a.rows <= 0x7FFFFFFF) {
+  if (a.cols % 4 == 0 && x_ok && u_ok && o_ok && n_ok && a.rows * blocks_per_row <= 0x7FFFFFFF) {
     if (a.rows == 0 || lanes_per_row == 0) return hipSuccess;
-    const dim3 grid((unsigned)a.rows, (unsigned)blocks_per_row);   // x: row, y: 1024-column slice
-    if (a.x == nullptr) hipLaunchKernelGGL(mask_quad_kernel<0>, grid, dim3(256), 0, s, a, lanes_per_row);
-    else if (a.x_dtype == 0) hipLaunchKernelGGL(mask_quad_kernel<1>, grid, dim3(256), 0, s, a, lanes_per_row);
-    else hipLaunchKernelGGL(mask_quad_kernel<2>, grid, dim3(256), 0, s, a, lanes_per_row);
+    const uint32_t slices = (uint32_t)blocks_per_row;
+    const int f = (a.u != nullptr ? MQ_U : 0) | (a.has_noise ? MQ_NOISE : 0) | (a.out != nullptr ? MQ_OUT : 0) |
+                  (a.dig != nullptr ? MQ_DIG : 0);
+    if (a.x == nullptr) mask_quad_for<0>(f)(slices, a, lanes_per_row, s);
+    else if (a.x_dtype == 0) mask_quad_for<1>(f)(slices, a, lanes_per_row, s);
+    else mask_quad_for<2>(f)(slices, a, lanes_per_row, s);
     return hipGetLastError();
   }
   const int64_t groups = (a.dig != nullptr) ? (64 * ((a.cols + 63) / 64)) / 16 : (a.cols + 15) / 16;

@@ -36,25 +36,47 @@ struct FwhtShape {
 
 __device__ __forceinline__ int fwht_pad(int idx) { return idx + (idx >> 5); }
 
-// Unscaled H_b (d * x) of the block at xr (d = signs at sg, or none) into v.
-// Every thread of the workgroup (FwhtShape<LOGB>::T of them) must call it;
-// sm must not be in use by other threads when it is called.
+// v[r] *= d of its element (load layout), d = +-1 from the int8 signs at sg.
 template <int LOGB>
-__device__ __forceinline__ void fwht_block(const float* __restrict__ xr, const int8_t* __restrict__ sg,
-                                           bool sign_on_load, float* sm, float (&v)[FwhtShape<LOGB>::E]) {
+__device__ __forceinline__ void apply_signs(const int8_t* __restrict__ sg, float (&v)[FwhtShape<LOGB>::E]) {
   using S = FwhtShape<LOGB>;
-  constexpr int T = S::T, LOGT = S::LOGT, E = S::E, LOGE = S::LOGE, NV = S::NV;
+  constexpr int T = S::T, NV = S::NV;
   const int t = threadIdx.x;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    const float4 f = ((const float4*)xr)[t + T * k];
-    v[4 * k + 0] = f.x; v[4 * k + 1] = f.y; v[4 * k + 2] = f.z; v[4 * k + 3] = f.w;
-    if (sign_on_load && sg) {
-      const char4 s4 = ((const char4*)sg)[t + T * k];
-      v[4 * k + 0] *= (float)s4.x; v[4 * k + 1] *= (float)s4.y;
-      v[4 * k + 2] *= (float)s4.z; v[4 * k + 3] *= (float)s4.w;
-    }
+    const char4 s4 = ((const char4*)sg)[t + T * k];
+    v[4 * k + 0] *= (float)s4.x; v[4 * k + 1] *= (float)s4.y;
+    v[4 * k + 2] *= (float)s4.z; v[4 * k + 3] *= (float)s4.w;
   }
+}
+
+// This thread's share of the block at xr in the load layout (register r of
+// thread t: element 4 (t + T (r / 4)) + r % 4), times the signs at sg if SG.
+// NT selects non-temporal loads, for data that is read once. Signs are a
+// compile-time choice: a run-time test between the loads serialises them.
+template <int LOGB, bool SG, bool NT>
+__device__ __forceinline__ void fwht_load(const float* __restrict__ xr, const int8_t* __restrict__ sg,
+                                          float (&v)[FwhtShape<LOGB>::E]) {
+  using S = FwhtShape<LOGB>;
+  constexpr int T = S::T, NV = S::NV;
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const f32x4* p = (const f32x4*)xr + t + T * k;
+    const f32x4 f = NT ? __builtin_nontemporal_load(p) : *p;
+    v[4 * k + 0] = f[0]; v[4 * k + 1] = f[1]; v[4 * k + 2] = f[2]; v[4 * k + 3] = f[3];
+  }
+  if (SG) apply_signs<LOGB>(sg, v);
+}
+
+// In-place unscaled H_b of a block held in the load layout. Every thread of
+// the workgroup (FwhtShape<LOGB>::T of them) must call it; sm must not be in
+// use by other threads when it is called.
+template <int LOGB>
+__device__ __forceinline__ void fwht_transform(float* sm, float (&v)[FwhtShape<LOGB>::E]) {
+  using S = FwhtShape<LOGB>;
+  constexpr int T = S::T, LOGT = S::LOGT, E = S::E, LOGE = S::LOGE;
+  const int t = threadIdx.x;
 
   // stages on the index bits held in registers: bits of r = 4 k + q
 #pragma unroll

@@ -10,10 +10,12 @@
 namespace mosaic {
 namespace {
 
-template <int LOGB>
+// SIGNS: 0 none, 1 applied on load (forward), 2 applied on store (inverse).
+// x is read once and y written once, so both use non-temporal accesses.
+template <int LOGB, int SIGNS>
 __global__ __launch_bounds__(FwhtShape<LOGB>::T) void fwht_kernel(
     const float* __restrict__ x, int64_t ldx, float* y, int64_t ldy, int64_t blocks_per_row,
-    const int8_t* __restrict__ signs, int inverse, float scale) {
+    const int8_t* __restrict__ signs, float scale) {
   using S = FwhtShape<LOGB>;
   constexpr int T = S::T, E = S::E, NV = S::NV, B = S::B;
   __shared__ float sm[S::SM];
@@ -22,19 +24,18 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void fwht_kernel(
   const int64_t blk = blockIdx.x - row * blocks_per_row;
   const float* xr = x + row * ldx + blk * B;
   float* yr = y + row * ldy + blk * B;
-  const int8_t* sg = signs ? signs + blk * B : nullptr;
+  const int8_t* sg = SIGNS ? signs + blk * B : nullptr;
 
   float v[E];
-  fwht_block<LOGB>(xr, sg, !inverse, sm, v);
-
+  fwht_load<LOGB, SIGNS == 1, true>(xr, sg, v);
+  fwht_transform<LOGB>(sm, v);
+#pragma unroll
+  for (int r = 0; r < E; ++r) v[r] *= scale;
+  if (SIGNS == 2) apply_signs<LOGB>(sg, v);
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    float4 f = make_float4(v[4 * k] * scale, v[4 * k + 1] * scale, v[4 * k + 2] * scale, v[4 * k + 3] * scale);
-    if (inverse && sg) {
-      const char4 s4 = ((const char4*)sg)[t + T * k];
-      f.x *= (float)s4.x; f.y *= (float)s4.y; f.z *= (float)s4.z; f.w *= (float)s4.w;
-    }
-    ((float4*)yr)[t + T * k] = f;
+    const f32x4 f = {v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
+    __builtin_nontemporal_store(f, (f32x4*)yr + t + T * k);
   }
 }
 
@@ -47,8 +48,15 @@ hipError_t launch_fwht(const float* x, int64_t ldx, float* y, int64_t ldy, int64
   const int64_t grid = rows * bpr;
   if (grid == 0) return hipSuccess;
   const float scale = (float)(1.0 / sqrt((double)B));
-  hipLaunchKernelGGL(fwht_kernel<LOGB>, dim3((unsigned)grid), dim3(T), 0, s, x, ldx, y, ldy, bpr, signs,
-                     inverse, scale);
+  if (signs == nullptr)
+    hipLaunchKernelGGL((fwht_kernel<LOGB, 0>), dim3((unsigned)grid), dim3(T), 0, s, x, ldx, y, ldy, bpr, signs,
+                       scale);
+  else if (!inverse)
+    hipLaunchKernelGGL((fwht_kernel<LOGB, 1>), dim3((unsigned)grid), dim3(T), 0, s, x, ldx, y, ldy, bpr, signs,
+                       scale);
+  else
+    hipLaunchKernelGGL((fwht_kernel<LOGB, 2>), dim3((unsigned)grid), dim3(T), 0, s, x, ldx, y, ldy, bpr, signs,
+                       scale);
   return hipGetLastError();
 }
 

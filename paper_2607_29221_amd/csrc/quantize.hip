@@ -105,6 +105,60 @@ __global__ __launch_bounds__(256) void quantize_rows_vec_kernel(const float* __r
   }
 }
 
+// Rows of at most 1024 NV elements: the row is read once, with non-temporal
+// loads, and kept in registers (thread t holds columns 4 (t + 256 k) .. + 3,
+// k < NV) between the max reduction and the code pass; stores are
+// non-temporal. Same arithmetic and output layout as the kernel above.
+template <int NV>
+__global__ __launch_bounds__(256) void quantize_rows_reg_kernel(const float* __restrict__ x, int64_t ldx,
+                                                                int64_t n, int32_t qmax, int32_t* q, int64_t ldq,
+                                                                int8_t* q_dig, int64_t q_pitch, float* scale) {
+  __shared__ float red[4];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const f32x4* xr = (const f32x4*)(x + row * ldx);
+  const int64_t nv = n / 4;
+  f32x4 f[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int64_t c = t + 256 * k;
+    f[k] = c < nv ? __builtin_nontemporal_load(xr + c) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+  float m = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k)
+    m = fmaxf(m, fmaxf(fmaxf(fabsf(f[k][0]), fabsf(f[k][1])), fmaxf(fabsf(f[k][2]), fabsf(f[k][3]))));
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((t & 63) == 0) red[t >> 6] = m;
+  __syncthreads();
+  const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
+  if (t == 0 && scale != nullptr) scale[row] = s;
+
+  const int64_t nchunks = q_dig ? 16 * ((n + 63) / 64) : nv;   // <= 256 NV; a multiple of 4 with digits
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int64_t c = t + 256 * k;
+    if (c >= nchunks) break;                                     // uniform per quad (256 % 4 == 0)
+    uint32_t v[4] = {0u, 0u, 0u, 0u};
+    if (c < nv) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (uint32_t)(int32_t)rintf(f[k][i] / s);
+      if (q != nullptr) {
+        const u32x4 ov = {v[0], v[1], v[2], v[3]};
+        __builtin_nontemporal_store(ov, (u32x4*)(q + row * ldq + 4 * c));
+      }
+    }
+    if (q_dig != nullptr) {
+      uint32_t o[4];
+      quad_digit_planes(v, (int)(c & 3), o);
+      const u32x4 ov = {o[0], o[1], o[2], o[3]};
+      __builtin_nontemporal_store(ov, (u32x4*)(q_dig + row * q_pitch + 16 * c));
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64_t n, int32_t qmax, int32_t* q,
@@ -113,7 +167,23 @@ hipError_t launch_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64
   const bool vec = n % 4 == 0 && ldx % 4 == 0 && ((uintptr_t)x & 15) == 0 &&
                    (q == nullptr || (ldq % 4 == 0 && ((uintptr_t)q & 15) == 0)) &&
                    (q_dig == nullptr || ((uintptr_t)q_dig & 15) == 0);
-  if (vec)
+  const dim3 grid((unsigned)rows);
+  if (vec && n <= 1024)
+    hipLaunchKernelGGL(quantize_rows_reg_kernel<1>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
+                       scale);
+  else if (vec && n <= 2048)
+    hipLaunchKernelGGL(quantize_rows_reg_kernel<2>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
+                       scale);
+  else if (vec && n <= 4096)
+    hipLaunchKernelGGL(quantize_rows_reg_kernel<4>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
+                       scale);
+  else if (vec && n <= 8192)
+    hipLaunchKernelGGL(quantize_rows_reg_kernel<8>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
+                       scale);
+  else if (vec && n <= 16384)
+    hipLaunchKernelGGL(quantize_rows_reg_kernel<16>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
+                       scale);
+  else if (vec)
     hipLaunchKernelGGL(quantize_rows_vec_kernel, dim3((unsigned)rows), dim3(256), 0, s, x, ldx, n, qmax, q, ldq,
                        q_dig, q_pitch, scale);
   else

@@ -37,7 +37,7 @@ __device__ __forceinline__ float block_max(float m, float* red) {
   return r;
 }
 
-template <int LOGB>
+template <int LOGB, bool SG>
 __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float* __restrict__ x, int64_t ldx,
                                                                      int64_t n, const int8_t* __restrict__ signs,
                                                                      float scale_b, float* amax_out) {
@@ -51,7 +51,8 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float
   float m = 0.0f;
   for (int64_t blk = 0; blk < n / B; ++blk) {
     float v[E];
-    fwht_block<LOGB>(xr + blk * B, signs ? signs + blk * B : nullptr, true, sm, v);
+    fwht_load<LOGB, SG, false>(xr + blk * B, SG ? signs + blk * B : nullptr, v);   // x is read again next launch
+    fwht_transform<LOGB>(sm, v);
 #pragma unroll
     for (int r = 0; r < E; ++r) m = fmaxf(m, fabsf(v[r] * scale_b));
     __syncthreads();                // the next block reuses the scratch
@@ -60,11 +61,16 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float
   if (threadIdx.x == 0) amax_out[row] = amax;
 }
 
-template <int LOGB>
+// SG, HU, HN: signs, u and noise present (compile-time, so that no run-time
+// test sits between a load and its use). Each 16-byte word of u is requested
+// where it is used: requesting a block's words ahead (before the transform,
+// or all before the first use) holds them in registers, fewer workgroups fit
+// and the pass ran 10-25% slower.
+template <int LOGB, bool SG, bool HU, bool HN>
 __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_mask_kernel(
     const float* __restrict__ x, int64_t ldx, int64_t n, const int8_t* __restrict__ signs, float scale_b,
-    int32_t qmax, const uint32_t* __restrict__ u, int64_t ldu, int32_t has_noise, RngArgs noise, int8_t* out_dig,
-    int64_t pitch, float* scale) {
+    int32_t qmax, const uint32_t* __restrict__ u, int64_t ldu, RngArgs noise, int8_t* out_dig, int64_t pitch,
+    float* scale) {
   using S = FwhtShape<LOGB>;
   constexpr int T = S::T, E = S::E, NV = S::NV, B = S::B;
   __shared__ float sm[S::SM];
@@ -75,44 +81,69 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_mask_kernel(
   const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
   for (int64_t blk = 0; blk < n / B; ++blk) {
     float v[E];
-    fwht_block<LOGB>(xr + blk * B, signs ? signs + blk * B : nullptr, true, sm, v);
+    fwht_load<LOGB, SG, true>(xr + blk * B, SG ? signs + blk * B : nullptr, v);
+    fwht_transform<LOGB>(sm, v);
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       // columns 4 c .. 4 c + 3 of the row; lanes t .. t + 3 hold one 16-column group
       const int64_t c = blk * (B / 4) + t + T * k;
+      const u32x4 uu = HU ? __builtin_nontemporal_load((const u32x4*)(u + row * ldu + 4 * c)) : u32x4{0, 0, 0, 0};
       uint32_t w[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)(int32_t)rintf((v[4 * k + q] * scale_b) / s);
-      if (u != nullptr) {
-        const uint4 uu = *(const uint4*)(u + row * ldu + 4 * c);
-        w[0] += uu.x; w[1] += uu.y; w[2] += uu.z; w[3] += uu.w;
-      }
-      if (has_noise) {
+      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)(int32_t)rintf((v[4 * k + q] * scale_b) / s) + uu[q];
+      if (HN) {
         uint32_t e[4];
         sample4_aligned(noise, (uint64_t)row * (uint64_t)n + (uint64_t)(4 * c), e);
         w[0] += e[0]; w[1] += e[1]; w[2] += e[2]; w[3] += e[3];
       }
       uint32_t o[4];
       quad_digit_planes(w, t & 3, o);
-      *(uint4*)(out_dig + row * pitch + 16 * c) = make_uint4(o[0], o[1], o[2], o[3]);
+      const u32x4 ov = {o[0], o[1], o[2], o[3]};
+      __builtin_nontemporal_store(ov, (u32x4*)(out_dig + row * pitch + 16 * c));
     }
     __syncthreads();                // the next block reuses the scratch
   }
   if (t == 0) scale[row] = s;       // every thread read the maximum before the first barrier
 }
 
+template <int LOGB, bool SG, bool HU, bool HN>
+hipError_t launch_rqm_t(const float* x, int64_t ldx, int64_t rows, int64_t n, const int8_t* signs, int32_t qmax,
+                        const uint32_t* u, int64_t ldu, const RngArgs* noise, int8_t* out_dig, int64_t pitch,
+                        float* scale, hipStream_t s) {
+  using S = FwhtShape<LOGB>;
+  const float scale_b = (float)(1.0 / sqrt((double)S::B));
+  hipLaunchKernelGGL((rqm_max_kernel<LOGB, SG>), dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, n, signs, scale_b,
+                     scale);
+  hipLaunchKernelGGL((rqm_mask_kernel<LOGB, SG, HU, HN>), dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, n, signs,
+                     scale_b, qmax, u, ldu, HN ? *noise : RngArgs{}, out_dig, pitch, scale);
+  return hipGetLastError();
+}
+
+template <int LOGB, bool SG, bool HU>
+hipError_t launch_rqm_n(const float* x, int64_t ldx, int64_t rows, int64_t n, const int8_t* signs, int32_t qmax,
+                        const uint32_t* u, int64_t ldu, const RngArgs* noise, int8_t* out_dig, int64_t pitch,
+                        float* scale, hipStream_t s) {
+  if (noise != nullptr)
+    return launch_rqm_t<LOGB, SG, HU, true>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+  return launch_rqm_t<LOGB, SG, HU, false>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+}
+
+template <int LOGB, bool SG>
+hipError_t launch_rqm_u(const float* x, int64_t ldx, int64_t rows, int64_t n, const int8_t* signs, int32_t qmax,
+                        const uint32_t* u, int64_t ldu, const RngArgs* noise, int8_t* out_dig, int64_t pitch,
+                        float* scale, hipStream_t s) {
+  if (u != nullptr)
+    return launch_rqm_n<LOGB, SG, true>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+  return launch_rqm_n<LOGB, SG, false>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+}
+
 template <int LOGB>
 hipError_t launch_rqm(const float* x, int64_t ldx, int64_t rows, int64_t n, const int8_t* signs, int32_t qmax,
                       const uint32_t* u, int64_t ldu, const RngArgs* noise, int8_t* out_dig, int64_t pitch,
                       float* scale, hipStream_t s) {
-  using S = FwhtShape<LOGB>;
-  const float scale_b = (float)(1.0 / sqrt((double)S::B));
-  hipLaunchKernelGGL(rqm_max_kernel<LOGB>, dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, n, signs, scale_b,
-                     scale);
-  hipLaunchKernelGGL(rqm_mask_kernel<LOGB>, dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, n, signs, scale_b,
-                     qmax, u, ldu, noise != nullptr ? 1 : 0, noise != nullptr ? *noise : RngArgs{}, out_dig, pitch,
-                     scale);
-  return hipGetLastError();
+  if (signs != nullptr)
+    return launch_rqm_u<LOGB, true>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
+  return launch_rqm_u<LOGB, false>(x, ldx, rows, n, signs, qmax, u, ldu, noise, out_dig, pitch, scale, s);
 }
 
 }  // namespace
