@@ -28,9 +28,9 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void fwht_kernel(
 
   float v[E];
   fwht_load<LOGB, SIGNS == 1, true>(xr, sg, v);
-  fwht_transform<LOGB>(sm, v);
+  const float sc = scale * fwht_transform<LOGB>(sm, v);   // the transform's lane sign folded into the scale
 #pragma unroll
-  for (int r = 0; r < E; ++r) v[r] *= scale;
+  for (int r = 0; r < E; ++r) v[r] *= sc;
   if (SIGNS == 2) apply_signs<LOGB>(sg, v);
 #pragma unroll
   for (int k = 0; k < NV; ++k) {

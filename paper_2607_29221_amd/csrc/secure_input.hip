@@ -52,7 +52,7 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float
   for (int64_t blk = 0; blk < n / B; ++blk) {
     float v[E];
     fwht_load<LOGB, SG, false>(xr + blk * B, SG ? signs + blk * B : nullptr, v);   // x is read again next launch
-    fwht_transform<LOGB>(sm, v);
+    fwht_transform<LOGB>(sm, v);    // the lane sign it returns does not change |y|
 #pragma unroll
     for (int r = 0; r < E; ++r) m = fmaxf(m, fabsf(v[r] * scale_b));
     __syncthreads();                // the next block reuses the scratch
@@ -67,7 +67,7 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float
 // or all before the first use) holds them in registers, fewer workgroups fit
 // and the pass ran 10-25% slower.
 template <int LOGB, bool SG, bool HU, bool HN>
-__global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_mask_kernel(
+__global__ __launch_bounds__(FwhtShape<LOGB>::T, FwhtShape<LOGB>::WAVES) void rqm_mask_kernel(
     const float* __restrict__ x, int64_t ldx, int64_t n, const int8_t* __restrict__ signs, float scale_b,
     int32_t qmax, const uint32_t* __restrict__ u, int64_t ldu, RngArgs noise, int8_t* out_dig, int64_t pitch,
     float* scale) {
@@ -82,7 +82,7 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_mask_kernel(
   for (int64_t blk = 0; blk < n / B; ++blk) {
     float v[E];
     fwht_load<LOGB, SG, true>(xr + blk * B, SG ? signs + blk * B : nullptr, v);
-    fwht_transform<LOGB>(sm, v);
+    const float sb = scale_b * fwht_transform<LOGB>(sm, v);   // the lane sign folded into the scale
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       // columns 4 c .. 4 c + 3 of the row; lanes t .. t + 3 hold one 16-column group
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_mask_kernel(
       const u32x4 uu = HU ? __builtin_nontemporal_load((const u32x4*)(u + row * ldu + 4 * c)) : u32x4{0, 0, 0, 0};
       uint32_t w[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)(int32_t)rintf((v[4 * k + q] * scale_b) / s) + uu[q];
+      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)(int32_t)rintf((v[4 * k + q] * sb) / s) + uu[q];
       if (HN) {
         uint32_t e[4];
         sample4_aligned(noise, (uint64_t)row * (uint64_t)n + (uint64_t)(4 * c), e);
