@@ -543,6 +543,9 @@ def main():
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--product-only", action="store_true",
                     help="only time the server ring product on uniform digits (for counter runs)")
+    ap.add_argument("--passes-only", action="store_true",
+                    help="only time the stand-alone passes (rotation, mask, samplers, quantisation, fused input "
+                         "pass; for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device three times (scale for HBM byte counters)")
     args = ap.parse_args()
@@ -553,6 +556,11 @@ def main():
 
     if args.product_only:
         print(json.dumps({"product_only": run_product_only()}))
+        return
+
+    if args.passes_only:
+        import torch
+        print(json.dumps({"passes": run_extras(torch.device("cuda:0"))}))
         return
 
     if args.copy_calibration:

@@ -105,15 +105,16 @@ __global__ __launch_bounds__(256) void quantize_rows_vec_kernel(const float* __r
   }
 }
 
-// Rows of at most 1024 NV elements: the row is read once, with non-temporal
-// loads, and kept in registers (thread t holds columns 4 (t + 256 k) .. + 3,
+// Rows of at most 4 NT NV elements: the row is read once, with non-temporal
+// loads, and kept in registers (thread t holds columns 4 (t + NT k) .. + 3,
 // k < NV) between the max reduction and the code pass; stores are
-// non-temporal. Same arithmetic and output layout as the kernel above.
-template <int NV>
-__global__ __launch_bounds__(256) void quantize_rows_reg_kernel(const float* __restrict__ x, int64_t ldx,
-                                                                int64_t n, int32_t qmax, int32_t* q, int64_t ldq,
-                                                                int8_t* q_dig, int64_t q_pitch, float* scale) {
-  __shared__ float red[4];
+// non-temporal. Same arithmetic and output layout as the kernels above.
+template <int NT, int NV>
+__global__ __launch_bounds__(NT) void quantize_rows_reg_kernel(const float* __restrict__ x, int64_t ldx,
+                                                               int64_t n, int32_t qmax, int32_t* q, int64_t ldq,
+                                                               int8_t* q_dig, int64_t q_pitch, float* scale) {
+  constexpr int NW = NT / 64;
+  __shared__ float red[NW];
   const int t = threadIdx.x;
   const int64_t row = blockIdx.x;
   const f32x4* xr = (const f32x4*)(x + row * ldx);
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(256) void quantize_rows_reg_kernel(const float* __r
   f32x4 f[NV];
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    const int64_t c = t + 256 * k;
+    const int64_t c = t + NT * k;
     f[k] = c < nv ? __builtin_nontemporal_load(xr + c) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   }
   float m = 0.0f;
@@ -132,15 +133,17 @@ __global__ __launch_bounds__(256) void quantize_rows_reg_kernel(const float* __r
   for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
   if ((t & 63) == 0) red[t >> 6] = m;
   __syncthreads();
-  const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float amax = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) amax = fmaxf(amax, red[w]);
   const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
   if (t == 0 && scale != nullptr) scale[row] = s;
 
-  const int64_t nchunks = q_dig ? 16 * ((n + 63) / 64) : nv;   // <= 256 NV; a multiple of 4 with digits
+  const int64_t nchunks = q_dig ? 16 * ((n + 63) / 64) : nv;   // <= NT NV; a multiple of 4 with digits
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    const int64_t c = t + 256 * k;
-    if (c >= nchunks) break;                                     // uniform per quad (256 % 4 == 0)
+    const int64_t c = t + NT * k;
+    if (c >= nchunks) break;                                     // uniform per quad (NT % 4 == 0)
     uint32_t v[4] = {0u, 0u, 0u, 0u};
     if (c < nv) {
 #pragma unroll
@@ -159,6 +162,13 @@ __global__ __launch_bounds__(256) void quantize_rows_reg_kernel(const float* __r
   }
 }
 
+template <int NT, int NV>
+void launch_quantize_reg(const float* x, int64_t ldx, int64_t rows, int64_t n, int32_t qmax, int32_t* q,
+                         int64_t ldq, int8_t* q_dig, int64_t q_pitch, float* scale, hipStream_t s) {
+  hipLaunchKernelGGL((quantize_rows_reg_kernel<NT, NV>), dim3((unsigned)rows), dim3(NT), 0, s, x, ldx, n, qmax, q,
+                     ldq, q_dig, q_pitch, scale);
+}
+
 }  // namespace
 
 hipError_t launch_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64_t n, int32_t qmax, int32_t* q,
@@ -167,22 +177,14 @@ hipError_t launch_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64
   const bool vec = n % 4 == 0 && ldx % 4 == 0 && ((uintptr_t)x & 15) == 0 &&
                    (q == nullptr || (ldq % 4 == 0 && ((uintptr_t)q & 15) == 0)) &&
                    (q_dig == nullptr || ((uintptr_t)q_dig & 15) == 0);
-  const dim3 grid((unsigned)rows);
-  if (vec && n <= 1024)
-    hipLaunchKernelGGL(quantize_rows_reg_kernel<1>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
-                       scale);
-  else if (vec && n <= 2048)
-    hipLaunchKernelGGL(quantize_rows_reg_kernel<2>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
-                       scale);
-  else if (vec && n <= 4096)
-    hipLaunchKernelGGL(quantize_rows_reg_kernel<4>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
-                       scale);
-  else if (vec && n <= 8192)
-    hipLaunchKernelGGL(quantize_rows_reg_kernel<8>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
-                       scale);
-  else if (vec && n <= 16384)
-    hipLaunchKernelGGL(quantize_rows_reg_kernel<16>, grid, dim3(256), 0, s, x, ldx, n, qmax, q, ldq, q_dig, q_pitch,
-                       scale);
+  // register-resident rows: 256 threads up to n = 16384, 1024 threads up to 65536
+  if (vec && n <= 1024) launch_quantize_reg<256, 1>(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, s);
+  else if (vec && n <= 2048) launch_quantize_reg<256, 2>(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, s);
+  else if (vec && n <= 4096) launch_quantize_reg<256, 4>(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, s);
+  else if (vec && n <= 8192) launch_quantize_reg<256, 8>(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, s);
+  else if (vec && n <= 16384) launch_quantize_reg<256, 16>(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, s);
+  else if (vec && n <= 32768) launch_quantize_reg<1024, 8>(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, s);
+  else if (vec && n <= 65536) launch_quantize_reg<1024, 16>(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, s);
   else if (vec)
     hipLaunchKernelGGL(quantize_rows_vec_kernel, dim3((unsigned)rows), dim3(256), 0, s, x, ldx, n, qmax, q, ldq,
                        q_dig, q_pitch, scale);

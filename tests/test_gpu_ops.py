@@ -278,13 +278,15 @@ def test_hadamard_in_place_roundtrip_and_no_signs():
 
 @pytest.mark.parametrize("rows,n,qmax", [(5, 100, 127), (16, 8192, 1997), (3, 28672, 567), (2, 64, 1),
                                          (7, 102, 127), (4, 4100, 300), (3, 1024, 127), (3, 2000, 127),
-                                         (2, 4096, 255), (2, 9000, 127), (2, 16384, 1000), (2, 16388, 77)])
+                                         (2, 4096, 255), (2, 9000, 127), (2, 16384, 1000), (2, 16388, 77),
+                                         (2, 40000, 127), (2, 65536, 300), (2, 70000, 511)])
 @pytest.mark.parametrize("offset", [0, 1])
 def test_quantize(rows, n, qmax, offset):
     """offset 1 reads rows that start one float into a wider buffer (not
     16-byte aligned): the general kernel; offset 0 with n % 4 == 0: the
-    register-resident kernel (n <= 16384: one size per power of two from
-    1024, each also with a ragged row) or the two-pass vector kernel."""
+    register-resident kernel (256 threads up to n = 16384, 1024 threads up
+    to 65536; each size class also with a ragged row) or, beyond, the
+    two-pass vector kernel."""
     x = _rng_np(n).standard_normal((rows, n)).astype(np.float32)
     x[1] = 0.0
     wide = torch.zeros((rows, n + 4), dtype=torch.float32, device="cuda")
