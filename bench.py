@@ -141,6 +141,7 @@ def run_gpu(steps: int, warmup: int, extras: bool):
         out["extras"]["decoder_stack"] = run_decoder_stack(dev)
         out["extras"]["integrity_check"] = run_integrity(dev)
         out["extras"]["matvec_sweep"] = run_matvec_sweep(dev)
+        out["extras"]["vendor_int8_gemm"] = run_vendor_int8(dev)
     return out
 
 
@@ -270,6 +271,33 @@ def run_extras(dev):
                                     "fused_gbs": round(rows * n * 12 / (ts[1] * 1e-3) / 1e9, 1)})
         del xs, U, Dg, y, q
     return res
+
+
+def run_vendor_int8(dev):
+    """Context for the MFMA figure: the vendor int8 GEMM (torch._int_mm, which
+    calls hipBLASLt) on uniformly random int8 operands with the int8 work of
+    the largest server launch as one plain GEMM (M = 2048, K = 4 x 8192 digit
+    columns, N = 30208, B column-major), in int8 TOP/s. Not part of the
+    product path."""
+    import torch
+
+    M, K, N = 2048, 4 * 8192, 30208
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    a = torch.randint(-128, 128, (M, K), dtype=torch.int8, device=dev, generator=g)
+    b = torch.randint(-128, 128, (N, K), dtype=torch.int8, device=dev, generator=g).t()
+    for _ in range(2):
+        torch._int_mm(a, b)
+    reps = 10
+    e0, e1 = _events(2)
+    e0.record()
+    for _ in range(reps):
+        torch._int_mm(a, b)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"M": M, "K": K, "N": N, "ms": round(ms, 3), "int8_tops": round(2.0 * M * K * N / (ms * 1e-3) / 1e12, 1),
+            "operands": "uniform int8"}
 
 
 def run_integrity(dev):
