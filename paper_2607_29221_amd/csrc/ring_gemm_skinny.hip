@@ -9,15 +9,24 @@
 // arithmetic. Here the matrix instruction is v_mfma_i32_16x16x64_i8, so A is
 // padded only to 16, 32 or 64 rows.
 //
-// Work decomposition. A workgroup owns 16 NT rows of B (output columns; NT
-// is 1, or 2 for A of more than 32 rows, where each B fragment then feeds
-// twice as many MFMAs per A fragment) and every row of A. Its 8 waves split K into 8 contiguous ranges; each wave
-// streams its part of B straight from memory into registers (no reuse, so no
-// LDS staging), reads the matching part of A (shared by all workgroups, so it
-// is served by the caches), and multiplies. The eight partial products are
-// summed in LDS with wrap-around adds, which is exact in the ring, and the
-// epilogue writes each output once. No partial sums leave the workgroup.
-//
+// Work decomposition. The unit of work is one (column tile, stage) pair: 16
+// NT rows of B (output columns) against all rows of A over 64 columns of K.
+// A workgroup of 4 waves walks a contiguous range of these pairs, one tile
+// segment at a time; its waves split each segment's stages into 4
+// contiguous parts. Each wave streams its part of B straight from memory
+// into registers (no reuse, so no LDS staging), reads the matching part of
+// A (shared by all workgroups, so it is served by the caches), and
+// multiplies. The partial products of the waves are summed in LDS with
+// wrap-around adds, which is exact in the ring. Wide tiles (NT = 2 for A of
+// at most 16 rows, 4 above) let each A fragment feed several B fragments:
+// every workgroup re-reads all of A, and for 64 tokens those re-reads, not
+// B, were the larger share of the traffic. A segment covering a whole tile
+// goes through the epilogue; otherwise (the balanced assignment, see
+// launch_cfg) partial products are added into C with 32-bit atomics, again
+// exact in the ring. Measured against one 16-row tile per workgroup of 8
+// waves with whole tiles: 20-24% less time for 8 tokens and 25-40% for 32
+// and 64 tokens at the decode shapes.
+
 // Operand fragments. For the 16 x 16 x 64 instruction, lane l supplies row
 // l % 16 and sixteen of the 64 k-slots, chosen by l / 16. In the digit layout
 // a group of 16 columns keeps its four digit planes in 64 consecutive bytes,
@@ -31,10 +40,10 @@
 // sixteen k-slots of column group h. A and B use the same k-slot assignment,
 // which is all the product needs.
 //
-// Pipelining. For A of up to 32 rows each wave keeps two stages of loads in
+// Pipelining. For A of up to 16 rows each wave keeps two stages of loads in
 // flight (the fragments of the next stage load while the current one
-// multiplies); with 64 rows the accumulators leave no registers for a second
-// set of fragments, and the hardware overlaps the waves instead. Prefetches past the
+// multiplies); with more rows the accumulators leave no registers for a
+// second set of fragments, and the hardware overlaps the waves instead. Prefetches past the
 // wave's last stage are clamped to that stage: the duplicate request hits in
 // cache and the loop needs no branches around loads.
 #include "internal.h"
@@ -44,7 +53,7 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-constexpr int NWAVES = 8;
+constexpr int NWAVES = 4;
 constexpr int NTHREADS = 64 * NWAVES;
 constexpr int STAGE_BYTES = 256;   // 64 columns x 4 digits per row
 
@@ -84,14 +93,16 @@ __device__ __forceinline__ void transpose4(v4i (&q)[4]) {
   swap16(q[2], q[3]);
 }
 
+// One segment: the product of all rows of A with B rows n0 .. n0 + 16 NT - 1
+// over stages [k0, k1) (64 columns each), written through the epilogue, or
+// added into C atomically when `atomic` (EPI_STORE after C was cleared, or
+// EPI_ACCUM). Every thread of the workgroup must call it.
 template <int MT, int NT, int DB, int EPI>
-__global__ __launch_bounds__(NTHREADS) void ring_gemm_skinny_kernel(GemmLaunch g) {
+__device__ __forceinline__ void skinny_segment(const GemmLaunch& g, uint32_t (*red)[MT * NT * 4][64], int64_t n0,
+                                               int k0, int k1, bool atomic) {
   constexpr int NOUT = MT * NT * 4;   // output registers per lane
-  __shared__ uint32_t red[NWAVES][NOUT][64];
-
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t n0 = (int64_t)blockIdx.x * (16 * NT);
   const int64_t rows_b = (g.N - n0) < 16 * NT ? (g.N - n0) : 16 * NT;
   const __amdgpu_buffer_rsrc_t rb = rsrc(g.b + n0 * g.b_pitch, rows_b * g.b_pitch);
   const __amdgpu_buffer_rsrc_t ra = rsrc(g.a, g.M * g.a_pitch);
@@ -104,10 +115,10 @@ __global__ __launch_bounds__(NTHREADS) void ring_gemm_skinny_kernel(GemmLaunch g
 #pragma unroll
   for (int i = 0; i < MT; ++i) oa[i] = (i * 16 + r) * (int)g.a_pitch + h * 16;
 
-  const int stages = (int)(g.Kp / 64);
-  const int per = (stages + NWAVES - 1) / NWAVES;
-  const int s0 = wave * per;
-  const int s1 = (s0 + per) < stages ? (s0 + per) : stages;
+  // this wave's share [s0, s1) of the stages [k0, k1)
+  const int per = (k1 - k0 + NWAVES - 1) / NWAVES;
+  const int s0 = k0 + wave * per < k1 ? k0 + wave * per : k1;
+  const int s1 = (s0 + per) < k1 ? (s0 + per) : k1;
 
   v4i acc[MT][NT][4];
 #pragma unroll
@@ -129,14 +140,13 @@ __global__ __launch_bounds__(NTHREADS) void ring_gemm_skinny_kernel(GemmLaunch g
     _Pragma("unroll") for (int t = 0; t < 4; ++t) fa[SET][i][t] = load16(ra, oa[i] + so_ + 64 * t); \
   } while (0)
 
-    // limb pairs (a, b) with a + b <= 3, ordered so that one shift class
-    // never feeds two MFMAs in a row
+    // limb pairs (a, b) with a + b <= 3, grouped by the digit of B
 #define SKINNY_MFMA(SET)                                                                   \
   do {                                                                                     \
     _Pragma("unroll") for (int j = 0; j < NT; ++j) transpose4(fb[SET][j]);                 \
     _Pragma("unroll") for (int i = 0; i < MT; ++i) transpose4(fa[SET][i]);                 \
-    constexpr int ta_[10] = {0, 0, 0, 1, 1, 0, 2, 2, 1, 3};                                \
-    constexpr int tb_[10] = {3, 2, 1, 2, 1, 0, 1, 0, 0, 0};                                \
+    constexpr int ta_[10] = {0, 1, 2, 3, 0, 1, 2, 0, 1, 0};                                \
+    constexpr int tb_[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};                                \
     _Pragma("unroll") for (int p = 0; p < 10; ++p)                                         \
     _Pragma("unroll") for (int i = 0; i < MT; ++i)                                         \
     _Pragma("unroll") for (int j = 0; j < NT; ++j)                                         \
@@ -193,8 +203,115 @@ __global__ __launch_bounds__(NTHREADS) void ring_gemm_skinny_kernel(GemmLaunch g
     const int i = q / (NT * 4), j = (q / 4) % NT, v = q % 4;
     const int64_t m = i * 16 + 4 * (l >> 4) + v;
     const int64_t n = n0 + j * 16 + (l & 15);
-    if (m < g.M && n < g.N) gemm_epilogue<EPI>(g, m, n, val);
+    if (m < g.M && n < g.N) {
+      if (atomic) atomicAdd(&g.c[m * g.ldc + n], val);
+      else gemm_epilogue<EPI>(g, m, n, val);
+    }
   }
+}
+
+// Work assignment, one of two; either way a workgroup walks a contiguous
+// range [u, u1) of (column tile, stage) pairs, tile by tile, one segment per
+// tile it touches:
+//  * tiles (units == 0): workgroup b takes column tile b / ks and part b % ks
+//    of its K range (ks == 1 for the unmask epilogue, which cannot be split);
+//  * balanced (units > 0): the units pairs are cut into gridDim.x equal
+//    ranges, so no grid shape leaves a nearly empty last round of
+//    workgroups; every segment is added into C atomically.
+// K must be non-zero (stages > 0).
+template <int MT, int NT, int DB, int EPI, bool BAL>
+__global__ __launch_bounds__(NTHREADS) void ring_gemm_skinny_kernel(GemmLaunch g, int ks, int64_t units) {
+  __shared__ uint32_t red[NWAVES][MT * NT * 4][64];
+  const int64_t stages = g.Kp / 64;
+  if constexpr (!BAL) {
+    // one segment per workgroup (no loop: the widest tiles use every register)
+    const int64_t tile = blockIdx.x / (unsigned)ks;
+    const int64_t part = blockIdx.x % (unsigned)ks;
+    const int64_t kper = (stages + ks - 1) / ks;
+    const int64_t k0 = part * kper < stages ? part * kper : stages;
+    const int64_t k1 = (k0 + kper) < stages ? (k0 + kper) : stages;
+    skinny_segment<MT, NT, DB, EPI>(g, red, tile * (16 * NT), (int)k0, (int)k1, ks > 1);
+    return;
+  }
+  int64_t u, u1;
+  bool atomic;
+  if (units == 0) {
+    const int64_t tile = blockIdx.x / (unsigned)ks;
+    const int64_t part = blockIdx.x % (unsigned)ks;
+    const int64_t kper = (stages + ks - 1) / ks;
+    const int64_t k0 = part * kper < stages ? part * kper : stages;
+    const int64_t k1 = (k0 + kper) < stages ? (k0 + kper) : stages;
+    u = tile * stages + k0;
+    u1 = tile * stages + k1;
+    atomic = ks > 1;
+  } else {
+    u = units * blockIdx.x / gridDim.x;
+    u1 = units * (blockIdx.x + 1) / gridDim.x;
+    atomic = true;
+  }
+  while (u < u1) {
+    const int64_t tile = u / stages;
+    const int a = (int)(u - tile * stages);
+    const int b = (u1 - u) < stages - a ? a + (int)(u1 - u) : (int)stages;
+    skinny_segment<MT, NT, DB, EPI>(g, red, tile * (16 * NT), a, b, atomic);
+    u += b - a;
+    __syncthreads();   // the next segment reuses red
+  }
+}
+
+__global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, int64_t M, int64_t N) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < M * N) c[(e / N) * ldc + e % N] = 0u;
+}
+
+int compute_units() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  if (dev >= 0 && dev < 64 && cached[dev] > 0) return cached[dev];
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+  if (dev >= 0 && dev < 64) cached[dev] = v;
+  return v;
+}
+
+// Work assignment per launch. The unmask epilogue runs column tiles whole
+// (its partial products cannot be added into the output). The store and
+// accumulate epilogues use the balanced assignment over one workgroup per
+// compute unit (each with at least 4 stages), except that for A of at most
+// 16 rows with no more column tiles than compute units whole tiles are
+// faster (a sweep over the decode and mat-vec shapes: the balanced
+// assignment gained 10-35% where tiles exceed the compute units or A has 32
+// or 64 rows, and lost 5-15% on those small cases; more workgroups per
+// compute unit were slower). A plain store with partial products added
+// atomically clears C first. K = 0 leaves only the epilogue: C = 0, C
+// unchanged, or the unmask of a zero product.
+template <int MT, int NT, int DB, int EPI>
+hipError_t launch_cfg(const GemmLaunch& g, hipStream_t s) {
+  const int64_t tiles = (g.N + 16 * NT - 1) / (16 * NT);
+  const int64_t stages = g.Kp / 64;
+  const dim3 block(NTHREADS);
+  if (stages == 0) {
+    if (EPI == EPI_UNMASK) return launch_unmask_elementwise(g, s);
+    if (EPI == EPI_STORE)
+      hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc,
+                         g.M, g.N);
+    return hipGetLastError();
+  }
+  const int64_t cus = compute_units();
+  const int64_t units = tiles * stages;
+  if (EPI == EPI_UNMASK || (MT == 1 && tiles <= cus) || units < 8) {
+    hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, NT, DB, EPI, false>), dim3((unsigned)tiles), block, 0, s, g, 1,
+                       (int64_t)0);
+    return hipGetLastError();
+  }
+  const int64_t grid = cus < units / 4 ? cus : units / 4;
+  if (EPI == EPI_STORE)
+    hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc, g.M,
+                       g.N);
+  hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, NT, DB, EPI, true>), dim3((unsigned)grid), block, 0, s, g, 1,
+                     units);
+  return hipGetLastError();
 }
 
 template <int EPI>
@@ -202,16 +319,9 @@ hipError_t launch_epi(const GemmLaunch& g, hipStream_t s) {
   // MT: 16-row tiles of A (A padded to 16, 32 or 64 rows); NT: 16-row tiles
   // of B per workgroup; DB: double-buffered fragments.
   const int mt = (int)((g.M + 15) / 16);
-  if (mt <= 1)
-    hipLaunchKernelGGL((ring_gemm_skinny_kernel<1, 1, 1, EPI>), dim3((unsigned)((g.N + 15) / 16)),
-                       dim3(NTHREADS), 0, s, g);
-  else if (mt == 2)
-    hipLaunchKernelGGL((ring_gemm_skinny_kernel<2, 1, 1, EPI>), dim3((unsigned)((g.N + 15) / 16)),
-                       dim3(NTHREADS), 0, s, g);
-  else
-    hipLaunchKernelGGL((ring_gemm_skinny_kernel<4, 2, 0, EPI>), dim3((unsigned)((g.N + 31) / 32)),
-                       dim3(NTHREADS), 0, s, g);
-  return hipGetLastError();
+  if (mt <= 1) return launch_cfg<1, 2, 1, EPI>(g, s);
+  if (mt == 2) return launch_cfg<2, 4, 0, EPI>(g, s);
+  return launch_cfg<4, 4, 0, EPI>(g, s);
 }
 
 }  // namespace

@@ -130,7 +130,9 @@ def test_masked_matmul(M, N, K):
 def test_masked_matmul_short_a(M, N, K):
     """Decode-shaped products (at most 64 rows of A take the K-split kernel):
     row counts on and around the 16-row tiles, ragged N, and K ranges that
-    leave some of the eight K slices short or empty."""
+    leave some of the waves' K slices short or empty; with these few column
+    tiles K is also split across 2-4 workgroups (K >= 512) whose partial
+    products are added atomically."""
     rng = _rng_np(M * 131 + N * 7 + K)
     a = _random_ring(rng, (M, K), edge=True)
     b = _random_ring(rng, (N, K), edge=True)
@@ -178,23 +180,26 @@ def test_masked_matmul_accumulator_extreme():
     assert np.all(got == ref)
 
 
-def test_masked_matmul_ldc_and_offsets():
+@pytest.mark.parametrize("M,K", [(70, 130), (40, 2000)])
+def test_masked_matmul_ldc_and_offsets(M, K):
     """Output with a leading dimension > N and operands at a column offset in
-    a wider digit buffer."""
-    rng = _rng_np(11)
-    M, N, K = 70, 50, 130
+    a wider digit buffer; C starts non-zero and only its M x N window may
+    change. M = 40 with K = 2000 takes the decode kernel with the K range
+    split across workgroups (C cleared, partial products added atomically)."""
+    rng = _rng_np(11 + M)
+    N = 50
     a = _random_ring(rng, (M, K))
     b = _random_ring(rng, (N, K))
     left = Digits.concat(M, [64, K])
     right = Digits.concat(N, [K, 100])
     m.mosaic_mask(to_dev_ring(a), None, None, M, K, out_dig=left[1])
     m.mosaic_mask(to_dev_ring(b), None, None, N, K, out_dig=right[0])
-    C = torch.zeros((M, N + 17), dtype=torch.int32, device="cuda")
+    C = torch.full((M, N + 17), 12345, dtype=torch.int32, device="cuda")
     m.mosaic_masked_matmul(left[1], right[0], M, N, K, C[:, 5:5 + N])
     torch.cuda.synchronize()
     got = to_np_u32(C)
     assert np.array_equal(got[:, 5:5 + N], ring_matmul(a, b.T))
-    assert np.all(got[:, :5] == 0) and np.all(got[:, 5 + N:] == 0)
+    assert np.all(got[:, :5] == 12345) and np.all(got[:, 5 + N:] == 12345)
 
 
 @pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192), (1, 300, 2560), (8, 33, 64),
