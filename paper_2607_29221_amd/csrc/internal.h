@@ -77,6 +77,18 @@ hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s
 // Products with at most SKINNY_MAX_M rows of A (decode shapes) run on a
 // kernel that streams B once and splits K inside each workgroup.
 constexpr int64_t SKINNY_MAX_M = 64;
+
+// Compute units of the current device (cached per device id).
+inline int compute_units() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  if (dev >= 0 && dev < 64 && cached[dev] > 0) return cached[dev];
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+  if (dev >= 0 && dev < 64) cached[dev] = v;
+  return v;
+}
 hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStream_t s);
 
 // Writes one recombined ring value of C = A B^T at (m, n) through the

@@ -264,16 +264,6 @@ __global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, 
   if (e < M * N) c[(e / N) * ldc + e % N] = 0u;
 }
 
-int compute_units() {
-  static int cached[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
-  if (dev >= 0 && dev < 64 && cached[dev] > 0) return cached[dev];
-  int v = 0;
-  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-  if (dev >= 0 && dev < 64) cached[dev] = v;
-  return v;
-}
 
 // Work assignment per launch. The unmask epilogue runs column tiles whole
 // (its partial products cannot be added into the output). The store and

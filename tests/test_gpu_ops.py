@@ -125,6 +125,16 @@ def test_masked_matmul(M, N, K):
     assert np.array_equal(got, ring_matmul(a, b.T))
 
 
+@pytest.mark.parametrize("M,N,K", [(200, 1000, 4096), (130, 3000, 2048)])
+def test_masked_matmul_mid_size(M, N, K):
+    """Tiled-kernel products with fewer tiles than compute units and a long
+    K range, checked in full."""
+    rng = _rng_np(M + N + K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
+
+
 @pytest.mark.parametrize("M", [1, 8, 15, 16, 17, 33, 48, 63, 64, 65])
 @pytest.mark.parametrize("N,K", [(33, 64), (100, 576), (16, 1000), (47, 4160)])
 def test_masked_matmul_short_a(M, N, K):
