@@ -142,6 +142,7 @@ def run_gpu(steps: int, warmup: int, extras: bool):
         out["extras"]["integrity_check"] = run_integrity(dev)
         out["extras"]["matvec_sweep"] = run_matvec_sweep(dev)
         out["extras"]["vendor_int8_gemm"] = run_vendor_int8(dev)
+        out["extras"]["client_overhead"] = run_client_overhead(dev)
     return out
 
 
@@ -378,6 +379,77 @@ def run_matvec_sweep(dev):
                     "client_online_ms": round(t[1] + t[3], 4), "init_x_ms": round(t[0], 4),
                     "total_ms": round(sum(t), 4)})
         del w, buf
+    return out
+
+
+def run_client_overhead(dev):
+    """The paper's outsourcing-efficiency sweep on one GPU: for eight model
+    shapes (attention output projection, MLP up, MLP down), the client's
+    runtime per one-token call -- Init X batched over 512 calls and divided
+    by 512, plus the online mask and unmask -- against computing W x
+    locally on the same GPU, as a bf16 matrix-vector product (torch.mv) and
+    as the same Z_2^32 product on plaintext digits (the local baseline is a
+    reading: the paper does not state its arithmetic). Depth-1 mask of rank
+    1536, sigma 0.5; HIP-event means over 20 calls."""
+    import torch
+
+    from paper_2607_29221_amd import mosaic as m
+    from paper_2607_29221_amd import protocol as gp
+    from paper_2607_29221_amd.mosaic import Digits
+    from synthetic_inputs import (OVERHEAD_BATCH, OVERHEAD_MODELS, OVERHEAD_SEED, PARAMS_PAPER_D1,
+                                  int8_matrix_device)
+
+    out, reps = [], 20
+    for mi, (name, d, attn_in, f) in enumerate(OVERHEAD_MODELS):
+        for kind, K, N in (("attn proj", attn_in, d), ("MLP up", d, f), ("MLP down", f, d)):
+            W = int8_matrix_device(N, K, OVERHEAD_SEED + 3 * mi, dev)
+            x = int8_matrix_device(1, K, OVERHEAD_SEED + 3 * mi + 1, dev)
+            w = gp.MaskedWeight(W, PARAMS_PAPER_D1, 0x6D6F736169630000 | (OVERHEAD_SEED + mi), weight_id=mi)
+            Wb = W.to(torch.bfloat16)
+            xb = x[0].to(torch.bfloat16)
+            Wd, xd = Digits.empty(N, K, dev), Digits.empty(1, K, dev)
+            m.mosaic_mask(W, None, None, N, K, out_dig=Wd)
+            m.mosaic_mask(x, None, None, 1, K, out_dig=xd)
+            yr = torch.empty((1, N), dtype=torch.int32, device=dev)
+            del W
+            bufb = gp.alloc_call(w, OVERHEAD_BATCH, dev)
+            buf1 = gp.alloc_call(w, 1, dev)
+            gp.init_x(w, 1, 1, buf1)
+            for i in range(2):
+                gp.init_x(w, OVERHEAD_BATCH, 2 + i, bufb)
+                gp.mask(w, x, 2 + i, buf1)
+                gp.unmask(w, 1, buf1)
+                torch.mv(Wb, xb)
+                m.mosaic_masked_matmul(xd, Wd, 1, N, K, yr)
+            torch.cuda.synchronize()
+            e = _events(6)
+            e[0].record()
+            for i in range(4):
+                gp.init_x(w, OVERHEAD_BATCH, 10 + i, bufb)
+            e[1].record()
+            for i in range(reps):
+                gp.mask(w, x, 20 + i, buf1)
+            e[2].record()
+            for i in range(reps):
+                gp.unmask(w, 1, buf1)
+            e[3].record()
+            for i in range(reps):
+                torch.mv(Wb, xb)
+            e[4].record()
+            for i in range(reps):
+                m.mosaic_masked_matmul(xd, Wd, 1, N, K, yr)
+            e[5].record()
+            torch.cuda.synchronize()
+            init_x = e[0].elapsed_time(e[1]) / 4 / OVERHEAD_BATCH
+            online = e[1].elapsed_time(e[2]) / reps + e[2].elapsed_time(e[3]) / reps
+            local = e[3].elapsed_time(e[4]) / reps
+            local_ring = e[4].elapsed_time(e[5]) / reps
+            out.append({"model": name, "matrix": kind, "K": K, "N": N, "init_x_ms_per_call": round(init_x, 5),
+                        "online_ms": round(online, 5), "local_bf16_mv_ms": round(local, 5),
+                        "local_ring_mv_ms": round(local_ring, 5),
+                        "client_over_local": round((init_x + online) / local, 4),
+                        "client_over_local_ring": round((init_x + online) / local_ring, 4)})
+            del w, Wb, xb, bufb, buf1, Wd, xd, yr
     return out
 
 

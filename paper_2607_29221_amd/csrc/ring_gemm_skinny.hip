@@ -269,11 +269,12 @@ __global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, 
 // (its partial products cannot be added into the output). The store and
 // accumulate epilogues use the balanced assignment over one workgroup per
 // compute unit (each with at least 4 stages), except that for A of at most
-// 16 rows with no more column tiles than compute units whole tiles are
-// faster (a sweep over the decode and mat-vec shapes: the balanced
-// assignment gained 10-35% where tiles exceed the compute units or A has 32
-// or 64 rows, and lost 5-15% on those small cases; more workgroups per
-// compute unit were slower). A plain store with partial products added
+// 16 rows with between 5/8 of and as many column tiles as compute units
+// whole tiles are faster (a sweep over the decode and mat-vec shapes: the
+// balanced assignment gained 10-35% where tiles exceed the compute units or
+// A has 32 or 64 rows, and lost 5-15% with 176-208 tiles; more workgroups
+// per compute unit were slower; with 64 tiles whole tiles left three
+// quarters of the compute units idle, 2.5x slower). A plain store with partial products added
 // atomically clears C first. K = 0 leaves only the epilogue: C = 0, C
 // unchanged, or the unmask of a zero product.
 template <int MT, int NT, int DB, int EPI>
@@ -290,7 +291,7 @@ hipError_t launch_cfg(const GemmLaunch& g, hipStream_t s) {
   }
   const int64_t cus = compute_units();
   const int64_t units = tiles * stages;
-  if (EPI == EPI_UNMASK || (MT == 1 && tiles <= cus) || units < 8) {
+  if (EPI == EPI_UNMASK || (MT == 1 && tiles <= cus && 8 * tiles >= 5 * cus) || units < 8) {
     hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, NT, DB, EPI, false>), dim3((unsigned)tiles), block, 0, s, g, 1,
                        (int64_t)0);
     return hipGetLastError();

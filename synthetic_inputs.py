@@ -167,6 +167,26 @@ DECODER_RING_SEED = 5
 MATVEC_N = (4096, 8192, 16384, 36864)
 MATVEC_SEED = 6
 
+# Client-overhead sweep (Section 7 outsourcing-efficiency figure, one token,
+# mask initialisation batched over 512 invocations). The figure gives only
+# each model's hidden size d; the matrix shapes are taken from the models'
+# published configurations: the attention output projection (heads x head
+# dimension -> d), the MLP up projection (d -> f) and the MLP down
+# projection (f -> d), f the dense feed-forward width.
+# (name, d, attention heads x head dimension, f)
+OVERHEAD_MODELS = (
+    ("LLaMA-3.2 1B", 2048, 2048, 8192),
+    ("Gemma-2 27B", 4608, 4096, 36864),
+    ("LLaMA-4 Maverick", 5120, 5120, 16384),
+    ("Kimi-K2.5", 7168, 8192, 18432),
+    ("DeepSeek-V3", 7168, 16384, 18432),
+    ("LLaMA-3.1 70B", 8192, 8192, 28672),
+    ("GPT-3 175B", 12288, 12288, 49152),
+    ("LLaMA-3.1 405B", 16384, 16384, 53248),
+)
+OVERHEAD_BATCH = 512
+OVERHEAD_SEED = 8
+
 
 def int8_matrix_device(rows: int, cols: int, seed: int, device):
     """Uniform int8 in [-127, 127] drawn by torch's generator on ``device``
