@@ -456,14 +456,16 @@ def run_client_overhead(dev):
 def run_decode(dev):
     """Decode-shaped calls (M in {1, 8, 64} tokens; (K, N) in {4096^2,
     4096 x 14336, 14336 x 4096}; depth-2 mask of ranks (1536, 1024) with
-    density-1/64 sparse LPN level). Per shape and M: the server product
+    density-1/64 sparse LPN level, and the whole call also at depth 3 with
+    ranks (1536, 1024, 652), sparse mode). Per shape and M: the server product
     ([Y' | Q], N + 2560 output columns) and the whole call (Init X, mask,
     server, unmask), HIP-event means over 20 calls; GB/s counts the server
     product's operand and output bytes once."""
     import torch
 
     from paper_2607_29221_amd import protocol as gp
-    from synthetic_inputs import DECODE_KN, DECODE_M, DECODE_SEED, PARAMS_PAPER_D2_SPARSE, int8_operands
+    from synthetic_inputs import (DECODE_KN, DECODE_M, DECODE_SEED, PARAMS_PAPER_D2_SPARSE, PARAMS_PAPER_D3_SPARSE,
+                                  int8_operands)
 
     res = []
     reps = 20
@@ -472,6 +474,7 @@ def run_decode(dev):
         Wd = torch.from_numpy(W).to(dev)
         w = gp.MaskedWeight(Wd, PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + idx, weight_id=idx, sparse_lpn=False)
         ws = gp.MaskedWeight(Wd, PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + idx, weight_id=idx, sparse_lpn=True)
+        w3 = gp.MaskedWeight(Wd, PARAMS_PAPER_D3_SPARSE, 0xDEC0DE00 + idx, weight_id=idx, sparse_lpn=True)
         for M in DECODE_M:
             Ad = torch.from_numpy(A[:M].copy()).to(dev)
             buf = gp.alloc_call(w, M, dev)
@@ -481,8 +484,11 @@ def run_decode(dev):
             bufs = gp.alloc_call(ws, M, dev)
             for i in range(3):
                 gp.run_call(ws, Ad, 10_000 + i, bufs)
+            buf3 = gp.alloc_call(w3, M, dev)
+            for i in range(3):
+                gp.run_call(w3, Ad, 10_000 + i, buf3)
             torch.cuda.synchronize()
-            e = _events(4)
+            e = _events(5)
             e[0].record()
             for i in range(reps):
                 gp.server(w, M, buf)
@@ -493,6 +499,9 @@ def run_decode(dev):
             for i in range(reps):
                 gp.run_call(ws, Ad, 20_000 + i, bufs)
             e[3].record()
+            for i in range(reps):
+                gp.run_call(w3, Ad, 20_000 + i, buf3)
+            e[4].record()
             # phases of the sparse-mode call: Init X is input independent (it
             # can run ahead of the token); mask, server and unmask are online
             ph = _events(4)
@@ -509,6 +518,7 @@ def run_decode(dev):
             server_ms = e[0].elapsed_time(e[1]) / reps
             call_ms = e[1].elapsed_time(e[2]) / reps
             call_sparse_ms = e[2].elapsed_time(e[3]) / reps
+            call_d3_ms = e[3].elapsed_time(e[4]) / reps
             init_x_ms = ph[0].elapsed_time(ph[1]) / reps
             online_ms = ph[1].elapsed_time(ph[2]) / reps
             Kp = 64 * ((K + 63) // 64)
@@ -518,9 +528,10 @@ def run_decode(dev):
                         "server_hbm_frac": round(byts / (server_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
                         "call_us": round(call_ms * 1e3, 2),
                         "call_us_sparse_lpn": round(call_sparse_ms * 1e3, 2),
+                        "call_us_d3_sparse_lpn": round(call_d3_ms * 1e3, 2),
                         "init_x_us_sparse_lpn": round(init_x_ms * 1e3, 2),
                         "online_us_sparse_lpn": round(online_ms * 1e3, 2)})
-        del w, ws
+        del w, ws, w3
     return res
 
 

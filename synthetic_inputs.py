@@ -61,6 +61,9 @@ PARAMS_D3_SPARSE_SMALL = ProtocolParams(ranks=(192, 128, 64), noise=NoiseSpec("d
 PARAMS_PAPER_D1 = ProtocolParams(ranks=(1536,), noise=NoiseSpec("dgauss", 0.5, 4))
 # Depth 2 with the paper's first two ranks (1536, 1024), sparse, no E.
 PARAMS_PAPER_D2_SPARSE = ProtocolParams(ranks=(1536, 1024), noise=NoiseSpec("zero", 0.0, 0))
+# Depth 3 with the paper's ranks (1536, 1024, 652) (Section 4.2 example
+# parameterisation), sparse levels at density 1/64, no E.
+PARAMS_PAPER_D3_SPARSE = ProtocolParams(ranks=(1536, 1024, 652), noise=NoiseSpec("zero", 0.0, 0))
 
 
 # ---------------------------------------------------------------------------

@@ -11,8 +11,9 @@ from oracle import sampling as smp
 from oracle.ring import lift, ring_add, ring_matmul, ring_sub
 from paper_2607_29221_amd import mosaic as m
 from paper_2607_29221_amd import protocol as gproto
-from synthetic_inputs import (PARAMS_D2_SPARSE, PARAMS_D3_SPARSE_SMALL, PARAMS_PAPER_D2_SPARSE, DECODE_KN,
-                              DECODE_M, DECODE_SEED, NoiseSpec, ProtocolParams, int8_operands)
+from synthetic_inputs import (PARAMS_D2_SPARSE, PARAMS_D3_SPARSE_SMALL, PARAMS_PAPER_D2_SPARSE,
+                              PARAMS_PAPER_D3_SPARSE, DECODE_KN, DECODE_M, DECODE_SEED, NoiseSpec, ProtocolParams,
+                              int8_operands)
 from tests.gpu_util import to_dev_ring, to_np_u32
 
 pytestmark = pytest.mark.gpu
@@ -129,6 +130,21 @@ def test_sparse_mode_decode_exact(shape_id):
     A, W = int8_operands(max(DECODE_M), K, N, DECODE_SEED)
     w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), PARAMS_PAPER_D2_SPARSE, 0xDEC0DE00 + shape_id, shape_id,
                             sparse_lpn=True)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    for Mi in DECODE_M:
+        buf = gproto.run_call(w, torch.from_numpy(np.ascontiguousarray(A[:Mi])).cuda(), call_id=Mi)
+        torch.cuda.synchronize()
+        assert np.array_equal(buf.Y.cpu().numpy().astype(np.float64), ref[:Mi])
+
+
+@pytest.mark.parametrize("sparse", [True, False])
+def test_paper_depth3_decode_exact(sparse):
+    """The paper's depth-3 ranks (1536, 1024, 652; the last padded to 704
+    digit columns) at the 4096 x 4096 decode shape, E = 0: Y equals A W^T
+    exactly for every token count, in sparse and dense mode."""
+    K, N = DECODE_KN[0]
+    A, W = int8_operands(max(DECODE_M), K, N, DECODE_SEED)
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), PARAMS_PAPER_D3_SPARSE, 0xDEC0DE30, 3, sparse_lpn=sparse)
     ref = A.astype(np.float64) @ W.astype(np.float64).T
     for Mi in DECODE_M:
         buf = gproto.run_call(w, torch.from_numpy(np.ascontiguousarray(A[:Mi])).cuda(), call_id=Mi)
