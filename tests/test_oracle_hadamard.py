@@ -7,7 +7,8 @@ import numpy as np
 import pytest
 import scipy.linalg
 
-from oracle.hadamard import fwht_unnormalised, rotate, sylvester_matrix
+from oracle.hadamard import (fwht_unnormalised, gf27_mul, gf27_quadratic_character, gf27_sub, paley_hadamard_28,
+                             rotate, rotate_kron28, sylvester_matrix)
 from oracle.sampling import sample_signs
 from synthetic_inputs import outlier_activations
 
@@ -87,3 +88,67 @@ def test_variance_reduction_figure():
     with open(GOLDEN) as f:
         g = json.load(f)["variance_reduction_n4096"]
     assert abs(4096 / math.log2(4096) - g["value"]) <= g["tolerance"]
+
+
+def test_gf27_is_a_field():
+    """GF(3)[t] / (t^3 + 2 t + 1): the modulus has no root in GF(3) (so it is
+    irreducible, being cubic); the multiplicative group of the 26 non-zero
+    elements is cyclic-order compatible (a^26 = 1), every non-zero element
+    has exactly one inverse, the product is associative and distributes
+    over subtraction; 13 non-zero squares and chi(-1) = -1 (27 = 3 mod 4)."""
+    assert all((r ** 3 + 2 * r + 1) % 3 != 0 for r in range(3))
+    for a in range(1, 27):
+        p = 1
+        for _ in range(26):
+            p = gf27_mul(p, a)
+        assert p == 1
+        assert sum(gf27_mul(a, b) == 1 for b in range(1, 27)) == 1
+    rng = np.random.default_rng(27)
+    for a, b, c in rng.integers(0, 27, (200, 3)):
+        assert gf27_mul(gf27_mul(a, b), c) == gf27_mul(a, gf27_mul(b, c))
+        assert gf27_mul(a, gf27_sub(b, c)) == gf27_sub(gf27_mul(a, b), gf27_mul(a, c))
+    chi = gf27_quadratic_character()
+    assert (chi == 1).sum() == 13 and (chi == -1).sum() == 13
+    assert chi[gf27_sub(0, 1)] == -1
+
+
+def test_paley_28_is_a_hadamard_matrix():
+    """Entries +-1 and H H^T = 28 I exactly; H = I + S with S skew-symmetric
+    (a skew-Hadamard matrix, as Paley's first construction gives)."""
+    H = paley_hadamard_28()
+    assert set(np.unique(H)) == {-1, 1}
+    assert np.array_equal(H @ H.T, 28 * np.eye(28, dtype=np.int64))
+    S = H - np.eye(28, dtype=np.int64)
+    assert np.array_equal(S, -S.T)
+
+
+@pytest.mark.parametrize("b", [4, 16])
+def test_kron28_rotation_matches_explicit_kronecker(b):
+    """The row rotation equals the explicit matrix (H_28 (x) H_b) / sqrt(28 b)
+    (numpy's Kronecker product, scipy's Sylvester H_b) applied to d * x, and
+    its inverse applies the transpose and then d."""
+    n = 28 * b
+    rng = np.random.default_rng(b)
+    x = rng.standard_normal((3, n))
+    d = np.where(rng.random(n) < 0.5, -1.0, 1.0)
+    K = np.kron(paley_hadamard_28().astype(np.float64), scipy.linalg.hadamard(b).astype(np.float64)) / math.sqrt(n)
+    assert np.allclose(rotate_kron28(x, d), (K @ (x * d).T).T, atol=1e-12)
+    assert np.allclose(rotate_kron28(x, d, inverse=True), (K.T @ x.T).T * d, atol=1e-12)
+
+
+def test_kron28_roundtrip_norm_and_outliers():
+    """n = 28672 = 28 x 1024: orthogonal (round trip, norms), and on outlier
+    rows the peak-to-RMS ratio falls at least as far as with the
+    block-diagonal rotation I_28 (x) H_1024, which mixes only within blocks."""
+    n = 28672
+    x = outlier_activations(16, n, seed=5)
+    d = sample_signs(n, 5)
+    y = rotate_kron28(x, d)
+    assert np.allclose(rotate_kron28(y, d, inverse=True), x, atol=1e-9)
+    assert np.allclose(np.linalg.norm(y, axis=1), np.linalg.norm(x.astype(np.float64), axis=1), rtol=1e-12)
+
+    def ratio(v):
+        return np.max(np.abs(v), axis=1) / np.sqrt(np.mean(v ** 2, axis=1))
+    kron, blockdiag = ratio(y), ratio(rotate(x, d, block=1024))
+    assert np.median(kron) <= np.median(blockdiag) + 1e-9
+    assert np.all(kron < math.sqrt(2 * math.log(2 * n)) + 1.0)
