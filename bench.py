@@ -148,7 +148,8 @@ def run_gpu(steps: int, warmup: int, extras: bool):
 
 def run_extras(dev):
     """Stand-alone passes at their own shapes: the rotation of a 4096 x 8192
-    fp32 activation (forward), the mask pass at the largest prefill shape
+    fp32 activation (forward), the rotations of a 4096 x 28672 activation
+    (H_28 (x) H_1024 and the block-diagonal forms), the mask pass at the largest prefill shape
     (with and without E_a), the three samplers writing digits at that shape,
     and the quantisation of a 4096 x 8192 fp32 activation. Buffers rotate
     through more than the 256 MB last-level cache."""
@@ -177,6 +178,38 @@ def run_extras(dev):
     res["fwht_4096x8192_us"] = round(t * 1e3, 2)
     res["fwht_gbs"] = round(rows * n * 8 / (t * 1e-3) / 1e9, 1)
     res["fwht_hbm_frac"] = round(res["fwht_gbs"] / HBM_PEAK_GBS, 3)
+    del xs, ys
+
+    # n = 28672 = 28 x 1024: H_28 (x) H_1024 against the block-diagonal
+    # rotations I_7 (x) H_4096 and I_28 (x) H_1024 (time, and the median
+    # max/RMS ratio of outlier rows after each)
+    from synthetic_inputs import outlier_activations
+    n28 = 28672
+    xs = [torch.randn(rows, n28, device=dev) for _ in range(2)]
+    xs[0][:64] = torch.from_numpy(outlier_activations(64, n28, seed=3)).to(dev)
+    ys = [torch.empty_like(xs[0]) for _ in range(2)]
+    s28 = torch.empty(n28, dtype=torch.int8, device=dev)
+    m.mosaic_sample_signs(m.rng(3, 0x70, 1, 0), n28, s28)
+    variants = (("kron28", lambda a, b: m.mosaic_hadamard28_rotate(a, b, signs=s28)),
+                ("blockdiag4096", lambda a, b: m.mosaic_hadamard_rotate(a, b, block=4096, signs=s28)),
+                ("blockdiag1024", lambda a, b: m.mosaic_hadamard_rotate(a, b, block=1024, signs=s28)))
+    res["rotation_28672"] = []
+    for name, fn in variants:
+        for i in range(3):
+            fn(xs[i % 2], ys[i % 2])
+        e0, e1 = _events(2)
+        e0.record()
+        for i in range(reps):
+            fn(xs[i % 2], ys[i % 2])
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps
+        fn(xs[0], ys[0])
+        v = ys[0][:64].double()
+        peak = (v.abs().amax(dim=1) / v.pow(2).mean(dim=1).sqrt()).median().item()
+        res["rotation_28672"].append({"variant": name, "us": round(t * 1e3, 2),
+                                      "gbs": round(rows * n28 * 8 / (t * 1e-3) / 1e9, 1),
+                                      "outlier_max_over_rms_median": round(peak, 3)})
     del xs, ys
 
     M, K = 2048, 28672

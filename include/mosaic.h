@@ -271,6 +271,23 @@ mosaic_status mosaic_hadamard_rotate(const float* x, int64_t ldx, float* y, int6
                                      int64_t rows, int64_t n, int64_t block,
                                      const int8_t* signs, int32_t inverse, void* stream);
 
+/* a7, for n = 28 b (e.g. 28672 = 28 x 1024): rotation by H_28 (x) H_b, which
+ * mixes every entry of a row (Section 5's rotation for a length that is not
+ * a power of two; the block-diagonal form above mixes only within blocks).
+ * Entry i b + j of a row v is entry j of block i:
+ *     forward:  y = (H_28 (x) H_b) (d * v) / sqrt(n)
+ *     inverse:  y = d * ((H_28^T (x) H_b) v) / sqrt(n)   (undoes forward)
+ * H_b is Sylvester-ordered as above; H_28 is Paley's first construction over
+ * GF(27) = GF(3)[t]/(t^3 + 2t + 1): H = I + S, S = [[0, 1^T], [-1, Q]],
+ * Q[i][k] = chi(e_i - e_k) with chi the quadratic character and e_i the
+ * element whose coefficients of 1, t, t^2 are the base-3 digits of i
+ * (H H^T = 28 I). b must be 256, 512 or 1024 (else MOSAIC_ERR_UNSUPPORTED).
+ * signs: n entries +-1 or NULL. Pointers, alignment, leading dimensions and
+ * in-place use as for mosaic_hadamard_rotate. fp32 throughout. */
+mosaic_status mosaic_hadamard28_rotate(const float* x, int64_t ldx, float* y, int64_t ldy,
+                                       int64_t rows, int64_t n,
+                                       const int8_t* signs, int32_t inverse, void* stream);
+
 /* a8. Per-row fixed-point quantisation (Pi_Sec-Linear, Init W step 2 and
  * online step 1): s_i = max_j |x(i, j)| / qmax (1 for an all-zero row),
  * q(i, j) = round-half-even(x(i, j) / s_i), both in fp32 arithmetic.

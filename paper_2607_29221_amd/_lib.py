@@ -56,6 +56,7 @@ _SIGNATURES = {
     "mosaic_sparse_gather_cols": ([c_i64, c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr, c_i64, c_i32, c_ptr],
                                   c_i32),
     "mosaic_hadamard_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
+    "mosaic_hadamard28_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
     "mosaic_quantize_rows": ([c_ptr, c_i64, c_i64, c_i64, c_i32, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_ptr],
                              c_i32),
 }

@@ -424,6 +424,33 @@ mosaic_status mosaic_hadamard_rotate(const float* x, int64_t ldx, float* y, int6
                     "hadamard launch");
 }
 
+mosaic_status mosaic_hadamard28_rotate(const float* x, int64_t ldx, float* y, int64_t ldy, int64_t rows, int64_t n,
+                                       const int8_t* signs, int32_t inverse, void* stream) {
+  if (rows < 0 || n < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || n == 0) return MOSAIC_OK;
+  if (x == nullptr || y == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "x or y is NULL");
+  if (!aligned16(x) || !aligned16(y)) return fail(MOSAIC_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
+  const int64_t b = n / 28;
+  int lb = 0;
+  while ((int64_t(1) << lb) < b) ++lb;
+  if (n % 28 != 0 || (int64_t(1) << lb) != b || !hadamard28_supported(lb))
+    return fail(MOSAIC_ERR_UNSUPPORTED, "n = %lld must be 28 b with b in {256, 512, 1024}", (long long)n);
+  if (ldx < n || ldy < n || ldx % 4 != 0 || ldy % 4 != 0)
+    return fail(MOSAIC_ERR_INVALID_ARG, "ldx and ldy must be >= n and multiples of 4");
+  if (signs != nullptr && !aligned16(signs)) return fail(MOSAIC_ERR_INVALID_ARG, "signs must be 16-byte aligned");
+  if (rows >= (int64_t(1) << 31)) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  {
+    const char* xb = (const char*)x;
+    const char* xe = (const char*)(x + (rows - 1) * ldx + n);
+    const char* yb = (const char*)y;
+    const char* ye = (const char*)(y + (rows - 1) * ldy + n);
+    if ((const float*)x != y && xb < ye && yb < xe) return fail(MOSAIC_ERR_INVALID_ARG, "x and y overlap");
+    if ((const float*)x == y && ldx != ldy) return fail(MOSAIC_ERR_INVALID_ARG, "in place needs ldx == ldy");
+  }
+  return hip_status(launch_hadamard28(x, ldx, y, ldy, rows, lb, signs, inverse != 0, (hipStream_t)stream),
+                    "hadamard28 launch");
+}
+
 mosaic_status mosaic_quantize_rows(const float* x, int64_t ldx, int64_t rows, int64_t n, int32_t qmax, int32_t* q,
                                    int64_t ldq, int8_t* q_dig, int64_t q_pitch, float* scale, void* stream) {
   if (rows < 0 || n < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");

@@ -157,12 +157,13 @@ __device__ __forceinline__ void reg_stage(float (&v)[E]) {
 // row swaps and run in registers. The stages on wave bits (index bits 8 and
 // 9, present for b >= 512) go through one LDS pass, whose write addresses
 // undo the two exchanges; for b <= 256 the exchanges are swapped back.
+// The stages that stay inside the wave (registers, lanes), for one block;
+// returns the lane sign c. For b >= 512 the element layout is left with the
+// two lane/register exchanges in place (the LDS pass undoes them).
 template <int LOGB>
-__device__ __forceinline__ float fwht_transform(float* sm, float (&v)[FwhtShape<LOGB>::E]) {
+__device__ __forceinline__ float fwht_in_wave(float (&v)[FwhtShape<LOGB>::E], int lane) {
   using S = FwhtShape<LOGB>;
-  constexpr int T = S::T, LOGT = S::LOGT, E = S::E;
-  const int t = threadIdx.x;
-  const int lane = t & 63;
+  constexpr int LOGT = S::LOGT, E = S::E;
 
   // stages on the index bits held in registers: bits of r = 4 k + q
 #pragma unroll
@@ -194,11 +195,40 @@ __device__ __forceinline__ float fwht_transform(float* sm, float (&v)[FwhtShape<
     lane_exchange<32, 1>(v);
     reg_stage<1>(v);
   }
-
   if constexpr (LOGT <= 6) {
     if constexpr (LOGT > 5) lane_exchange<32, 1>(v);
     if constexpr (LOGT > 4) lane_exchange<16, 2>(v);
-  } else {
+  }
+  return c;
+}
+
+// In-place unscaled H_b of NB blocks held in the load layout (v[k] one block),
+// up to a sign per lane: returns c = +-1 such that the true result in every
+// register of this thread is c * v[k][r] (callers fold c into the scale they
+// apply anyway). Every thread of the workgroup (FwhtShape<LOGB>::T of them)
+// must call it; sm (NB x FwhtShape<LOGB>::SM floats) must not be in use by
+// other threads when it is called (it is untouched for b <= 256). The NB
+// blocks share the LDS pass, so its two barriers are paid once.
+//
+// Index bits of the element in register r of thread t (t = lane + 64 wave):
+// bits 0-1 are r % 4, bits 2 .. 1 + log2 T are t, the rest are r / 4. The
+// stages on register bits run in registers. Those on lane bits 0-3 (index
+// bits 2-5) take the partner's value by DPP or swizzle; those on lane bits 4
+// and 5 (index bits 6, 7) exchange the lane bit with register bit 1 or 0 by
+// row swaps and run in registers. The stages on wave bits (index bits 8 and
+// 9, present for b >= 512) go through one LDS pass, whose write addresses
+// undo the two exchanges; for b <= 256 the exchanges are swapped back.
+template <int LOGB, int NB>
+__device__ __forceinline__ float fwht_transform_blocks(float* sm, float (&v)[NB][FwhtShape<LOGB>::E]) {
+  using S = FwhtShape<LOGB>;
+  constexpr int T = S::T, LOGT = S::LOGT, E = S::E, SM = S::SM;
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  float c = 1.0f;
+#pragma unroll
+  for (int k = 0; k < NB; ++k) c = fwht_in_wave<LOGB>(v[k], lane);   // the same c for every block
+
+  if constexpr (LOGT > 6) {
     // Write every element at its index: register r of lane l now holds the
     // element of lane (l & 15) + 16 bit1(r) + 32 bit0(r), register
     // (r & ~3) + bit5(l) + 2 bit4(l). The per-register part of the index is a
@@ -206,40 +236,53 @@ __device__ __forceinline__ float fwht_transform(float* sm, float (&v)[FwhtShape<
     const int base = 4 * ((t & ~63) + (lane & 15)) + ((lane >> 5) & 1) + 2 * ((lane >> 4) & 1);
     const int pbase = fwht_pad(base);
 #pragma unroll
-    for (int r = 0; r < E; ++r) {
-      const int off = 64 * ((r >> 1) & 1) + 128 * (r & 1) + 4 * T * (r >> 2);
-      sm[pbase + off + (off >> 5)] = v[r];
-    }
+    for (int k = 0; k < NB; ++k)
+#pragma unroll
+      for (int r = 0; r < E; ++r) {
+        const int off = 64 * ((r >> 1) & 1) + 128 * (r & 1) + 4 * T * (r >> 2);
+        sm[k * SM + pbase + off + (off >> 5)] = v[k][r];
+      }
     __syncthreads();
     // wave bits [8, 2 + LOGT): one pass over groups of 2^e elements
     constexpr int p = 8, e = LOGT - 6, n_in = 1 << e, groups = E / n_in;
-    for (int gi = 0; gi < groups; ++gi) {
-      const int o = t + T * gi;
-      const int low = o & ((1 << p) - 1);
-      const int high = o >> p;
-      const int gbase = low | (high << (p + e));
-      float w[n_in];
 #pragma unroll
-      for (int i = 0; i < n_in; ++i) w[i] = sm[fwht_pad(gbase | (i << p))];
+    for (int k = 0; k < NB; ++k) {
+      for (int gi = 0; gi < groups; ++gi) {
+        const int o = t + T * gi;
+        const int low = o & ((1 << p) - 1);
+        const int high = o >> p;
+        const int gbase = low | (high << (p + e));
+        float w[n_in];
 #pragma unroll
-      for (int h = 1; h < n_in; h <<= 1) {
+        for (int i = 0; i < n_in; ++i) w[i] = sm[k * SM + fwht_pad(gbase | (i << p))];
 #pragma unroll
-        for (int i = 0; i < n_in; ++i) {
-          if ((i & h) == 0) {
-            const float a = w[i], b = w[i + h];
-            w[i] = a + b;
-            w[i + h] = a - b;
+        for (int h = 1; h < n_in; h <<= 1) {
+#pragma unroll
+          for (int i = 0; i < n_in; ++i) {
+            if ((i & h) == 0) {
+              const float a = w[i], b = w[i + h];
+              w[i] = a + b;
+              w[i + h] = a - b;
+            }
           }
         }
-      }
 #pragma unroll
-      for (int i = 0; i < n_in; ++i) sm[fwht_pad(gbase | (i << p))] = w[i];
+        for (int i = 0; i < n_in; ++i) sm[k * SM + fwht_pad(gbase | (i << p))] = w[i];
+      }
     }
     __syncthreads();
 #pragma unroll
-    for (int r = 0; r < E; ++r) v[r] = sm[fwht_pad(4 * (t + T * (r >> 2)) + (r & 3))];
+    for (int k = 0; k < NB; ++k)
+#pragma unroll
+      for (int r = 0; r < E; ++r) v[k][r] = sm[k * SM + fwht_pad(4 * (t + T * (r >> 2)) + (r & 3))];
   }
   return c;
+}
+
+// One block (see fwht_transform_blocks).
+template <int LOGB>
+__device__ __forceinline__ float fwht_transform(float* sm, float (&v)[FwhtShape<LOGB>::E]) {
+  return fwht_transform_blocks<LOGB, 1>(sm, reinterpret_cast<float (&)[1][FwhtShape<LOGB>::E]>(v));
 }
 
 }  // namespace mosaic

@@ -216,6 +216,9 @@ hipError_t launch_unmask_elementwise(const GemmLaunch& g, hipStream_t s);
 hipError_t launch_hadamard(const float* x, int64_t ldx, float* y, int64_t ldy, int64_t rows,
                            int64_t n, int log2_block, const int8_t* signs, int inverse,
                            hipStream_t s);
+bool hadamard28_supported(int log2_block);
+hipError_t launch_hadamard28(const float* x, int64_t ldx, float* y, int64_t ldy, int64_t rows, int log2_block,
+                             const int8_t* signs, int inverse, hipStream_t s);
 
 // Fused rotate + quantise + mask of Pi_Sec-Linear's input (secure_input.hip).
 bool rotate_quantize_mask_supported(int log2_block);

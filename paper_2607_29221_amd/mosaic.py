@@ -239,6 +239,14 @@ def mosaic_hadamard_rotate(x: torch.Tensor, y: torch.Tensor, block: Optional[int
                                               _stream()), "mosaic_hadamard_rotate")
 
 
+def mosaic_hadamard28_rotate(x: torch.Tensor, y: torch.Tensor, signs: Optional[torch.Tensor] = None,
+                             inverse: bool = False) -> None:
+    rows, n = x.shape
+    _check(_lib.load().mosaic_hadamard28_rotate(x.data_ptr(), x.stride(0), y.data_ptr(), y.stride(0), rows, n,
+                                                _ptr(signs), 1 if inverse else 0, _stream()),
+           "mosaic_hadamard28_rotate")
+
+
 def mosaic_quantize_rows(x: torch.Tensor, qmax: int, q: Optional[torch.Tensor] = None,
                          q_dig: Optional[Digits] = None, scale: Optional[torch.Tensor] = None) -> None:
     rows, n = x.shape

@@ -107,6 +107,22 @@ def test_unmask_validation(lib):
     assert call(R=40000, qp=4 * 40000 + 64, lp=4 * 40000 + 64) == UNSUPPORTED
 
 
+def test_hadamard28_validation(lib):
+    def call(x=FAKE, ldx=28672, y=FAKE + (1 << 24), ldy=28672, rows=2, n=28672, signs=None, inv=0):
+        return lib.mosaic_hadamard28_rotate(x, ldx, y, ldy, rows, n, signs, inv, None)
+    assert call(n=28 * 100, ldx=2800, ldy=2800) == UNSUPPORTED   # b not a power of two
+    assert call(n=28 * 2048, ldx=57344, ldy=57344) == UNSUPPORTED
+    assert call(n=28 * 128, ldx=3584, ldy=3584) == UNSUPPORTED
+    assert call(n=1000, ldx=1000, ldy=1000) == UNSUPPORTED        # not 28 b
+    assert call(ldx=28670) == INVALID
+    assert call(x=FAKE + 4) == INVALID                            # misaligned
+    assert call(y=FAKE + 64) == INVALID                           # overlapping, not in place
+    assert call(y=FAKE, ldy=28676) == INVALID                     # in place with different ld
+    assert call(x=None) == INVALID
+    assert call(signs=FAKE + 2) == INVALID
+    assert call(rows=0) == 0 and call(rows=-1) == INVALID
+
+
 def test_count_mismatches_validation(lib):
     assert lib.mosaic_count_mismatches(FAKE, 4, FAKE, 4, 2, 4, None, None) == INVALID      # no count
     assert lib.mosaic_count_mismatches(None, 4, FAKE, 4, 2, 4, FAKE, None) == INVALID

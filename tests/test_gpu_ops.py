@@ -274,6 +274,41 @@ def test_hadamard(rows, n, block, inverse):
     assert np.all(err <= 1e-5), err.max()
 
 
+@pytest.mark.parametrize("rows,b", [(3, 256), (2, 512), (5, 1024)])
+@pytest.mark.parametrize("inverse", [False, True])
+def test_hadamard28(rows, b, inverse):
+    """H_28 (x) H_b rotation (n = 28 b) against the oracle's float64
+    rotation: max relative error per row <= 1e-5."""
+    n = 28 * b
+    x = _rng_np(n + rows).standard_normal((rows, n)).astype(np.float32)
+    x[0, 5] *= 50.0
+    signs = smp.sample_signs(n, SEED, 2)
+    xd = torch.from_numpy(x).cuda()
+    y = torch.empty_like(xd)
+    m.mosaic_hadamard28_rotate(xd, y, signs=torch.from_numpy(signs).cuda(), inverse=inverse)
+    torch.cuda.synchronize()
+    ref = ohad.rotate_kron28(x.astype(np.float64), signs, inverse=inverse)
+    err = np.max(np.abs(y.cpu().numpy().astype(np.float64) - ref), axis=1) / np.max(np.abs(ref), axis=1)
+    assert np.all(err <= 1e-5), err.max()
+
+
+def test_hadamard28_in_place_roundtrip_and_no_signs():
+    rows, n = 4, 28672
+    x = _rng_np(28).standard_normal((rows, n)).astype(np.float32)
+    signs = torch.from_numpy(smp.sample_signs(n, SEED, 3)).cuda()
+    xd = torch.from_numpy(x).cuda()
+    m.mosaic_hadamard28_rotate(xd, xd, signs=signs)
+    m.mosaic_hadamard28_rotate(xd, xd, signs=signs, inverse=True)
+    torch.cuda.synchronize()
+    back = xd.cpu().numpy()
+    assert np.max(np.abs(back - x) / np.max(np.abs(x), axis=1, keepdims=True)) <= 1e-5
+    y = torch.empty((rows, n), dtype=torch.float32, device="cuda")
+    m.mosaic_hadamard28_rotate(torch.from_numpy(x).cuda(), y)
+    torch.cuda.synchronize()
+    ref = ohad.rotate_kron28(x.astype(np.float64), np.ones(n, dtype=np.int8))
+    assert np.max(np.abs(y.cpu().numpy() - ref) / np.max(np.abs(ref), axis=1, keepdims=True)) <= 1e-5
+
+
 def test_hadamard_in_place_roundtrip_and_no_signs():
     rows, n = 8, 8192
     x = _rng_np(9).standard_normal((rows, n)).astype(np.float32)
