@@ -572,8 +572,10 @@ def run_decoder_stack(dev):
     """Secure forward of the synthetic 70B-style stack (hidden 8192, 64/8
     heads, FFN 28672, 4 layers, 4096 tokens; int8 weights, depth-1 rank-1536
     mask, sigma = 0.5) against its float32 plaintext forward: per-layer
-    relative l2 error and cosine similarity, and forward times (Init W of the
-    16 weight matrices is outside the timed region)."""
+    relative l2 error and cosine similarity, forward times (Init W of the
+    16 weight matrices is outside the timed region), and the time split of
+    the secure forward by phase (Init X, input pass, server product, unmask
+    with dequantisation, and everything else)."""
     import torch
 
     from paper_2607_29221_amd import decoder as dec
@@ -596,6 +598,26 @@ def run_decoder_stack(dev):
         e[2].record()
         torch.cuda.synchronize()
         errs = [dec.error_metrics(g, r) for g, r in zip(got, ref)]
+        # time split of a further forward: the linear layers' phases from
+        # events at their boundaries, the rest (norms, attention, SwiGLU,
+        # residuals, buffer allocation) as the remainder
+        marks = []
+        for layer in sd.layers:
+            for lin in layer.values():
+                lin.phase_events = marks
+        f0, f1 = _events(2)
+        f0.record()
+        sd.forward(x)
+        f1.record()
+        torch.cuda.synchronize()
+        split = {"init_x": 0.0, "input": 0.0, "server": 0.0, "unmask": 0.0}
+        for (_, a), (name, b) in zip(marks, marks[1:]):
+            if name in split:
+                split[name] += a.elapsed_time(b)
+        total = f0.elapsed_time(f1)
+        split = {k: round(v, 2) for k, v in split.items()}
+        split["non_linear_and_other"] = round(total - sum(split.values()), 2)
+        split["total"] = round(total, 2)
     finally:
         torch.backends.cuda.matmul.allow_tf32 = prev
     tokens = DECODER["batch"] * DECODER["seq"]
@@ -605,6 +627,7 @@ def run_decoder_stack(dev):
             "secure_forward_ms": round(secure_ms, 2),
             "plaintext_fp32_forward_ms": round(e[1].elapsed_time(e[2]), 2),
             "secure_linear_ring_tops": round(2.0 * macs / (secure_ms * 1e-3) / 1e12, 2),
+            "time_split_ms": split,
             "per_layer": [{"rel_l2": round(v["rel_l2"], 5), "cosine": round(v["cosine"], 6)} for v in errs]}
 
 

@@ -78,6 +78,16 @@ class SecureLinear:
         self.last_scales: Optional[torch.Tensor] = None
         self.last_buf: Optional[gp.CallBuffers] = None
         self.fused = True                   # fused input pass when the shape allows
+        # When set to a list, each call appends (phase, event) pairs recorded
+        # on the current stream at the phase boundaries: "begin", "init_x",
+        # "input" (rotation, quantisation, mask), "server", "unmask".
+        self.phase_events: Optional[list] = None
+
+    def _mark(self, phase: str) -> None:
+        if self.phase_events is not None:
+            ev = torch.cuda.Event(enable_timing=True)
+            ev.record()
+            self.phase_events.append((phase, ev))
 
     def quantize_activations(self, x: torch.Tensor):
         """Rotated, quantised activations: (codes int32 M x K, scales M)."""
@@ -98,7 +108,9 @@ class SecureLinear:
             raise ValueError("x must be a contiguous float32 tensor (M x K)")
         M = x.shape[0]
         buf = gp.alloc_call(self.w, M, x.device)
+        self._mark("begin")
         gp.init_x(self.w, M, call_id, buf)
+        self._mark("init_x")
         codes = None
         done = False
         if self.fused and not keep_codes:
@@ -115,9 +127,12 @@ class SecureLinear:
         if not done:
             codes, s_x = self.quantize_activations(x)
             gp.mask(self.w, codes, call_id, buf)
+        self._mark("input")
         gp.server(self.w, M, buf)
+        self._mark("server")
         y = torch.empty((M, self.N), dtype=torch.float32, device=x.device)
         gp.unmask(self.w, M, buf, y_f32=y, s_rows=s_x, s_cols=self.s_w)
+        self._mark("unmask")
         if keep_codes:
             self.last_codes, self.last_scales, self.last_buf = codes, s_x, buf
         return y
