@@ -7,45 +7,44 @@
 // limb products with i + j <= 3 grouped by shift class into four int32
 // accumulators (the emulation of Section 6.1), recombined with wrap-around
 // arithmetic. Here the matrix instruction is v_mfma_i32_16x16x64_i8, so A is
-// padded only to 16, 32 or 64 rows.
+// padded only to 16, 32, 48 or 64 rows.
 //
-// Work decomposition. The unit of work is one (column tile, stage) pair: 16
-// NT rows of B (output columns) against all rows of A over 64 columns of K.
-// A workgroup of 4 waves walks a contiguous range of these pairs, one tile
-// segment at a time; its waves split each segment's stages into 4
-// contiguous parts. Each wave streams its part of B straight from memory
-// into registers (no reuse, so no LDS staging), reads the matching part of
-// A (shared by all workgroups, so it is served by the caches), and
-// multiplies. The partial products of the waves are summed in LDS with
-// wrap-around adds, which is exact in the ring. Wide tiles (NT = 2 for A of
-// at most 16 rows, 4 above) let each A fragment feed several B fragments:
-// every workgroup re-reads all of A, and for 64 tokens those re-reads, not
-// B, were the larger share of the traffic. A segment covering a whole tile
-// goes through the epilogue; otherwise (the balanced assignment, see
-// launch_cfg) partial products are added into C with 32-bit atomics, again
-// exact in the ring. Measured against one 16-row tile per workgroup of 8
-// waves with whole tiles: 20-24% less time for 8 tokens and 25-40% for 32
-// and 64 tokens at the decode shapes.
-
+// Two kernels:
+//
+// ring_gemm_skinny_kernel (store and accumulate epilogues). The unit of work
+// is one (column tile, stage) pair: 128 rows of B (output columns) against
+// all rows of A over 64 columns of K. The units are cut into one contiguous
+// range per compute unit, so every grid shape keeps the chip busy; a
+// workgroup walks its range tile by tile and adds each tile's partial
+// product into C with 32-bit atomics (exact in the ring; C is cleared first
+// for a plain store). Both operands of a stage are staged in LDS by direct
+// buffer-to-LDS loads, three stages resident and loads issued two stages
+// ahead, so data in flight costs no registers. The four waves of a
+// workgroup split the tile's columns (32 each): the A stage is fetched once
+// per workgroup and read from LDS by every wave, where a split of K between
+// the waves would fetch all of A once per wave and need a reduction of the
+// waves' partial products. Measured against that K-split design (B streamed
+// into registers): 20-26% less time for 16 and 32 tokens, 35% for 64, 4-10%
+// for one token, at the decode and mat-vec shapes.
+//
+// ring_gemm_skinny_unmask_kernel (unmask epilogue, whose inputs cannot take
+// partial products). One workgroup per column tile of 32 (A of at most 16
+// rows) or 64 rows of B computes the whole K range: its 4 waves split the
+// stages, stream their part of B straight into registers and sum their
+// partial products in LDS, then the tile goes through the epilogue.
+//
+// LDS layout (shared-A kernel). A stage row is 256 bytes: 4 groups of 16
+// columns, each holding its 4 digit planes in 64 consecutive bytes, i.e. 16
+// chunks of 16 bytes. Chunk c of row R sits in slot c ^ (R & 15), so 16
+// lanes reading one chunk of 16 consecutive rows touch all 64 banks once. A
+// direct load writes 64 consecutive 16-byte slots (4 rows); each lane
+// fetches the chunk that belongs to its slot.
+//
 // Operand fragments. For the 16 x 16 x 64 instruction, lane l supplies row
-// l % 16 and sixteen of the 64 k-slots, chosen by l / 16. In the digit layout
-// a group of 16 columns keeps its four digit planes in 64 consecutive bytes,
-// and a stage (64 columns) of a row is 256 consecutive bytes. Load t of a
-// wave reads bytes 64 t .. 64 t + 63 of the stage in all 16 rows (lane l takes
-// the 16 bytes at 64 t + 16 (l / 16)), so every load consumes whole 64-byte
-// segments; lane group h then holds digit h of column group t in register
-// quad t. A 4 x 4 transpose between lane groups and register quads (two
-// rounds of lane-swap instructions) turns that into digit t of column group
-// h in quad t: the fragment of digit t, with lane group h covering the
-// sixteen k-slots of column group h. A and B use the same k-slot assignment,
-// which is all the product needs.
-//
-// Pipelining. For A of up to 16 rows each wave keeps two stages of loads in
-// flight (the fragments of the next stage load while the current one
-// multiplies); with more rows the accumulators leave no registers for a
-// second set of fragments, and the hardware overlaps the waves instead. Prefetches past the
-// wave's last stage are clamped to that stage: the duplicate request hits in
-// cache and the loop needs no branches around loads.
+// l % 16 and sixteen of the 64 k-slots, chosen by h = l / 16. Lane (h, r)
+// takes chunk 4 h + t of row r for the fragment of digit t: digit t of
+// column group h. A and B use the same k-slot assignment, which is all the
+// product needs.
 #include "internal.h"
 
 namespace mosaic {
@@ -53,9 +52,183 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-constexpr int NWAVES = 4;
-constexpr int NTHREADS = 64 * NWAVES;
-constexpr int STAGE_BYTES = 256;   // 64 columns x 4 digits per row
+constexpr int ROWB = 256;   // bytes per row per stage: 64 columns x 4 digits
+
+// limb pairs (a, b) with a + b <= 3, grouped by the digit of B
+__device__ constexpr int kLimbA[10] = {0, 1, 2, 3, 0, 1, 2, 0, 1, 0};
+__device__ constexpr int kLimbB[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
+
+// ---------------------------------------------------------------------------
+// Shared-A kernel (store and accumulate epilogues)
+
+constexpr int SA_WAVES = 4;
+constexpr int SA_THREADS = 64 * SA_WAVES;
+constexpr int SA_NTW = 2;                          // 16-row B tiles per wave
+constexpr int SA_BN = SA_WAVES * SA_NTW * 16;      // B rows per column tile
+constexpr int SA_NS = 3;                           // stages resident in LDS
+
+// Direct buffer-to-LDS load of 16 bytes per lane: lane l writes LDS bytes
+// [lds_off + 16 l, lds_off + 16 l + 16). Inline assembly, so that the
+// compiler, which cannot tell these writes from later LDS reads, does not
+// drain every outstanding load before each read; completion is tracked by
+// hand (wait_vm) before the barrier that publishes a stage. M0 (the LDS
+// base) is set inside the same statement; nothing else in this kernel uses
+// M0.
+__device__ __forceinline__ void dma16(v4i rs, uint32_t lds_off, int voff, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds_off), "v"(voff), "s"(rs), "s"(soff) : "memory");
+}
+
+// Raw buffer descriptor over [base, base + bytes): out-of-range lanes read 0.
+__device__ __forceinline__ v4i make_rsrc(const void* base, int64_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  return v4i{(int)(uint32_t)b, (int)((uint32_t)(b >> 32) & 0xFFFFu), (int)bytes, (int)0x00020000u};
+}
+
+// s_waitcnt with only the vector-memory counter constrained: vmcnt(N)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup b computes units [units b / grid, units (b + 1) / grid) of the
+// tiles x stages (column tile, stage) pairs, tile-major. K must be non-zero.
+template <int MT>
+__global__ __launch_bounds__(SA_THREADS, 1) void ring_gemm_skinny_kernel(GemmLaunch g, int64_t units) {
+  constexpr int ASZ = 16 * MT * ROWB;              // A part of a stage
+  constexpr int STG = ASZ + SA_BN * ROWB;          // one stage
+  constexpr int QA = MT;                           // direct loads per wave per stage: A ...
+  constexpr int QB = 4 * SA_NTW;                   // ... and B (1 KiB each)
+  constexpr int QU = QA + QB;
+  static_assert(SA_NS * STG <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) char lds[SA_NS * STG];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t stages = g.Kp / 64;
+  const int64_t u0 = units * blockIdx.x / gridDim.x;
+  const int64_t cnt = units * (blockIdx.x + 1) / gridDim.x - u0;
+  if (cnt <= 0) return;
+
+  // direct loads: wave w fills A rows 4 MT w .. +4 MT and B rows 32 w .. +32
+  // of every stage, 4 rows per load
+  const int lr = lane >> 4, ls = lane & 15;
+  int va[QA], vb[QB];
+#pragma unroll
+  for (int q = 0; q < QA; ++q) {
+    const int R = wave * 4 * MT + 4 * q + lr;
+    va[q] = R * (int)g.a_pitch + ((ls ^ (R & 15)) << 4);
+  }
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    const int R = wave * 16 * SA_NTW + 4 * q + lr;
+    vb[q] = R * (int)g.b_pitch + ((ls ^ (R & 15)) << 4);
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+  const v4i rsa = make_rsrc(g.a, g.M * g.a_pitch);
+
+  // load cursor: (tile, stage) of the next unit to fetch
+  int64_t lt = u0 / stages, lst = u0 - lt * stages;
+  auto fetch = [&](int slot) {
+    const int64_t n0 = lt * SA_BN;
+    const int64_t rows_b = (g.N - n0) < SA_BN ? (g.N - n0) : SA_BN;
+    const v4i rsb = make_rsrc(g.b + n0 * g.b_pitch, rows_b * g.b_pitch);
+    const int soff = (int)lst * ROWB;
+    const uint32_t base = lds0 + (uint32_t)slot * STG;
+#pragma unroll
+    for (int q = 0; q < QA; ++q) dma16(rsa, base + (wave * 4 * MT + 4 * q) * ROWB, va[q], soff);
+#pragma unroll
+    for (int q = 0; q < QB; ++q) dma16(rsb, base + ASZ + (wave * 16 * SA_NTW + 4 * q) * ROWB, vb[q], soff);
+    if (++lst == stages) {
+      lst = 0;
+      ++lt;
+    }
+  };
+
+  const int r = lane & 15, h = lane >> 4;
+  int fo[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) fo[t] = r * ROWB + (((4 * h + t) ^ r) << 4);
+
+  v4i acc[MT][SA_NTW][4];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < SA_NTW; ++j)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[i][j][c] = v4i{0, 0, 0, 0};
+
+#pragma unroll
+  for (int s = 0; s < SA_NS - 1; ++s)
+    if (s < cnt) fetch(s);
+
+  int64_t ct = u0 / stages, cst = u0 - ct * stages;   // (tile, stage) being computed
+  for (int64_t k = 0; k < cnt; ++k) {
+    // Unit k has landed once at most the later units this wave already
+    // issued are in flight (vector-memory counts return in order; atomics
+    // of earlier flushes only make the wait longer). The barrier then
+    // publishes everyone's loads of unit k and guarantees that no wave still
+    // reads unit k - 1, whose slot the next fetch refills.
+    if (k + 1 < cnt) wait_vm<QU>();
+    else wait_vm<0>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (k + SA_NS - 1 < cnt) fetch((int)((k + SA_NS - 1) % SA_NS));
+
+    const char* sa = lds + (int)(k % SA_NS) * STG;
+    const char* sb = sa + ASZ + wave * 16 * SA_NTW * ROWB;
+    v4i fa[MT][4], fb[SA_NTW][4];
+#pragma unroll
+    for (int j = 0; j < SA_NTW; ++j)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) fb[j][t] = *(const v4i*)(sb + j * 16 * ROWB + fo[t]);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) fa[i][t] = *(const v4i*)(sa + i * 16 * ROWB + fo[t]);
+
+    // consecutive MFMAs share the B fragment and write different accumulators
+#pragma unroll
+    for (int p = 0; p < 10; ++p)
+#pragma unroll
+      for (int j = 0; j < SA_NTW; ++j)
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+          acc[i][j][kLimbA[p] + kLimbB[p]] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+              fa[i][kLimbA[p]], fb[j][kLimbB[p]], acc[i][j][kLimbA[p] + kLimbB[p]], 0, 0, 0);
+
+    if (++cst == stages || k == cnt - 1) {
+      // add this tile's partial product into C. Output layout of the 16 x 16
+      // MFMA: register v of lane l holds row 4 (l / 16) + v, column l % 16.
+      const int64_t n0 = ct * SA_BN + wave * 16 * SA_NTW;
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < SA_NTW; ++j)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const uint32_t val = (uint32_t)acc[i][j][0][v] + ((uint32_t)acc[i][j][1][v] << 8) +
+                                 ((uint32_t)acc[i][j][2][v] << 16) + ((uint32_t)acc[i][j][3][v] << 24);
+            const int64_t m = i * 16 + 4 * h + v;
+            const int64_t n = n0 + j * 16 + r;
+            if (m < g.M && n < g.N) atomicAdd(&g.c[m * g.ldc + n], val);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc[i][j][c][v] = 0;
+          }
+      cst = 0;
+      ++ct;
+    }
+  }
+  wait_vm<0>();   // no direct load outlives the workgroup's LDS
+}
+
+// ---------------------------------------------------------------------------
+// K-split kernel (unmask epilogue)
+
+constexpr int KS_WAVES = 4;
+constexpr int KS_THREADS = 64 * KS_WAVES;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, int64_t bytes) {
   // out-of-range offsets read as zero
@@ -93,16 +266,26 @@ __device__ __forceinline__ void transpose4(v4i (&q)[4]) {
   swap16(q[2], q[3]);
 }
 
-// One segment: the product of all rows of A with B rows n0 .. n0 + 16 NT - 1
-// over stages [k0, k1) (64 columns each), written through the epilogue, or
-// added into C atomically when `atomic` (EPI_STORE after C was cleared, or
-// EPI_ACCUM). Every thread of the workgroup must call it.
-template <int MT, int NT, int DB, int EPI>
-__device__ __forceinline__ void skinny_segment(const GemmLaunch& g, uint32_t (*red)[MT * NT * 4][64], int64_t n0,
-                                               int k0, int k1, bool atomic) {
+// Workgroup b: column tile b (16 NT rows of B), all stages, split into 4
+// contiguous parts, one per wave. Load t of a wave reads bytes 64 t .. +64
+// of the stage in all 16 rows of a tile (lane (h, r) the 16 bytes at
+// 64 t + 16 h of row r), so every load consumes whole 64-byte segments; lane
+// group h then holds digit h of column group t in register quad t, and a
+// 4 x 4 transpose between lane groups and register quads (two rounds of
+// lane-swap instructions) turns that into the fragment of digit t. For A of
+// up to 16 rows each wave keeps two stages of loads in flight; with more
+// rows the accumulators leave no registers for a second set of fragments.
+// Prefetches past the wave's last stage are clamped to that stage: the
+// duplicate request hits in cache and the loop needs no branches around
+// loads. K must be non-zero.
+template <int MT, int NT, int DB>
+__global__ __launch_bounds__(KS_THREADS) void ring_gemm_skinny_unmask_kernel(GemmLaunch g) {
   constexpr int NOUT = MT * NT * 4;   // output registers per lane
+  __shared__ uint32_t red[KS_WAVES][NOUT][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int stages = (int)(g.Kp / 64);
+  const int64_t n0 = (int64_t)blockIdx.x * (16 * NT);
   const int64_t rows_b = (g.N - n0) < 16 * NT ? (g.N - n0) : 16 * NT;
   const __amdgpu_buffer_rsrc_t rb = rsrc(g.b + n0 * g.b_pitch, rows_b * g.b_pitch);
   const __amdgpu_buffer_rsrc_t ra = rsrc(g.a, g.M * g.a_pitch);
@@ -115,10 +298,10 @@ __device__ __forceinline__ void skinny_segment(const GemmLaunch& g, uint32_t (*r
 #pragma unroll
   for (int i = 0; i < MT; ++i) oa[i] = (i * 16 + r) * (int)g.a_pitch + h * 16;
 
-  // this wave's share [s0, s1) of the stages [k0, k1)
-  const int per = (k1 - k0 + NWAVES - 1) / NWAVES;
-  const int s0 = k0 + wave * per < k1 ? k0 + wave * per : k1;
-  const int s1 = (s0 + per) < k1 ? (s0 + per) : k1;
+  // this wave's share [s0, s1) of the stages
+  const int per = (stages + KS_WAVES - 1) / KS_WAVES;
+  const int s0 = wave * per < stages ? wave * per : stages;
+  const int s1 = (s0 + per) < stages ? (s0 + per) : stages;
 
   v4i acc[MT][NT][4];
 #pragma unroll
@@ -131,27 +314,24 @@ __device__ __forceinline__ void skinny_segment(const GemmLaunch& g, uint32_t (*r
   if (s0 < s1) {
     v4i fa[1 + DB][MT][4], fb[1 + DB][NT][4];
 
-#define SKINNY_LOAD(SET, S)                                                                \
+#define KS_LOAD(SET, S)                                                                    \
   do {                                                                                     \
-    const int so_ = (S) * STAGE_BYTES;                                                     \
+    const int so_ = (S) * ROWB;                                                            \
     _Pragma("unroll") for (int j = 0; j < NT; ++j)                                         \
     _Pragma("unroll") for (int t = 0; t < 4; ++t) fb[SET][j][t] = load16(rb, ob[j] + so_ + 64 * t); \
     _Pragma("unroll") for (int i = 0; i < MT; ++i)                                         \
     _Pragma("unroll") for (int t = 0; t < 4; ++t) fa[SET][i][t] = load16(ra, oa[i] + so_ + 64 * t); \
   } while (0)
 
-    // limb pairs (a, b) with a + b <= 3, grouped by the digit of B
-#define SKINNY_MFMA(SET)                                                                   \
+#define KS_MFMA(SET)                                                                       \
   do {                                                                                     \
     _Pragma("unroll") for (int j = 0; j < NT; ++j) transpose4(fb[SET][j]);                 \
     _Pragma("unroll") for (int i = 0; i < MT; ++i) transpose4(fa[SET][i]);                 \
-    constexpr int ta_[10] = {0, 1, 2, 3, 0, 1, 2, 0, 1, 0};                                \
-    constexpr int tb_[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};                                \
     _Pragma("unroll") for (int p = 0; p < 10; ++p)                                         \
     _Pragma("unroll") for (int i = 0; i < MT; ++i)                                         \
     _Pragma("unroll") for (int j = 0; j < NT; ++j)                                         \
-      acc[i][j][ta_[p] + tb_[p]] = __builtin_amdgcn_mfma_i32_16x16x64_i8(                  \
-          fa[SET][i][ta_[p]], fb[SET][j][tb_[p]], acc[i][j][ta_[p] + tb_[p]], 0, 0, 0);    \
+      acc[i][j][kLimbA[p] + kLimbB[p]] = __builtin_amdgcn_mfma_i32_16x16x64_i8(            \
+          fa[SET][i][kLimbA[p]], fb[SET][j][kLimbB[p]], acc[i][j][kLimbA[p] + kLimbB[p]], 0, 0, 0); \
   } while (0)
 
     // Position i of the wave's walk visits stage s0 + (i + rot) mod cnt.
@@ -160,30 +340,28 @@ __device__ __forceinline__ void skinny_segment(const GemmLaunch& g, uint32_t (*r
     // (which would queue on a few L2 channels).
     const int cnt = s1 - s0;
     const int rot = (int)(blockIdx.x % (unsigned)cnt);
-#define SKINNY_STAGE(i) (s0 + (((i) + rot) < cnt ? ((i) + rot) : ((i) + rot - cnt)))
+#define KS_STAGE(i) (s0 + (((i) + rot) < cnt ? ((i) + rot) : ((i) + rot - cnt)))
     if constexpr (DB) {
-      SKINNY_LOAD(0, SKINNY_STAGE(0));
-      SKINNY_LOAD(DB, SKINNY_STAGE(1 < cnt ? 1 : cnt - 1));
+      KS_LOAD(0, KS_STAGE(0));
+      KS_LOAD(DB, KS_STAGE(1 < cnt ? 1 : cnt - 1));
       for (int i = 0; i < cnt; i += 2) {
-        SKINNY_MFMA(0);
-        SKINNY_LOAD(0, SKINNY_STAGE((i + 2) < cnt ? (i + 2) : cnt - 1));
-        if (i + 1 < cnt) SKINNY_MFMA(DB);
-        SKINNY_LOAD(DB, SKINNY_STAGE((i + 3) < cnt ? (i + 3) : cnt - 1));
+        KS_MFMA(0);
+        KS_LOAD(0, KS_STAGE((i + 2) < cnt ? (i + 2) : cnt - 1));
+        if (i + 1 < cnt) KS_MFMA(DB);
+        KS_LOAD(DB, KS_STAGE((i + 3) < cnt ? (i + 3) : cnt - 1));
       }
     } else {
       for (int i = 0; i < cnt; ++i) {
-        SKINNY_LOAD(0, SKINNY_STAGE(i));
-        SKINNY_MFMA(0);
+        KS_LOAD(0, KS_STAGE(i));
+        KS_MFMA(0);
       }
     }
-#undef SKINNY_STAGE
-#undef SKINNY_LOAD
-#undef SKINNY_MFMA
+#undef KS_STAGE
+#undef KS_LOAD
+#undef KS_MFMA
   }
 
-  // recombine the shift classes, then sum the eight K ranges in LDS.
-  // Output layout of the 16 x 16 MFMA: register v of lane l holds row
-  // 4 (l / 16) + v, column l % 16.
+  // recombine the shift classes, then sum the waves' K ranges in LDS
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -195,67 +373,15 @@ __device__ __forceinline__ void skinny_segment(const GemmLaunch& g, uint32_t (*r
             ((uint32_t)acc[i][j][2][v] << 16) + ((uint32_t)acc[i][j][3][v] << 24);
   __syncthreads();
 
-  for (int idx = threadIdx.x; idx < NOUT * 64; idx += NTHREADS) {
+  for (int idx = threadIdx.x; idx < NOUT * 64; idx += KS_THREADS) {
     const int q = idx >> 6, l = idx & 63;
     uint32_t val = 0;
 #pragma unroll
-    for (int w = 0; w < NWAVES; ++w) val += red[w][q][l];
+    for (int w = 0; w < KS_WAVES; ++w) val += red[w][q][l];
     const int i = q / (NT * 4), j = (q / 4) % NT, v = q % 4;
     const int64_t m = i * 16 + 4 * (l >> 4) + v;
     const int64_t n = n0 + j * 16 + (l & 15);
-    if (m < g.M && n < g.N) {
-      if (atomic) atomicAdd(&g.c[m * g.ldc + n], val);
-      else gemm_epilogue<EPI>(g, m, n, val);
-    }
-  }
-}
-
-// Work assignment, one of two; either way a workgroup walks a contiguous
-// range [u, u1) of (column tile, stage) pairs, tile by tile, one segment per
-// tile it touches:
-//  * tiles (units == 0): workgroup b takes column tile b / ks and part b % ks
-//    of its K range (ks == 1 for the unmask epilogue, which cannot be split);
-//  * balanced (units > 0): the units pairs are cut into gridDim.x equal
-//    ranges, so no grid shape leaves a nearly empty last round of
-//    workgroups; every segment is added into C atomically.
-// K must be non-zero (stages > 0).
-template <int MT, int NT, int DB, int EPI, bool BAL>
-__global__ __launch_bounds__(NTHREADS) void ring_gemm_skinny_kernel(GemmLaunch g, int ks, int64_t units) {
-  __shared__ uint32_t red[NWAVES][MT * NT * 4][64];
-  const int64_t stages = g.Kp / 64;
-  if constexpr (!BAL) {
-    // one segment per workgroup (no loop: the widest tiles use every register)
-    const int64_t tile = blockIdx.x / (unsigned)ks;
-    const int64_t part = blockIdx.x % (unsigned)ks;
-    const int64_t kper = (stages + ks - 1) / ks;
-    const int64_t k0 = part * kper < stages ? part * kper : stages;
-    const int64_t k1 = (k0 + kper) < stages ? (k0 + kper) : stages;
-    skinny_segment<MT, NT, DB, EPI>(g, red, tile * (16 * NT), (int)k0, (int)k1, ks > 1);
-    return;
-  }
-  int64_t u, u1;
-  bool atomic;
-  if (units == 0) {
-    const int64_t tile = blockIdx.x / (unsigned)ks;
-    const int64_t part = blockIdx.x % (unsigned)ks;
-    const int64_t kper = (stages + ks - 1) / ks;
-    const int64_t k0 = part * kper < stages ? part * kper : stages;
-    const int64_t k1 = (k0 + kper) < stages ? (k0 + kper) : stages;
-    u = tile * stages + k0;
-    u1 = tile * stages + k1;
-    atomic = ks > 1;
-  } else {
-    u = units * blockIdx.x / gridDim.x;
-    u1 = units * (blockIdx.x + 1) / gridDim.x;
-    atomic = true;
-  }
-  while (u < u1) {
-    const int64_t tile = u / stages;
-    const int a = (int)(u - tile * stages);
-    const int b = (u1 - u) < stages - a ? a + (int)(u1 - u) : (int)stages;
-    skinny_segment<MT, NT, DB, EPI>(g, red, tile * (16 * NT), a, b, atomic);
-    u += b - a;
-    __syncthreads();   // the next segment reuses red
+    if (m < g.M && n < g.N) gemm_epilogue<EPI_UNMASK>(g, m, n, val);
   }
 }
 
@@ -264,64 +390,54 @@ __global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, 
   if (e < M * N) c[(e / N) * ldc + e % N] = 0u;
 }
 
-
-// Work assignment per launch. The unmask epilogue runs column tiles whole
-// (its partial products cannot be added into the output). The store and
-// accumulate epilogues use the balanced assignment over one workgroup per
-// compute unit (each with at least 4 stages), except that for A of at most
-// 16 rows with between 5/8 of and as many column tiles as compute units
-// whole tiles are faster (a sweep over the decode and mat-vec shapes: the
-// balanced assignment gained 10-35% where tiles exceed the compute units or
-// A has 32 or 64 rows, and lost 5-15% with 176-208 tiles; more workgroups
-// per compute unit were slower; with 64 tiles whole tiles left three
-// quarters of the compute units idle, 2.5x slower). A plain store with partial products added
-// atomically clears C first. K = 0 leaves only the epilogue: C = 0, C
-// unchanged, or the unmask of a zero product.
-template <int MT, int NT, int DB, int EPI>
-hipError_t launch_cfg(const GemmLaunch& g, hipStream_t s) {
-  const int64_t tiles = (g.N + 16 * NT - 1) / (16 * NT);
-  const int64_t stages = g.Kp / 64;
-  const dim3 block(NTHREADS);
-  if (stages == 0) {
-    if (EPI == EPI_UNMASK) return launch_unmask_elementwise(g, s);
-    if (EPI == EPI_STORE)
-      hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc,
-                         g.M, g.N);
-    return hipGetLastError();
-  }
+// Store and accumulate: the (tile, stage) units cut into one range per
+// compute unit (at least 2 units each); a plain store clears C first.
+template <int MT>
+hipError_t launch_shared_a(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
+  const int64_t tiles = (g.N + SA_BN - 1) / SA_BN;
+  const int64_t units = tiles * (g.Kp / 64);
   const int64_t cus = compute_units();
-  const int64_t units = tiles * stages;
-  if (EPI == EPI_UNMASK || (MT == 1 && tiles <= cus && 8 * tiles >= 5 * cus) || units < 8) {
-    hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, NT, DB, EPI, false>), dim3((unsigned)tiles), block, 0, s, g, 1,
-                       (int64_t)0);
-    return hipGetLastError();
-  }
-  const int64_t grid = cus < units / 4 ? cus : units / 4;
-  if (EPI == EPI_STORE)
+  const int64_t grid = cus < (units + 1) / 2 ? cus : (units + 1) / 2;
+  if (epi == EPI_STORE)
     hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc, g.M,
                        g.N);
-  hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, NT, DB, EPI, true>), dim3((unsigned)grid), block, 0, s, g, 1,
-                     units);
+  hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT>), dim3((unsigned)grid), dim3(SA_THREADS), 0, s, g, units);
   return hipGetLastError();
 }
 
-template <int EPI>
-hipError_t launch_epi(const GemmLaunch& g, hipStream_t s) {
-  // MT: 16-row tiles of A (A padded to 16, 32 or 64 rows); NT: 16-row tiles
-  // of B per workgroup; DB: double-buffered fragments.
-  const int mt = (int)((g.M + 15) / 16);
-  if (mt <= 1) return launch_cfg<1, 2, 1, EPI>(g, s);
-  if (mt == 2) return launch_cfg<2, 4, 0, EPI>(g, s);
-  return launch_cfg<4, 4, 0, EPI>(g, s);
+template <int MT, int NT, int DB>
+hipError_t launch_unmask(const GemmLaunch& g, hipStream_t s) {
+  const int64_t tiles = (g.N + 16 * NT - 1) / (16 * NT);
+  hipLaunchKernelGGL((ring_gemm_skinny_unmask_kernel<MT, NT, DB>), dim3((unsigned)tiles), dim3(KS_THREADS), 0, s, g);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  if (epi == EPI_STORE) return launch_epi<EPI_STORE>(g, s);
-  if (epi == EPI_ACCUM) return launch_epi<EPI_ACCUM>(g, s);
-  return launch_epi<EPI_UNMASK>(g, s);
+  const int mt = (int)((g.M + 15) / 16);
+  if (g.Kp == 0) {
+    // K = 0 leaves only the epilogue: C = 0, C unchanged, or the unmask of a
+    // zero product
+    if (epi == EPI_UNMASK) return launch_unmask_elementwise(g, s);
+    if (epi == EPI_STORE)
+      hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc,
+                         g.M, g.N);
+    return hipGetLastError();
+  }
+  if (epi == EPI_UNMASK) {
+    // NT: 16-row tiles of B per workgroup; DB: double-buffered fragments
+    if (mt <= 1) return launch_unmask<1, 2, 1>(g, s);
+    if (mt == 2) return launch_unmask<2, 4, 0>(g, s);
+    return launch_unmask<4, 4, 0>(g, s);
+  }
+  switch (mt) {
+    case 1: return launch_shared_a<1>(g, epi, s);
+    case 2: return launch_shared_a<2>(g, epi, s);
+    case 3: return launch_shared_a<3>(g, epi, s);
+    default: return launch_shared_a<4>(g, epi, s);
+  }
 }
 
 }  // namespace mosaic

@@ -138,12 +138,24 @@ def test_masked_matmul_mid_size(M, N, K):
 @pytest.mark.parametrize("M", [1, 8, 15, 16, 17, 33, 48, 63, 64, 65])
 @pytest.mark.parametrize("N,K", [(33, 64), (100, 576), (16, 1000), (47, 4160)])
 def test_masked_matmul_short_a(M, N, K):
-    """Decode-shaped products (at most 64 rows of A take the K-split kernel):
-    row counts on and around the 16-row tiles, ragged N, and K ranges that
-    leave some of the waves' K slices short or empty; with these few column
-    tiles K is also split across 2-4 workgroups (K >= 512) whose partial
-    products are added atomically."""
+    """Decode-shaped products (at most 64 rows of A take the shared-A decode
+    kernel): row counts on and around the 16-row tiles, ragged N inside one
+    128-row column tile, and K ranges of 1 to 65 stages cut into per-workgroup
+    ranges whose partial products are added atomically."""
     rng = _rng_np(M * 131 + N * 7 + K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
+
+
+@pytest.mark.parametrize("M", [1, 16, 17, 40, 64])
+@pytest.mark.parametrize("N,K", [(1000, 4160), (3000, 576), (300, 64), (2049, 1024)])
+def test_masked_matmul_short_a_many_tiles(M, N, K):
+    """Decode kernel over several 128-row column tiles with a ragged last
+    tile: the workgroups' (tile, stage) ranges start and end inside tiles and
+    cross tile boundaries (one to a few stages each), or hold single-stage
+    tiles (K = 64)."""
+    rng = _rng_np(M * 17 + N * 5 + K)
     a = _random_ring(rng, (M, K), edge=True)
     b = _random_ring(rng, (N, K), edge=True)
     assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
@@ -194,8 +206,8 @@ def test_masked_matmul_accumulator_extreme():
 def test_masked_matmul_ldc_and_offsets(M, K):
     """Output with a leading dimension > N and operands at a column offset in
     a wider digit buffer; C starts non-zero and only its M x N window may
-    change. M = 40 with K = 2000 takes the decode kernel with the K range
-    split across workgroups (C cleared, partial products added atomically)."""
+    change. M = 40 with K = 2000 takes the decode kernel (the window cleared,
+    partial products of the workgroups' K ranges added atomically)."""
     rng = _rng_np(11 + M)
     N = 50
     a = _random_ring(rng, (M, K))
