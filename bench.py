@@ -507,7 +507,8 @@ def run_decode(dev):
     ranks (1536, 1024, 652), sparse mode). Per shape and M: the server product
     ([Y' | Q], N + 2560 output columns) and the whole call (Init X, mask,
     server, unmask), HIP-event means over 20 calls; GB/s counts the server
-    product's operand and output bytes once. Calls cycle through distinct
+    product's operand and output bytes once. The server loop is also timed
+    as a replayed HIP graph of the same 20 calls (no host launch cost). Calls cycle through distinct
     masked weights (independent masks of the same W) whose server matrices
     together exceed the last-level cache three times."""
     import torch
@@ -541,6 +542,20 @@ def run_decode(dev):
                 for j in range(nrot):
                     gp.run_call(ws_[j], Ad, 10_000 + j, bs_[j])
             torch.cuda.synchronize()
+            # the server loop once more as a replayed graph: kernel time without
+            # the host's per-call launch cost (which bounds the eager loop at
+            # the smaller shapes)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for i in range(reps):
+                    gp.server(wl[i % nrot], M, bl[i % nrot])
+            graph.replay()
+            torch.cuda.synchronize()
+            ge = _events(2)
+            ge[0].record()
+            for _ in range(3):
+                graph.replay()
+            ge[1].record()
             e = _events(5)
             e[0].record()
             for i in range(reps):
@@ -570,6 +585,8 @@ def run_decode(dev):
             ph[2].record()
             torch.cuda.synchronize()
             server_ms = e[0].elapsed_time(e[1]) / reps
+            server_graph_ms = ge[0].elapsed_time(ge[1]) / (3 * reps)
+            del graph
             call_ms = e[1].elapsed_time(e[2]) / reps
             call_sparse_ms = e[2].elapsed_time(e[3]) / reps
             call_d3_ms = e[3].elapsed_time(e[4]) / reps
@@ -579,6 +596,8 @@ def run_decode(dev):
             res.append({"K": K, "N": N, "M": M, "server_us": round(server_ms * 1e3, 2),
                         "server_gbs": round(byts / (server_ms * 1e-3) / 1e9, 1),
                         "server_hbm_frac": round(byts / (server_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
+                        "server_us_graph": round(server_graph_ms * 1e3, 2),
+                        "server_hbm_frac_graph": round(byts / (server_graph_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
                         "call_us": round(call_ms * 1e3, 2),
                         "call_us_sparse_lpn": round(call_sparse_ms * 1e3, 2),
                         "call_us_d3_sparse_lpn": round(call_d3_ms * 1e3, 2),

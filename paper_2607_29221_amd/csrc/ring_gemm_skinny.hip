@@ -7,7 +7,7 @@
 // limb products with i + j <= 3 grouped by shift class into four int32
 // accumulators (the emulation of Section 6.1), recombined with wrap-around
 // arithmetic. Here the matrix instruction is v_mfma_i32_16x16x64_i8, so A is
-// padded only to 16, 32, 48 or 64 rows.
+// padded only to 16, 32 or 64 rows.
 //
 // Two kernels:
 //
@@ -19,13 +19,17 @@
 // product into C with 32-bit atomics (exact in the ring; C is cleared first
 // for a plain store). Both operands of a stage are staged in LDS by direct
 // buffer-to-LDS loads, three stages resident and loads issued two stages
-// ahead, so data in flight costs no registers. The four waves of a
-// workgroup split the tile's columns (32 each): the A stage is fetched once
-// per workgroup and read from LDS by every wave, where a split of K between
-// the waves would fetch all of A once per wave and need a reduction of the
-// waves' partial products. Measured against that K-split design (B streamed
-// into registers): 20-26% less time for 16 and 32 tokens, 35% for 64, 4-10%
-// for one token, at the decode and mat-vec shapes.
+// ahead, so data in flight costs no registers. The waves of a workgroup
+// split the tile's columns (32 each, 4 column groups): the A stage is
+// fetched once per workgroup and read from LDS by every wave, where a split
+// of K between the waves would fetch all of A once per wave and need a
+// reduction of the waves' partial products. For A of more than 16 rows a
+// second row of 4 waves takes the other half of A's rows (8 waves, two per
+// SIMD: one wave's MFMAs run while the other waits at the barrier or on
+// LDS), and A of 33-64 rows is padded to 64. Measured against the K-split
+// design (B streamed into registers) at the decode and mat-vec shapes:
+// 4-10% less time for one token, 20-26% for 16 and 32 tokens, about 50% for
+// 64 (35% with one row of waves).
 //
 // ring_gemm_skinny_unmask_kernel (unmask epilogue, whose inputs cannot take
 // partial products). One workgroup per column tile of 32 (A of at most 16
@@ -61,10 +65,9 @@ __device__ constexpr int kLimbB[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
 // ---------------------------------------------------------------------------
 // Shared-A kernel (store and accumulate epilogues)
 
-constexpr int SA_WAVES = 4;
-constexpr int SA_THREADS = 64 * SA_WAVES;
+constexpr int SA_WN = 4;                           // waves along the tile's columns
 constexpr int SA_NTW = 2;                          // 16-row B tiles per wave
-constexpr int SA_BN = SA_WAVES * SA_NTW * 16;      // B rows per column tile
+constexpr int SA_BN = SA_WN * SA_NTW * 16;         // B rows per column tile
 constexpr int SA_NS = 3;                           // stages resident in LDS
 
 // Direct buffer-to-LDS load of 16 bytes per lane: lane l writes LDS bytes
@@ -80,9 +83,13 @@ __device__ __forceinline__ void dma16(v4i rs, uint32_t lds_off, int voff, int so
 }
 
 // Raw buffer descriptor over [base, base + bytes): out-of-range lanes read 0.
+// The arguments are uniform; readfirstlane states it, so the descriptor
+// stays in scalar registers as the direct load requires.
 __device__ __forceinline__ v4i make_rsrc(const void* base, int64_t bytes) {
   const uint64_t b = (uint64_t)base;
-  return v4i{(int)(uint32_t)b, (int)((uint32_t)(b >> 32) & 0xFFFFu), (int)bytes, (int)0x00020000u};
+  return v4i{__builtin_amdgcn_readfirstlane((int)(uint32_t)b),
+             __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xFFFFu)),
+             __builtin_amdgcn_readfirstlane((int)bytes), (int)0x00020000u};
 }
 
 // s_waitcnt with only the vector-memory counter constrained: vmcnt(N)
@@ -93,36 +100,43 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // Workgroup b computes units [units b / grid, units (b + 1) / grid) of the
-// tiles x stages (column tile, stage) pairs, tile-major. K must be non-zero.
-template <int MT>
-__global__ __launch_bounds__(SA_THREADS, 1) void ring_gemm_skinny_kernel(GemmLaunch g, int64_t units) {
+// tiles x stages (column tile, stage) pairs, tile-major, with WM x 4 waves:
+// wave (wm, wn) multiplies A row tiles wm MT / WM .. +MT / WM with B row tiles
+// 2 wn, 2 wn + 1 of the column tile. K must be non-zero.
+template <int MT, int WM>
+__global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(GemmLaunch g, int64_t units) {
+  constexpr int NW = WM * SA_WN;
+  constexpr int MTW = MT / WM;                     // A row tiles per wave
+  static_assert(MT % WM == 0, "A row tiles split evenly between the rows of waves");
   constexpr int ASZ = 16 * MT * ROWB;              // A part of a stage
   constexpr int STG = ASZ + SA_BN * ROWB;          // one stage
-  constexpr int QA = MT;                           // direct loads per wave per stage: A ...
-  constexpr int QB = 4 * SA_NTW;                   // ... and B (1 KiB each)
+  static_assert((4 * MT) % NW == 0 && (SA_BN / 4) % NW == 0, "direct loads split evenly between the waves");
+  constexpr int QA = 4 * MT / NW;                  // direct loads per wave per stage: A ...
+  constexpr int QB = SA_BN / 4 / NW;               // ... and B (1 KiB = 4 rows each)
   constexpr int QU = QA + QB;
   static_assert(SA_NS * STG <= 160 * 1024, "LDS");
   __shared__ __attribute__((aligned(1024))) char lds[SA_NS * STG];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / SA_WN, wn = wave % SA_WN;
   const int64_t stages = g.Kp / 64;
   const int64_t u0 = units * blockIdx.x / gridDim.x;
   const int64_t cnt = units * (blockIdx.x + 1) / gridDim.x - u0;
   if (cnt <= 0) return;
 
-  // direct loads: wave w fills A rows 4 MT w .. +4 MT and B rows 32 w .. +32
-  // of every stage, 4 rows per load
+  // direct loads: wave w fills A rows 4 QA w .. +4 QA and B rows 4 QB w .. +4 QB
+  // of every stage
   const int lr = lane >> 4, ls = lane & 15;
   int va[QA], vb[QB];
 #pragma unroll
   for (int q = 0; q < QA; ++q) {
-    const int R = wave * 4 * MT + 4 * q + lr;
+    const int R = wave * 4 * QA + 4 * q + lr;
     va[q] = R * (int)g.a_pitch + ((ls ^ (R & 15)) << 4);
   }
 #pragma unroll
   for (int q = 0; q < QB; ++q) {
-    const int R = wave * 16 * SA_NTW + 4 * q + lr;
+    const int R = wave * 4 * QB + 4 * q + lr;
     vb[q] = R * (int)g.b_pitch + ((ls ^ (R & 15)) << 4);
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
@@ -137,9 +151,9 @@ __global__ __launch_bounds__(SA_THREADS, 1) void ring_gemm_skinny_kernel(GemmLau
     const int soff = (int)lst * ROWB;
     const uint32_t base = lds0 + (uint32_t)slot * STG;
 #pragma unroll
-    for (int q = 0; q < QA; ++q) dma16(rsa, base + (wave * 4 * MT + 4 * q) * ROWB, va[q], soff);
+    for (int q = 0; q < QA; ++q) dma16(rsa, base + (wave * 4 * QA + 4 * q) * ROWB, va[q], soff);
 #pragma unroll
-    for (int q = 0; q < QB; ++q) dma16(rsb, base + ASZ + (wave * 16 * SA_NTW + 4 * q) * ROWB, vb[q], soff);
+    for (int q = 0; q < QB; ++q) dma16(rsb, base + ASZ + (wave * 4 * QB + 4 * q) * ROWB, vb[q], soff);
     if (++lst == stages) {
       lst = 0;
       ++lt;
@@ -151,9 +165,9 @@ __global__ __launch_bounds__(SA_THREADS, 1) void ring_gemm_skinny_kernel(GemmLau
 #pragma unroll
   for (int t = 0; t < 4; ++t) fo[t] = r * ROWB + (((4 * h + t) ^ r) << 4);
 
-  v4i acc[MT][SA_NTW][4];
+  v4i acc[MTW][SA_NTW][4];
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+  for (int i = 0; i < MTW; ++i)
 #pragma unroll
     for (int j = 0; j < SA_NTW; ++j)
 #pragma unroll
@@ -177,15 +191,15 @@ __global__ __launch_bounds__(SA_THREADS, 1) void ring_gemm_skinny_kernel(GemmLau
     asm volatile("" ::: "memory");
     if (k + SA_NS - 1 < cnt) fetch((int)((k + SA_NS - 1) % SA_NS));
 
-    const char* sa = lds + (int)(k % SA_NS) * STG;
-    const char* sb = sa + ASZ + wave * 16 * SA_NTW * ROWB;
-    v4i fa[MT][4], fb[SA_NTW][4];
+    const char* sa = lds + (int)(k % SA_NS) * STG + wm * MTW * 16 * ROWB;
+    const char* sb = lds + (int)(k % SA_NS) * STG + ASZ + wn * 16 * SA_NTW * ROWB;
+    v4i fa[MTW][4], fb[SA_NTW][4];
 #pragma unroll
     for (int j = 0; j < SA_NTW; ++j)
 #pragma unroll
       for (int t = 0; t < 4; ++t) fb[j][t] = *(const v4i*)(sb + j * 16 * ROWB + fo[t]);
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MTW; ++i)
 #pragma unroll
       for (int t = 0; t < 4; ++t) fa[i][t] = *(const v4i*)(sa + i * 16 * ROWB + fo[t]);
 
@@ -195,23 +209,23 @@ __global__ __launch_bounds__(SA_THREADS, 1) void ring_gemm_skinny_kernel(GemmLau
 #pragma unroll
       for (int j = 0; j < SA_NTW; ++j)
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
+        for (int i = 0; i < MTW; ++i)
           acc[i][j][kLimbA[p] + kLimbB[p]] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
               fa[i][kLimbA[p]], fb[j][kLimbB[p]], acc[i][j][kLimbA[p] + kLimbB[p]], 0, 0, 0);
 
     if (++cst == stages || k == cnt - 1) {
       // add this tile's partial product into C. Output layout of the 16 x 16
       // MFMA: register v of lane l holds row 4 (l / 16) + v, column l % 16.
-      const int64_t n0 = ct * SA_BN + wave * 16 * SA_NTW;
+      const int64_t n0 = ct * SA_BN + wn * 16 * SA_NTW;
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+      for (int i = 0; i < MTW; ++i)
 #pragma unroll
         for (int j = 0; j < SA_NTW; ++j)
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const uint32_t val = (uint32_t)acc[i][j][0][v] + ((uint32_t)acc[i][j][1][v] << 8) +
                                  ((uint32_t)acc[i][j][2][v] << 16) + ((uint32_t)acc[i][j][3][v] << 24);
-            const int64_t m = i * 16 + 4 * h + v;
+            const int64_t m = (wm * MTW + i) * 16 + 4 * h + v;
             const int64_t n = n0 + j * 16 + r;
             if (m < g.M && n < g.N) atomicAdd(&g.c[m * g.ldc + n], val);
 #pragma unroll
@@ -392,7 +406,7 @@ __global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, 
 
 // Store and accumulate: the (tile, stage) units cut into one range per
 // compute unit (at least 2 units each); a plain store clears C first.
-template <int MT>
+template <int MT, int WM>
 hipError_t launch_shared_a(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
   const int64_t tiles = (g.N + SA_BN - 1) / SA_BN;
   const int64_t units = tiles * (g.Kp / 64);
@@ -401,7 +415,7 @@ hipError_t launch_shared_a(const GemmLaunch& g, EpilogueKind epi, hipStream_t s)
   if (epi == EPI_STORE)
     hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc, g.M,
                        g.N);
-  hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT>), dim3((unsigned)grid), dim3(SA_THREADS), 0, s, g, units);
+  hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, WM>), dim3((unsigned)grid), dim3(64 * WM * SA_WN), 0, s, g, units);
   return hipGetLastError();
 }
 
@@ -432,12 +446,11 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
     if (mt == 2) return launch_unmask<2, 4, 0>(g, s);
     return launch_unmask<4, 4, 0>(g, s);
   }
-  switch (mt) {
-    case 1: return launch_shared_a<1>(g, epi, s);
-    case 2: return launch_shared_a<2>(g, epi, s);
-    case 3: return launch_shared_a<3>(g, epi, s);
-    default: return launch_shared_a<4>(g, epi, s);
-  }
+  // MT: 16-row tiles of A (33-64 rows padded to 64: faster than 48 rows on
+  // one row of waves); WM: rows of 4 waves
+  if (mt <= 1) return launch_shared_a<1, 1>(g, epi, s);
+  if (mt == 2) return launch_shared_a<2, 2>(g, epi, s);
+  return launch_shared_a<4, 2>(g, epi, s);
 }
 
 }  // namespace mosaic

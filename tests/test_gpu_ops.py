@@ -161,6 +161,35 @@ def test_masked_matmul_short_a_many_tiles(M, N, K):
     assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
 
 
+@pytest.mark.parametrize("M,N,K", [(1, 1000, 4160), (64, 700, 1024), (200, 300, 512)])
+def test_masked_matmul_graph_replay(M, N, K):
+    """The product captured in a HIP graph (decode kernel: C cleared by a
+    kernel, partial products added atomically; tiled kernel) and replayed
+    three times, with C overwritten and other work run eagerly between the
+    replays: every replay equals the eagerly launched product."""
+    rng = _rng_np(M + 3 * N + 7 * K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    A, B = Digits.empty(M, K), Digits.empty(N, K)
+    m.mosaic_mask(to_dev_ring(a), None, None, M, K, out_dig=A)
+    m.mosaic_mask(to_dev_ring(b), None, None, N, K, out_dig=B)
+    C = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    m.mosaic_masked_matmul(A, B, M, N, K, C)
+    torch.cuda.synchronize()
+    eager = to_np_u32(C)
+    assert np.array_equal(eager, ring_matmul(a, b.T))
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        m.mosaic_masked_matmul(A, B, M, N, K, C)
+    for rep in range(3):
+        C.fill_(12345 + rep)
+        m.mosaic_mask(to_dev_ring(b), None, None, N, K, out_dig=Digits.empty(N, K))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(to_np_u32(C), eager), rep
+
+
 @pytest.mark.parametrize("M", [5, 64])
 def test_masked_matmul_accumulator_extreme_short_a(M):
     N, K = 40, 32767
