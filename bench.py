@@ -37,6 +37,26 @@ HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 3 * 256 * 2 ** 20
 
 
+def _graph_ms(step, reps: int) -> float:
+    """Mean time per call of ``step(i)`` for i < reps, captured once as a HIP
+    graph and replayed (one warm-up replay, three timed): the device time of
+    the calls without the host's per-launch cost."""
+    import torch
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(reps):
+            step(i)
+    graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = _events(2)
+    e0.record()
+    for _ in range(3):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / (3 * reps)
+
+
 def _rotation(bytes_per_copy: int) -> int:
     """Number of distinct copies (at least 2) that together reach ROTATE_BYTES."""
     return max(2, -(-ROTATE_BYTES // max(1, bytes_per_copy)))
@@ -507,8 +527,9 @@ def run_decode(dev):
     ranks (1536, 1024, 652), sparse mode). Per shape and M: the server product
     ([Y' | Q], N + 2560 output columns) and the whole call (Init X, mask,
     server, unmask), HIP-event means over 20 calls; GB/s counts the server
-    product's operand and output bytes once. The server loop is also timed
-    as a replayed HIP graph of the same 20 calls (no host launch cost). Calls cycle through distinct
+    product's operand and output bytes once. The server loop and the three
+    whole-call loops are also timed as replayed HIP graphs of 20 calls (the
+    device time without the host's per-launch cost). Calls cycle through distinct
     masked weights (independent masks of the same W) whose server matrices
     together exceed the last-level cache three times."""
     import torch
@@ -542,20 +563,13 @@ def run_decode(dev):
                 for j in range(nrot):
                     gp.run_call(ws_[j], Ad, 10_000 + j, bs_[j])
             torch.cuda.synchronize()
-            # the server loop once more as a replayed graph: kernel time without
-            # the host's per-call launch cost (which bounds the eager loop at
-            # the smaller shapes)
-            graph = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(graph):
-                for i in range(reps):
-                    gp.server(wl[i % nrot], M, bl[i % nrot])
-            graph.replay()
-            torch.cuda.synchronize()
-            ge = _events(2)
-            ge[0].record()
-            for _ in range(3):
-                graph.replay()
-            ge[1].record()
+            # the loops once more as replayed graphs: device time without the
+            # host's per-launch cost (which bounds the eager whole-call loops)
+            server_graph_ms = _graph_ms(lambda i: gp.server(wl[i % nrot], M, bl[i % nrot]), reps)
+            call_graph_ms = _graph_ms(lambda i: gp.run_call(wl[i % nrot], Ad, 40_000 + i, bl[i % nrot]), reps)
+            call_sparse_graph_ms = _graph_ms(lambda i: gp.run_call(wsl[i % nrot], Ad, 40_000 + i, bsl[i % nrot]),
+                                             reps)
+            call_d3_graph_ms = _graph_ms(lambda i: gp.run_call(w3l[i % nrot], Ad, 40_000 + i, b3l[i % nrot]), reps)
             e = _events(5)
             e[0].record()
             for i in range(reps):
@@ -585,8 +599,6 @@ def run_decode(dev):
             ph[2].record()
             torch.cuda.synchronize()
             server_ms = e[0].elapsed_time(e[1]) / reps
-            server_graph_ms = ge[0].elapsed_time(ge[1]) / (3 * reps)
-            del graph
             call_ms = e[1].elapsed_time(e[2]) / reps
             call_sparse_ms = e[2].elapsed_time(e[3]) / reps
             call_d3_ms = e[3].elapsed_time(e[4]) / reps
@@ -601,6 +613,9 @@ def run_decode(dev):
                         "call_us": round(call_ms * 1e3, 2),
                         "call_us_sparse_lpn": round(call_sparse_ms * 1e3, 2),
                         "call_us_d3_sparse_lpn": round(call_d3_ms * 1e3, 2),
+                        "call_us_graph": round(call_graph_ms * 1e3, 2),
+                        "call_us_sparse_lpn_graph": round(call_sparse_graph_ms * 1e3, 2),
+                        "call_us_d3_sparse_lpn_graph": round(call_d3_graph_ms * 1e3, 2),
                         "init_x_us_sparse_lpn": round(init_x_ms * 1e3, 2),
                         "online_us_sparse_lpn": round(online_ms * 1e3, 2), "weights_rotated": nrot})
             del bl, bsl, b3l

@@ -237,6 +237,9 @@ __global__ __launch_bounds__(1024) void count_mismatches_kernel(const uint32_t* 
   }
 }
 
+// y = ym - kc - c elementwise (kc, c optional). c may share memory with y or
+// y_f32 element for element: each thread reads its element of c before it
+// writes that element.
 __global__ __launch_bounds__(256) void unmask_elementwise_kernel(GemmLaunch g) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t i = gid / g.N;
@@ -244,6 +247,7 @@ __global__ __launch_bounds__(256) void unmask_elementwise_kernel(GemmLaunch g) {
   if (i >= g.M) return;
   uint32_t v = g.ym[i * g.ldy + j];
   if (g.kc != nullptr) v -= g.kc[i * g.ldk + j];
+  if (g.c != nullptr) v -= g.c[i * g.ldc + j];
   if (g.y != nullptr) g.y[i * g.ldo + j] = (int32_t)v;
   if (g.y_f32 != nullptr)
     g.y_f32[i * g.ldf + j] = (float)(int32_t)v * g.s_rows[i] * g.s_cols[j];

@@ -60,7 +60,8 @@ struct GemmLaunch {
   // EPI_STORE
   uint32_t* c;
   int64_t ldc;
-  // EPI_UNMASK: out = ym - kc - acc
+  // EPI_UNMASK: out = ym - kc - acc (the elementwise unmask subtracts c,
+  // when set, as a finished product)
   const uint32_t* ym;
   int64_t ldy;
   const uint32_t* kc;

@@ -278,6 +278,46 @@ def test_unmask(M, N, R, with_k):
     assert np.array_equal(y.cpu().numpy(), ref.view(np.int32))
 
 
+@pytest.mark.parametrize("M", [1, 20, 64])
+@pytest.mark.parametrize("case", ["y", "y_and_f32", "f32", "y_is_ym", "y_is_kc", "f32_over_ym"])
+def test_unmask_short_a_outputs(M, case):
+    """Unmask with at most 64 rows over several column tiles (N = 700, R =
+    1088): an output that shares no memory with the inputs holds the product
+    until the elementwise pass (y, y with y_f32, y_f32 alone); in place on ym
+    or kc, or y_f32 over ym's memory, the whole-tile kernel runs. Every
+    case equals the oracle."""
+    N, R = 700, 1088
+    rng = _rng_np(M * 3 + len(case))
+    ym = _random_ring(rng, (M, N))
+    kc = _random_ring(rng, (M, N))
+    q = _random_ring(rng, (M, R))
+    l = _random_ring(rng, (N, R))
+    Q, L = Digits.empty(M, R), Digits.empty(N, R)
+    m.mosaic_mask(to_dev_ring(q), None, None, M, R, out_dig=Q)
+    m.mosaic_mask(to_dev_ring(l), None, None, N, R, out_dig=L)
+    ymd, kcd = to_dev_ring(ym), to_dev_ring(kc)
+    sr = torch.rand(M, device="cuda") * 1e-3
+    sc = torch.rand(N, device="cuda") * 1e-3
+    want_f32 = case in ("y_and_f32", "f32", "f32_over_ym")
+    y = {"y": torch.empty((M, N), dtype=torch.int32, device="cuda"),
+         "y_and_f32": torch.empty((M, N), dtype=torch.int32, device="cuda"),
+         "y_is_ym": ymd, "y_is_kc": kcd}.get(case)
+    yf = None
+    if case in ("y_and_f32", "f32"):
+        yf = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    elif case == "f32_over_ym":
+        yf = ymd.view(torch.float32)
+    m.mosaic_unmask(ymd, kcd, Q, L, M, N, R, y=y, s_rows=sr if want_f32 else None,
+                    s_cols=sc if want_f32 else None, y_f32=yf)
+    torch.cuda.synchronize()
+    yi = ring_sub(ring_sub(ym, kc), ring_matmul(q, l.T)).view(np.int32)
+    if y is not None:
+        assert np.array_equal(y.cpu().numpy(), yi)
+    if want_f32:
+        ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+        assert np.array_equal(yf.cpu().numpy(), ref)
+
+
 @pytest.mark.parametrize("M,N", [(40, 90), (150, 90), (150, 92), (300, 260)])
 def test_unmask_dequantised(M, N):
     rng = _rng_np(5 + M + N)
