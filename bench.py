@@ -725,9 +725,10 @@ def run_product_only():
 
 
 def run_cpu_baseline():
-    """The oracle on a bounded sample of the same workload: 128 tokens x 128
+    """The oracle on a bounded sample of the same workload: 384 tokens x 128
     output columns of the (K, N) = (8192, 8192) shape, full per-call path
-    (Init X, mask, server product incl. Q, unmask; about 15 s of CPU work);
+    (Init X, mask, server product incl. Q, unmask; 10-25 s of CPU work on the
+    hosts seen so far);
     Init W for those 128 weight rows is prepared outside the timed region.
     At this output width the rank-1536 mask products (U_a and Q, M K r ring
     MACs each) dominate the oracle's work, so its rate per plaintext ring op
@@ -737,7 +738,7 @@ def run_cpu_baseline():
     from oracle import protocol as op
     from synthetic_inputs import PARAMS_PAPER_D1, PREFILL_SEED, int8_operands
 
-    K, N, Ms, Ns = 8192, 8192, 128, 128
+    K, N, Ms, Ns = 8192, 8192, 384, 128
     A, W = int8_operands(2048, K, N, PREFILL_SEED)
     seed = 0x6D6F736169630000 | PREFILL_SEED
     ws = op.init_w(W[:Ns], PARAMS_PAPER_D1, seed, 0)
