@@ -57,6 +57,37 @@ def _graph_ms(step, reps: int) -> float:
     return e0.elapsed_time(e1) / (3 * reps)
 
 
+def _settle(step, seconds: float = 0.025) -> None:
+    """Untimed calls of step(i) for some tens of milliseconds before a
+    stand-alone pass is timed: an ALU-heavy kernel started after other work
+    ran up to 25% slower for its first ~10 ms (the mask pass with noise drawn
+    in the pass measured 104-112 us over its first 30-60 launches and 87-89 us
+    after), a transient of the chip's clock and power control rather than of
+    the kernel."""
+    import torch
+    t0, i = time.perf_counter(), 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            step(i)
+            i += 1
+        torch.cuda.synchronize()
+
+
+def _warm_up(dev, seconds: float = 2.0) -> None:
+    """Runs fp32 matrix products for a few seconds before stand-alone timings:
+    the GPU raises its clocks only after some time under load, and ALU-heavy
+    kernels timed in the first seconds of a process (the samplers, the mask
+    pass with noise drawn in the pass) measured up to 20% slower."""
+    import torch
+    a = torch.randn(4096, 4096, device=dev)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            b = a @ a
+        torch.cuda.synchronize()
+    del a, b
+
+
 def _rotation(bytes_per_copy: int) -> int:
     """Number of distinct copies (at least 2) that together reach ROTATE_BYTES."""
     return max(2, -(-ROTATE_BYTES // max(1, bytes_per_copy)))
@@ -194,8 +225,7 @@ def run_extras(dev):
     ys = [torch.empty_like(xs[0]) for _ in range(nbuf)]
     signs = torch.empty(n, dtype=torch.int8, device=dev)
     m.mosaic_sample_signs(m.rng(3, 0x70, 0, 0), n, signs)
-    for i in range(3):
-        m.mosaic_hadamard_rotate(xs[i % nbuf], ys[i % nbuf], signs=signs)
+    _settle(lambda i: m.mosaic_hadamard_rotate(xs[i % nbuf], ys[i % nbuf], signs=signs))
     reps = 30
     e0, e1 = _events(2)
     e0.record()
@@ -224,8 +254,7 @@ def run_extras(dev):
                 ("blockdiag1024", lambda a, b: m.mosaic_hadamard_rotate(a, b, block=1024, signs=s28)))
     res["rotation_28672"] = []
     for name, fn in variants:
-        for i in range(3):
-            fn(xs[i % 2], ys[i % 2])
+        _settle(lambda i: fn(xs[i % 2], ys[i % 2]))
         e0, e1 = _events(2)
         e0.record()
         for i in range(reps):
@@ -247,8 +276,8 @@ def run_extras(dev):
     D = [Digits.empty(M, K, dev) for _ in range(nbuf)]
     noise = m.rng(2, 0x50, 0, m.DIST_DGAUSS, sigma=0.5, bound=4)
     for with_noise in (False, True):
-        for i in range(3):
-            m.mosaic_mask(A[i], U[i], noise if with_noise else None, M, K, out_dig=D[i])
+        _settle(lambda i: m.mosaic_mask(A[i % nbuf], U[i % nbuf], noise if with_noise else None, M, K,
+                                        out_dig=D[i % nbuf]))
         e0, e1 = _events(2)
         e0.record()
         for i in range(reps):
@@ -266,8 +295,7 @@ def run_extras(dev):
     for name, r in (("uniform", m.rng(2, 0x20, 0, m.DIST_UNIFORM)),
                     ("dgauss", m.rng(2, 0x50, 0, m.DIST_DGAUSS, sigma=0.5, bound=4)),
                     ("sparse", m.rng(2, 0x40, 0, m.DIST_SPARSE, log2_inv_density=6))):
-        for i in range(3):
-            m.mosaic_sample(r, M, K, out_dig=D[i])
+        _settle(lambda i: m.mosaic_sample(r, M, K, out_dig=D[i % nbuf]))
         e0, e1 = _events(2)
         e0.record()
         for i in range(reps):
@@ -284,8 +312,7 @@ def run_extras(dev):
     xs = [torch.randn(rows, n, device=dev) for _ in range(nbuf)]
     qs = [torch.empty((rows, n), dtype=torch.int32, device=dev) for _ in range(nbuf)]
     sc = torch.empty(rows, dtype=torch.float32, device=dev)
-    for i in range(3):
-        m.mosaic_quantize_rows(xs[i], 1997, q=qs[i], scale=sc)
+    _settle(lambda i: m.mosaic_quantize_rows(xs[i % nbuf], 1997, q=qs[i % nbuf], scale=sc))
     e0, e1 = _events(2)
     e0.record()
     for i in range(reps):
@@ -320,8 +347,7 @@ def run_extras(dev):
 
         ts = []
         for fn in (separate, fused):
-            for i in range(2):
-                fn(i)
+            _settle(fn)
             e0, e1 = _events(2)
             e0.record()
             for i in range(10):
@@ -785,11 +811,13 @@ def main():
 
     if args.passes_only:
         import torch
+        _warm_up(torch.device("cuda:0"))
         print(json.dumps({"passes": run_extras(torch.device("cuda:0"))}))
         return
 
     if args.decode_only:
         import torch
+        _warm_up(torch.device("cuda:0"))
         print(json.dumps({"decode": run_decode(torch.device("cuda:0"))}))
         return
 
