@@ -279,13 +279,13 @@ def test_unmask(M, N, R, with_k):
 
 
 @pytest.mark.parametrize("M", [1, 20, 64])
-@pytest.mark.parametrize("case", ["y", "y_and_f32", "f32", "y_is_ym", "y_is_kc", "f32_over_ym"])
+@pytest.mark.parametrize("case", ["y", "y_and_f32", "f32", "y_is_ym", "y_is_kc", "f32_over_ym", "y_is_ym_and_f32"])
 def test_unmask_short_a_outputs(M, case):
     """Unmask with at most 64 rows over several column tiles (N = 700, R =
     1088): an output that shares no memory with the inputs holds the product
-    until the elementwise pass (y, y with y_f32, y_f32 alone); in place on ym
-    or kc, or y_f32 over ym's memory, the whole-tile kernel runs. Every
-    case equals the oracle."""
+    until the elementwise pass (y, y with y_f32, y_f32 alone, and y_f32 when
+    y is in place on ym); in place on ym or kc, or y_f32 over ym's memory,
+    the whole-tile kernel runs. Every case equals the oracle."""
     N, R = 700, 1088
     rng = _rng_np(M * 3 + len(case))
     ym = _random_ring(rng, (M, N))
@@ -298,12 +298,12 @@ def test_unmask_short_a_outputs(M, case):
     ymd, kcd = to_dev_ring(ym), to_dev_ring(kc)
     sr = torch.rand(M, device="cuda") * 1e-3
     sc = torch.rand(N, device="cuda") * 1e-3
-    want_f32 = case in ("y_and_f32", "f32", "f32_over_ym")
+    want_f32 = case in ("y_and_f32", "f32", "f32_over_ym", "y_is_ym_and_f32")
     y = {"y": torch.empty((M, N), dtype=torch.int32, device="cuda"),
          "y_and_f32": torch.empty((M, N), dtype=torch.int32, device="cuda"),
-         "y_is_ym": ymd, "y_is_kc": kcd}.get(case)
+         "y_is_ym": ymd, "y_is_kc": kcd, "y_is_ym_and_f32": ymd}.get(case)
     yf = None
-    if case in ("y_and_f32", "f32"):
+    if case in ("y_and_f32", "f32", "y_is_ym_and_f32"):
         yf = torch.empty((M, N), dtype=torch.float32, device="cuda")
     elif case == "f32_over_ym":
         yf = ymd.view(torch.float32)
