@@ -163,7 +163,11 @@ mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch,
  * (then q and l are ignored). y: M x N int32 (ldo), the centred lift.
  * Optional dequantisation (Pi_Sec-Linear, online step 3): if y_f32 is not
  * NULL it receives (float)y(i, j) * s_rows[i] * s_cols[j] (ldf); y may then
- * be NULL. */
+ * be NULL. An output may coincide with ym or kc element for element (in
+ * place, same leading dimension); otherwise outputs and inputs must not
+ * overlap. Output memory may hold intermediate values while the call runs
+ * (with at most 64 rows, an output that shares no memory with the inputs
+ * accumulates the product before the final pass). */
 mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy,
                             const uint32_t* kc, int64_t ldk,
                             const int8_t* q_dig, int64_t q_pitch,
