@@ -318,6 +318,28 @@ def test_unmask_short_a_outputs(M, case):
         assert np.array_equal(yf.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("M", [130, 257])
+@pytest.mark.parametrize("target", ["ym", "kc"])
+def test_unmask_in_place_tiled(M, target):
+    """Unmask through the tiled kernel (more than 64 rows) with y in place on
+    ym or on kc: each thread loads its chunks' inputs before storing."""
+    N, R = 300, 192
+    rng = _rng_np(M + 11 * len(target))
+    ym = _random_ring(rng, (M, N))
+    kc = _random_ring(rng, (M, N))
+    q = _random_ring(rng, (M, R))
+    l = _random_ring(rng, (N, R))
+    Q, L = Digits.empty(M, R), Digits.empty(N, R)
+    m.mosaic_mask(to_dev_ring(q), None, None, M, R, out_dig=Q)
+    m.mosaic_mask(to_dev_ring(l), None, None, N, R, out_dig=L)
+    ymd, kcd = to_dev_ring(ym), to_dev_ring(kc)
+    y = ymd if target == "ym" else kcd
+    m.mosaic_unmask(ymd, kcd, Q, L, M, N, R, y=y)
+    torch.cuda.synchronize()
+    ref = ring_sub(ring_sub(ym, kc), ring_matmul(q, l.T)).view(np.int32)
+    assert np.array_equal(y.cpu().numpy(), ref)
+
+
 @pytest.mark.parametrize("M,N", [(40, 90), (150, 90), (150, 92), (300, 260)])
 def test_unmask_dequantised(M, N):
     rng = _rng_np(5 + M + N)
