@@ -553,7 +553,8 @@ def run_decode(dev):
     ranks (1536, 1024, 652), sparse mode). Per shape and M: the server product
     ([Y' | Q], N + 2560 output columns) and the whole call (Init X, mask,
     server, unmask), HIP-event means over 20 calls; GB/s counts the server
-    product's operand and output bytes once. The server loop and the three
+    product's operand and output bytes once; ring-TOPS counts the plaintext
+    product's 2 M K N ring ops over the server time. The server loop and the three
     whole-call loops are also timed as replayed HIP graphs of 20 calls (the
     device time without the host's per-launch cost). Calls cycle through distinct
     masked weights (independent masks of the same W) whose server matrices
@@ -634,6 +635,7 @@ def run_decode(dev):
             res.append({"K": K, "N": N, "M": M, "server_us": round(server_ms * 1e3, 2),
                         "server_gbs": round(byts / (server_ms * 1e-3) / 1e9, 1),
                         "server_hbm_frac": round(byts / (server_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
+                        "server_ring_tops": round(2.0 * M * K * N / (server_ms * 1e-3) / 1e12, 3),
                         "server_us_graph": round(server_graph_ms * 1e3, 2),
                         "server_hbm_frac_graph": round(byts / (server_graph_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3),
                         "call_us": round(call_ms * 1e3, 2),
