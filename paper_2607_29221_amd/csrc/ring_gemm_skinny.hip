@@ -42,7 +42,8 @@
 // With the short K of unmasking (the rank) that kernel has only N / 32 or
 // N / 64 workgroups: at the decode unmask shapes (N 4096 / 14336, rank 1024 /
 // 2560) the two-phase path takes 1.5-3.3x less time for 64 tokens, 6-23%
-// less for 8, and is within 5% either way for one token.
+// less for 8, and is within 5% either way for one token; for A of at most
+// 16 rows it runs only when the factor is large (see the launcher).
 //
 // LDS layout (shared-A kernel). A stage row is 256 bytes: 4 groups of 16
 // columns, each holding its 4 digit planes in 64 consecutive bytes, i.e. 16
@@ -248,9 +249,6 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
 // ---------------------------------------------------------------------------
 // K-split kernel (unmask epilogue)
 
-constexpr int KS_WAVES = 4;
-constexpr int KS_THREADS = 64 * KS_WAVES;
-
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, int64_t bytes) {
   // out-of-range offsets read as zero
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
@@ -287,22 +285,22 @@ __device__ __forceinline__ void transpose4(v4i (&q)[4]) {
   swap16(q[2], q[3]);
 }
 
-// Workgroup b: column tile b (16 NT rows of B), all stages, split into 4
+// Workgroup b: column tile b (16 NT rows of B), all stages, split into W
 // contiguous parts, one per wave. Load t of a wave reads bytes 64 t .. +64
 // of the stage in all 16 rows of a tile (lane (h, r) the 16 bytes at
 // 64 t + 16 h of row r), so every load consumes whole 64-byte segments; lane
 // group h then holds digit h of column group t in register quad t, and a
 // 4 x 4 transpose between lane groups and register quads (two rounds of
-// lane-swap instructions) turns that into the fragment of digit t. For A of
-// up to 16 rows each wave keeps two stages of loads in flight; with more
-// rows the accumulators leave no registers for a second set of fragments.
-// Prefetches past the wave's last stage are clamped to that stage: the
-// duplicate request hits in cache and the loop needs no branches around
-// loads. K must be non-zero.
-template <int MT, int NT, int DB>
-__global__ __launch_bounds__(KS_THREADS) void ring_gemm_skinny_unmask_kernel(GemmLaunch g) {
+// lane-swap instructions) turns that into the fragment of digit t. Each
+// wave holds S sets of fragments, so S stages of loads are in flight while
+// it multiplies; with more than 16 rows of A the accumulators leave room for
+// one set only. Prefetches past the wave's last stage are clamped to that
+// stage: the duplicate request hits in cache and the loop needs no branches
+// around loads. K must be non-zero.
+template <int MT, int NT, int S, int W>
+__global__ __launch_bounds__(64 * W) void ring_gemm_skinny_unmask_kernel(GemmLaunch g) {
   constexpr int NOUT = MT * NT * 4;   // output registers per lane
-  __shared__ uint32_t red[KS_WAVES][NOUT][64];
+  __shared__ uint32_t red[W][NOUT][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int stages = (int)(g.Kp / 64);
@@ -320,7 +318,7 @@ __global__ __launch_bounds__(KS_THREADS) void ring_gemm_skinny_unmask_kernel(Gem
   for (int i = 0; i < MT; ++i) oa[i] = (i * 16 + r) * (int)g.a_pitch + h * 16;
 
   // this wave's share [s0, s1) of the stages
-  const int per = (stages + KS_WAVES - 1) / KS_WAVES;
+  const int per = (stages + W - 1) / W;
   const int s0 = wave * per < stages ? wave * per : stages;
   const int s1 = (s0 + per) < stages ? (s0 + per) : stages;
 
@@ -333,7 +331,7 @@ __global__ __launch_bounds__(KS_THREADS) void ring_gemm_skinny_unmask_kernel(Gem
       for (int c = 0; c < 4; ++c) acc[i][j][c] = v4i{0, 0, 0, 0};
 
   if (s0 < s1) {
-    v4i fa[1 + DB][MT][4], fb[1 + DB][NT][4];
+    v4i fa[S][MT][4], fb[S][NT][4];
 
 #define KS_LOAD(SET, S)                                                                    \
   do {                                                                                     \
@@ -362,14 +360,15 @@ __global__ __launch_bounds__(KS_THREADS) void ring_gemm_skinny_unmask_kernel(Gem
     const int cnt = s1 - s0;
     const int rot = (int)(blockIdx.x % (unsigned)cnt);
 #define KS_STAGE(i) (s0 + (((i) + rot) < cnt ? ((i) + rot) : ((i) + rot - cnt)))
-    if constexpr (DB) {
-      KS_LOAD(0, KS_STAGE(0));
-      KS_LOAD(DB, KS_STAGE(1 < cnt ? 1 : cnt - 1));
-      for (int i = 0; i < cnt; i += 2) {
-        KS_MFMA(0);
-        KS_LOAD(0, KS_STAGE((i + 2) < cnt ? (i + 2) : cnt - 1));
-        if (i + 1 < cnt) KS_MFMA(DB);
-        KS_LOAD(DB, KS_STAGE((i + 3) < cnt ? (i + 3) : cnt - 1));
+    if constexpr (S > 1) {
+#pragma unroll
+      for (int q = 0; q < S; ++q) KS_LOAD(q, KS_STAGE(q < cnt ? q : cnt - 1));
+      for (int i = 0; i < cnt; i += S) {
+#pragma unroll
+        for (int q = 0; q < S; ++q) {
+          if (q == 0 || i + q < cnt) KS_MFMA(q);
+          KS_LOAD(q, KS_STAGE((i + q + S) < cnt ? (i + q + S) : cnt - 1));
+        }
       }
     } else {
       for (int i = 0; i < cnt; ++i) {
@@ -394,11 +393,11 @@ __global__ __launch_bounds__(KS_THREADS) void ring_gemm_skinny_unmask_kernel(Gem
             ((uint32_t)acc[i][j][2][v] << 16) + ((uint32_t)acc[i][j][3][v] << 24);
   __syncthreads();
 
-  for (int idx = threadIdx.x; idx < NOUT * 64; idx += KS_THREADS) {
+  for (int idx = threadIdx.x; idx < NOUT * 64; idx += 64 * W) {
     const int q = idx >> 6, l = idx & 63;
     uint32_t val = 0;
 #pragma unroll
-    for (int w = 0; w < KS_WAVES; ++w) val += red[w][q][l];
+    for (int w = 0; w < W; ++w) val += red[w][q][l];
     const int i = q / (NT * 4), j = (q / 4) % NT, v = q % 4;
     const int64_t m = i * 16 + 4 * (l >> 4) + v;
     const int64_t n = n0 + j * 16 + (l & 15);
@@ -461,10 +460,10 @@ uint32_t* unmask_scratch(const GemmLaunch& g, int64_t* ld) {
   return nullptr;
 }
 
-template <int MT, int NT, int DB>
+template <int MT, int NT, int S, int W>
 hipError_t launch_unmask(const GemmLaunch& g, hipStream_t s) {
   const int64_t tiles = (g.N + 16 * NT - 1) / (16 * NT);
-  hipLaunchKernelGGL((ring_gemm_skinny_unmask_kernel<MT, NT, DB>), dim3((unsigned)tiles), dim3(KS_THREADS), 0, s, g);
+  hipLaunchKernelGGL((ring_gemm_skinny_unmask_kernel<MT, NT, S, W>), dim3((unsigned)tiles), dim3(64 * W), 0, s, g);
   return hipGetLastError();
 }
 
@@ -483,8 +482,13 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
     return hipGetLastError();
   }
   if (epi == EPI_UNMASK) {
+    // The two-phase path costs two more launches (clear, elementwise): for
+    // A of at most 16 rows it pays only once the factor read is large (one
+    // row against rank-1536 factors of 12-96 MiB, the single launch took
+    // 0-20% less device time; at 168 MiB the two were equal).
+    const bool two_phase = mt >= 2 || g.N * 4 * g.Kp >= (int64_t(128) << 20);
     int64_t ldp = 0;
-    uint32_t* prod = unmask_scratch(g, &ldp);
+    uint32_t* prod = two_phase ? unmask_scratch(g, &ldp) : nullptr;
     if (prod != nullptr) {
       GemmLaunch p = g;
       p.c = prod;
@@ -496,10 +500,15 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
       if (e != hipSuccess) return e;
       return launch_unmask_elementwise(p, s);
     }
-    // NT: 16-row tiles of B per workgroup; DB: double-buffered fragments
-    if (mt <= 1) return launch_unmask<1, 2, 1>(g, s);
-    if (mt == 2) return launch_unmask<2, 4, 0>(g, s);
-    return launch_unmask<4, 4, 0>(g, s);
+    // NT: 16-row tiles of B per workgroup; S: stages in flight per wave;
+    // W: waves splitting K. One tile per workgroup while that leaves no
+    // compute unit idle (one row, 2048 x 1536 factor: 7.6 against 10.9 us).
+    // For one row, 8 or 16 waves and 3 to 6 stages in flight were slower at
+    // every size tried (factors of 12-96 MiB: by 4-50%).
+    if (mt <= 1 && g.N <= 16 * compute_units()) return launch_unmask<1, 1, 2, 4>(g, s);
+    if (mt <= 1) return launch_unmask<1, 2, 2, 4>(g, s);
+    if (mt == 2) return launch_unmask<2, 4, 1, 4>(g, s);
+    return launch_unmask<4, 4, 1, 4>(g, s);
   }
   // MT: 16-row tiles of A (33-64 rows padded to 64: faster than 48 rows on
   // one row of waves); WM: rows of 4 waves

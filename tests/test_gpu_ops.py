@@ -254,9 +254,13 @@ def test_masked_matmul_ldc_and_offsets(M, K):
 
 
 @pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192), (1, 300, 2560), (8, 33, 64),
-                                   (200, 132, 192), (130, 256, 64), (257, 4, 128)])
+                                   (200, 132, 192), (130, 256, 64), (257, 4, 128), (1, 4096, 1536),
+                                   (1, 4200, 1536), (16, 4111, 320)])
 @pytest.mark.parametrize("with_k", [True, False])
 def test_unmask(M, N, R, with_k):
+    """Y = Ym - Kc - Q L^T against the oracle; at up to 16 rows the kernel
+    takes one 16-column tile per workgroup up to N = 16 x compute units
+    (4096 on 256 units) and two above (4111, 4200: ragged last tiles)."""
     rng = _rng_np(M + N + R)
     ym = _random_ring(rng, (M, N))
     kc = _random_ring(rng, (M, N)) if with_k else None
@@ -282,10 +286,11 @@ def test_unmask(M, N, R, with_k):
 @pytest.mark.parametrize("case", ["y", "y_and_f32", "f32", "y_is_ym", "y_is_kc", "f32_over_ym", "y_is_ym_and_f32"])
 def test_unmask_short_a_outputs(M, case):
     """Unmask with at most 64 rows over several column tiles (N = 700, R =
-    1088): an output that shares no memory with the inputs holds the product
-    until the elementwise pass (y, y with y_f32, y_f32 alone, and y_f32 when
-    y is in place on ym); in place on ym or kc, or y_f32 over ym's memory,
-    the whole-tile kernel runs. Every case equals the oracle."""
+    1088): for 20 and 64 rows an output that shares no memory with the
+    inputs holds the product until the elementwise pass (y, y with y_f32,
+    y_f32 alone, and y_f32 when y is in place on ym); in place on ym or kc,
+    or y_f32 over ym's memory, and for one row with this small factor, the
+    whole-tile kernel runs. Every case equals the oracle."""
     N, R = 700, 1088
     rng = _rng_np(M * 3 + len(case))
     ym = _random_ring(rng, (M, N))
@@ -314,6 +319,34 @@ def test_unmask_short_a_outputs(M, case):
     if y is not None:
         assert np.array_equal(y.cpu().numpy(), yi)
     if want_f32:
+        ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+        assert np.array_equal(yf.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("with_f32", [False, True])
+def test_unmask_one_row_large_factor(with_f32):
+    """One row against a large factor (N = 16384, R = 2048: 128 MiB of
+    digits): the product goes through the disjoint output and the
+    elementwise pass; equal to the oracle."""
+    M, N, R = 1, 16384, 2048
+    rng = _rng_np(77 + with_f32)
+    ym = _random_ring(rng, (M, N))
+    kc = _random_ring(rng, (M, N))
+    q = _random_ring(rng, (M, R))
+    l = _random_ring(rng, (N, R))
+    Q, L = Digits.empty(M, R), Digits.empty(N, R)
+    m.mosaic_mask(to_dev_ring(q), None, None, M, R, out_dig=Q)
+    m.mosaic_mask(to_dev_ring(l), None, None, N, R, out_dig=L)
+    y = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    sr = torch.rand(M, device="cuda") * 1e-3
+    sc = torch.rand(N, device="cuda") * 1e-3
+    yf = torch.empty((M, N), dtype=torch.float32, device="cuda") if with_f32 else None
+    m.mosaic_unmask(to_dev_ring(ym), to_dev_ring(kc), Q, L, M, N, R, y=y, s_rows=sr if with_f32 else None,
+                    s_cols=sc if with_f32 else None, y_f32=yf)
+    torch.cuda.synchronize()
+    yi = ring_sub(ring_sub(ym, kc), ring_matmul(q, l.T)).view(np.int32)
+    assert np.array_equal(y.cpu().numpy(), yi)
+    if with_f32:
         ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
         assert np.array_equal(yf.cpu().numpy(), ref)
 
