@@ -8,9 +8,11 @@ from __future__ import annotations
 
 import ctypes
 import os
+from typing import Optional
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmosaic.so")
+_DEFAULT_LIB_PATH = LIB_PATH
 
 c_i32 = ctypes.c_int32
 c_i64 = ctypes.c_int64
@@ -66,11 +68,30 @@ EXPORTED = tuple(_SIGNATURES)
 _lib = None
 
 
+def stale_reason() -> Optional[str]:
+    """Why the in-tree library does not match the sources, or None. The build
+    writes a digest of its sources beside the library; a library built from
+    other sources (an edit after the last build) would run other kernels
+    than the ones in the tree."""
+    from . import build as _build
+    if not os.path.exists(_build.STAMP):
+        return f"{_build.STAMP} is missing"
+    with open(_build.STAMP) as f:
+        stamp = f.read().strip()
+    if stamp != _build.source_digest():
+        return "the sources under csrc/ or include/ changed after the last build"
+    return None
+
+
 def load() -> ctypes.CDLL:
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2607_29221_amd.build`")
+        if LIB_PATH == _DEFAULT_LIB_PATH:
+            why = stale_reason()
+            if why is not None:
+                raise RuntimeError(f"{LIB_PATH} is stale ({why}): run `python -m paper_2607_29221_amd.build`")
         lib = ctypes.CDLL(LIB_PATH)
         for name, (args, res) in _SIGNATURES.items():
             fn = getattr(lib, name)

@@ -2,10 +2,14 @@
 
 Every HIP source under csrc/ is compiled to an object file under _build/ and
 linked into paper_2607_29221_amd/libmosaic.so. Run ``python -m
-paper_2607_29221_amd.build`` (or ``__graft_entry__.build()``).
+paper_2607_29221_amd.build`` (or ``__graft_entry__.build()``). Beside the
+library the build writes libmosaic.so.sources, a digest of every file it was
+built from (csrc/, include/) and of the compiler flags; the loader refuses a
+library whose digest no longer matches the sources.
 """
 from __future__ import annotations
 
+import hashlib
 import os
 import subprocess
 import sys
@@ -16,6 +20,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmosaic.so")
+STAMP = LIB + ".sources"
+INCLUDE = os.path.join(ROOT, "include")
 ARCH = os.environ.get("MOSAIC_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -25,6 +31,21 @@ FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-x", "hip",
          # keep the compiler from forming packed fp32 instructions
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-command-line-argument"]
+
+
+def source_digest() -> str:
+    """sha256 over the names and contents of every file under csrc/ and
+    include/, the compiler flags and the target architecture."""
+    h = hashlib.sha256()
+    h.update(" ".join(FLAGS + [HIPCC]).encode())
+    for d in (CSRC, INCLUDE):
+        for name in sorted(os.listdir(d)):
+            path = os.path.join(d, name)
+            if os.path.isfile(path):
+                h.update(name.encode() + b"\0")
+                with open(path, "rb") as f:
+                    h.update(f.read())
+    return h.hexdigest()
 
 
 def _compile(src: str) -> str:
@@ -37,6 +58,7 @@ def _compile(src: str) -> str:
 
 
 def build(verbose: bool = False) -> str:
+    digest = source_digest()
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
@@ -46,6 +68,8 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}\n{res.stderr}")
     os.replace(tmp, LIB)
+    with open(STAMP, "w") as f:
+        f.write(digest + "\n")
     if verbose:
         print(f"built {LIB}")
     return LIB

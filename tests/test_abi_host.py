@@ -35,6 +35,22 @@ def test_every_declared_symbol_is_exported(lib):
     assert set(names) == set(_lib.EXPORTED)
 
 
+def test_library_matches_sources():
+    """The in-tree library was built from the sources in the tree."""
+    assert _lib.stale_reason() is None
+
+
+def test_stale_library_is_refused(monkeypatch):
+    """A library whose recorded source digest differs from the sources is
+    not loaded (it would run other kernels than the tree holds)."""
+    from paper_2607_29221_amd import build
+    monkeypatch.setattr(build, "source_digest", lambda: "0" * 64)
+    monkeypatch.setattr(_lib, "_lib", None)
+    assert "changed after the last build" in _lib.stale_reason()
+    with pytest.raises(RuntimeError, match="stale"):
+        _lib.load()
+
+
 def test_abi_version(lib):
     m = re.search(r"#define MOSAIC_ABI_VERSION (\d+)", open(HEADER).read())
     assert lib.mosaic_abi_version() == int(m.group(1))
