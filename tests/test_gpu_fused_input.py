@@ -31,7 +31,7 @@ def _separate(x, block, signs, qmax, u, noise):
 @pytest.mark.parametrize("rows,n,block,qmax", [(5, 8192, 8192, 1997), (3, 28672, 4096, 567), (4, 1024, 1024, 300),
                                                (2, 16384, 16384, 1000), (3, 3072, 1024, 127), (2, 32768, 4096, 511),
                                                (2, 36864, 4096, 400), (3, 6144, 2048, 255), (3, 8192, 4096, 777),
-                                               (3, 8192, 1024, 1997)])
+                                               (3, 8192, 1024, 1997), (2, 16384, 8192, 1500)])
 @pytest.mark.parametrize("with_u,with_noise", [(True, True), (False, False), (True, False)])
 def test_fused_matches_separate_passes(rows, n, block, qmax, with_u, with_noise):
     x = torch.from_numpy(outlier_activations(rows, n, rows + n)).cuda()

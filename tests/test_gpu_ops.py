@@ -395,7 +395,8 @@ def test_unmask_dequantised(M, N):
 
 @pytest.mark.parametrize("rows,n,block", [(3, 16, 16), (4, 32, 32), (5, 64, 64), (3, 128, 128), (2, 4096, 256),
                                           (3, 512, 512), (4, 1024, 1024), (3, 2048, 2048), (3, 28672, 4096),
-                                          (6, 8192, 8192), (2, 16384, 16384), (2, 32768, 32768)])
+                                          (6, 8192, 8192), (3, 24576, 8192), (2, 16384, 16384),
+                                          (2, 32768, 32768)])
 @pytest.mark.parametrize("inverse", [False, True])
 def test_hadamard(rows, n, block, inverse):
     x = _rng_np(n + rows).standard_normal((rows, n)).astype(np.float32)
