@@ -24,10 +24,12 @@ namespace mosaic {
 
 __host__ __device__ constexpr int ilog2c(int v) { return v <= 1 ? 0 : 1 + ilog2c(v >> 1); }
 
-template <int LOGB>
+// TMAX: most threads per block transform (256, or 512 for kernels that want
+// more waves per block).
+template <int LOGB, int TMAX = 256>
 struct FwhtShape {
   static constexpr int B = 1 << LOGB;
-  static constexpr int T = (B / 4 < 256) ? B / 4 : 256;   // threads per block transform
+  static constexpr int T = (B / 4 < TMAX) ? B / 4 : TMAX;  // threads per block transform
   static constexpr int LOGT = ilog2c(T);
   static constexpr int E = B / T;                           // elements per thread, >= 4
   static constexpr int LOGE = LOGB - LOGT;
@@ -37,15 +39,29 @@ struct FwhtShape {
   // SIMD (T = 256: one wave per SIMD per workgroup), capped at 4; used as the
   // occupancy the register allocation must allow
   static constexpr int LDS_WG = (160 * 1024) / (SM * 4);
-  static constexpr int WAVES = T < 256 ? 4 : (LDS_WG < 4 ? (LDS_WG < 1 ? 1 : LDS_WG) : 4);
+  static constexpr int WG_W = T >= 256 ? T / 256 : 1;     // waves per SIMD of one workgroup
+  static constexpr int WAVES = T < 256 ? 4 : (LDS_WG * WG_W < 4 ? (LDS_WG < 1 ? WG_W : LDS_WG * WG_W) : 4);
 };
+
+// Threads per block transform in the rotation kernel and the fused input
+// kernels (they must agree: the thread count fixes which butterfly stages
+// run in registers, lanes or LDS, and so the rounding). 512 for b = 8192,
+// where the block's LDS (33 KiB) admits four workgroups per compute unit:
+// eight waves per workgroup instead of four double the waves resident and
+// halve each thread's share of the block (4096 x 8192 rotation: 45.3 against
+// 47.0 us); 256 otherwise.
+__host__ __device__ constexpr int fwht_tmax(int logb) { return logb == 13 ? 512 : 256; }
+
+// One thread's share of a block, as registers.
+template <int LOGB, int TMAX = 256>
+using FwhtRegs = float[FwhtShape<LOGB, TMAX>::E];
 
 __device__ __forceinline__ int fwht_pad(int idx) { return idx + (idx >> 5); }
 
 // v[r] *= d of its element (load layout), d = +-1 from the int8 signs at sg.
-template <int LOGB>
-__device__ __forceinline__ void apply_signs(const int8_t* __restrict__ sg, float (&v)[FwhtShape<LOGB>::E]) {
-  using S = FwhtShape<LOGB>;
+template <int LOGB, int TMAX = 256>
+__device__ __forceinline__ void apply_signs(const int8_t* __restrict__ sg, FwhtRegs<LOGB, TMAX>& v) {
+  using S = FwhtShape<LOGB, TMAX>;
   constexpr int T = S::T, NV = S::NV;
   const int t = threadIdx.x;
 #pragma unroll
@@ -60,10 +76,10 @@ __device__ __forceinline__ void apply_signs(const int8_t* __restrict__ sg, float
 // thread t: element 4 (t + T (r / 4)) + r % 4), times the signs at sg if SG.
 // NT selects non-temporal loads, for data that is read once. Signs are a
 // compile-time choice: a run-time test between the loads serialises them.
-template <int LOGB, bool SG, bool NT>
+template <int LOGB, bool SG, bool NT, int TMAX = 256>
 __device__ __forceinline__ void fwht_load(const float* __restrict__ xr, const int8_t* __restrict__ sg,
-                                          float (&v)[FwhtShape<LOGB>::E]) {
-  using S = FwhtShape<LOGB>;
+                                          FwhtRegs<LOGB, TMAX>& v) {
+  using S = FwhtShape<LOGB, TMAX>;
   constexpr int T = S::T, NV = S::NV;
   const int t = threadIdx.x;
 #pragma unroll
@@ -72,7 +88,7 @@ __device__ __forceinline__ void fwht_load(const float* __restrict__ xr, const in
     const f32x4 f = NT ? __builtin_nontemporal_load(p) : *p;
     v[4 * k + 0] = f[0]; v[4 * k + 1] = f[1]; v[4 * k + 2] = f[2]; v[4 * k + 3] = f[3];
   }
-  if (SG) apply_signs<LOGB>(sg, v);
+  if (SG) apply_signs<LOGB, TMAX>(sg, v);
 }
 
 // Value of x held by lane (lane ^ M) of the wave, M in {1, 2, 4, 8}: DPP
@@ -160,9 +176,9 @@ __device__ __forceinline__ void reg_stage(float (&v)[E]) {
 // The stages that stay inside the wave (registers, lanes), for one block;
 // returns the lane sign c. For b >= 512 the element layout is left with the
 // two lane/register exchanges in place (the LDS pass undoes them).
-template <int LOGB>
-__device__ __forceinline__ float fwht_in_wave(float (&v)[FwhtShape<LOGB>::E], int lane) {
-  using S = FwhtShape<LOGB>;
+template <int LOGB, int TMAX = 256>
+__device__ __forceinline__ float fwht_in_wave(FwhtRegs<LOGB, TMAX>& v, int lane) {
+  using S = FwhtShape<LOGB, TMAX>;
   constexpr int LOGT = S::LOGT, E = S::E;
 
   // stages on the index bits held in registers: bits of r = 4 k + q
@@ -218,15 +234,15 @@ __device__ __forceinline__ float fwht_in_wave(float (&v)[FwhtShape<LOGB>::E], in
 // row swaps and run in registers. The stages on wave bits (index bits 8 and
 // 9, present for b >= 512) go through one LDS pass, whose write addresses
 // undo the two exchanges; for b <= 256 the exchanges are swapped back.
-template <int LOGB, int NB>
-__device__ __forceinline__ float fwht_transform_blocks(float* sm, float (&v)[NB][FwhtShape<LOGB>::E]) {
-  using S = FwhtShape<LOGB>;
+template <int LOGB, int NB, int TMAX = 256>
+__device__ __forceinline__ float fwht_transform_blocks(float* sm, FwhtRegs<LOGB, TMAX> (&v)[NB]) {
+  using S = FwhtShape<LOGB, TMAX>;
   constexpr int T = S::T, LOGT = S::LOGT, E = S::E, SM = S::SM;
   const int t = threadIdx.x;
   const int lane = t & 63;
   float c = 1.0f;
 #pragma unroll
-  for (int k = 0; k < NB; ++k) c = fwht_in_wave<LOGB>(v[k], lane);   // the same c for every block
+  for (int k = 0; k < NB; ++k) c = fwht_in_wave<LOGB, TMAX>(v[k], lane);   // the same c for every block
 
   if constexpr (LOGT > 6) {
     // Write every element at its index: register r of lane l now holds the
@@ -280,9 +296,9 @@ __device__ __forceinline__ float fwht_transform_blocks(float* sm, float (&v)[NB]
 }
 
 // One block (see fwht_transform_blocks).
-template <int LOGB>
-__device__ __forceinline__ float fwht_transform(float* sm, float (&v)[FwhtShape<LOGB>::E]) {
-  return fwht_transform_blocks<LOGB, 1>(sm, reinterpret_cast<float (&)[1][FwhtShape<LOGB>::E]>(v));
+template <int LOGB, int TMAX = 256>
+__device__ __forceinline__ float fwht_transform(float* sm, FwhtRegs<LOGB, TMAX>& v) {
+  return fwht_transform_blocks<LOGB, 1, TMAX>(sm, reinterpret_cast<FwhtRegs<LOGB, TMAX> (&)[1]>(v));
 }
 
 }  // namespace mosaic

@@ -13,10 +13,11 @@ namespace {
 // SIGNS: 0 none, 1 applied on load (forward), 2 applied on store (inverse).
 // x is read once and y written once, so both use non-temporal accesses.
 template <int LOGB, int SIGNS>
-__global__ __launch_bounds__(FwhtShape<LOGB>::T) void fwht_kernel(
+__global__ __launch_bounds__((FwhtShape<LOGB, fwht_tmax(LOGB)>::T)) void fwht_kernel(
     const float* __restrict__ x, int64_t ldx, float* y, int64_t ldy, int64_t blocks_per_row,
     const int8_t* __restrict__ signs, float scale) {
-  using S = FwhtShape<LOGB>;
+  constexpr int TM = fwht_tmax(LOGB);
+  using S = FwhtShape<LOGB, TM>;
   constexpr int T = S::T, E = S::E, NV = S::NV, B = S::B;
   __shared__ float sm[S::SM];
   const int t = threadIdx.x;
@@ -27,11 +28,11 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void fwht_kernel(
   const int8_t* sg = SIGNS ? signs + blk * B : nullptr;
 
   float v[E];
-  fwht_load<LOGB, SIGNS == 1, true>(xr, sg, v);
-  const float sc = scale * fwht_transform<LOGB>(sm, v);   // the transform's lane sign folded into the scale
+  fwht_load<LOGB, SIGNS == 1, true, TM>(xr, sg, v);
+  const float sc = scale * fwht_transform<LOGB, TM>(sm, v);   // the transform's lane sign folded into the scale
 #pragma unroll
   for (int r = 0; r < E; ++r) v[r] *= sc;
-  if (SIGNS == 2) apply_signs<LOGB>(sg, v);
+  if (SIGNS == 2) apply_signs<LOGB, TM>(sg, v);
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const f32x4 f = {v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
@@ -42,8 +43,8 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void fwht_kernel(
 template <int LOGB>
 hipError_t launch_fwht(const float* x, int64_t ldx, float* y, int64_t ldy, int64_t rows, int64_t n,
                        const int8_t* signs, int inverse, hipStream_t s) {
-  constexpr int B = FwhtShape<LOGB>::B;
-  constexpr int T = FwhtShape<LOGB>::T;
+  constexpr int B = FwhtShape<LOGB, fwht_tmax(LOGB)>::B;
+  constexpr int T = FwhtShape<LOGB, fwht_tmax(LOGB)>::T;
   const int64_t bpr = n / B;
   const int64_t grid = rows * bpr;
   if (grid == 0) return hipSuccess;

@@ -30,9 +30,13 @@
 namespace mosaic {
 namespace {
 
+// The block shape of the rotation kernel for the same b (same butterfly order).
+template <int LOGB>
+using FS = FwhtShape<LOGB, fwht_tmax(LOGB)>;
+
 template <int LOGB>
 __device__ __forceinline__ float block_max(float m, float* red) {
-  constexpr int T = FwhtShape<LOGB>::T;
+  constexpr int T = FS<LOGB>::T;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
@@ -44,12 +48,12 @@ __device__ __forceinline__ float block_max(float m, float* red) {
 }
 
 template <int LOGB, bool SG>
-__global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float* __restrict__ x, int64_t ldx,
+__global__ __launch_bounds__((FS<LOGB>::T)) void rqm_max_kernel(const float* __restrict__ x, int64_t ldx,
                                                                      int64_t n, const int8_t* __restrict__ signs,
                                                                      float scale_b, float* amax_out) {
-  using S = FwhtShape<LOGB>;
+  using S = FS<LOGB>;
   constexpr int E = S::E, B = S::B;
-  static_assert(S::T == 256, "four full waves per workgroup");
+  static_assert(S::T % 256 == 0, "full waves on every SIMD");
   __shared__ float sm[S::SM];
   __shared__ float red[S::T / 64];
   const int64_t row = blockIdx.x;
@@ -57,8 +61,9 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float
   float m = 0.0f;
   for (int64_t blk = 0; blk < n / B; ++blk) {
     float v[E];
-    fwht_load<LOGB, SG, false>(xr + blk * B, SG ? signs + blk * B : nullptr, v);   // x is read again next launch
-    fwht_transform<LOGB>(sm, v);    // the lane sign it returns does not change |y|
+    // x is read again by the next launch: cached loads
+    fwht_load<LOGB, SG, false, fwht_tmax(LOGB)>(xr + blk * B, SG ? signs + blk * B : nullptr, v);
+    fwht_transform<LOGB, fwht_tmax(LOGB)>(sm, v);    // the lane sign it returns does not change |y|
 #pragma unroll
     for (int r = 0; r < E; ++r) m = fmaxf(m, fabsf(v[r] * scale_b));
     __syncthreads();                // the next block reuses the scratch
@@ -73,11 +78,11 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_max_kernel(const float
 // or all before the first use) holds them in registers, fewer workgroups fit
 // and the pass ran 10-25% slower.
 template <int LOGB, bool SG, bool HU, bool HN>
-__global__ __launch_bounds__(FwhtShape<LOGB>::T, FwhtShape<LOGB>::WAVES) void rqm_mask_kernel(
+__global__ __launch_bounds__((FS<LOGB>::T), (FS<LOGB>::WAVES)) void rqm_mask_kernel(
     const float* __restrict__ x, int64_t ldx, int64_t n, const int8_t* __restrict__ signs, float scale_b,
     int32_t qmax, const uint32_t* __restrict__ u, int64_t ldu, RngArgs noise, int8_t* out_dig, int64_t pitch,
     float* scale) {
-  using S = FwhtShape<LOGB>;
+  using S = FS<LOGB>;
   constexpr int T = S::T, E = S::E, NV = S::NV, B = S::B;
   __shared__ float sm[S::SM];
   const int t = threadIdx.x;
@@ -87,8 +92,8 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T, FwhtShape<LOGB>::WAVES) void rq
   const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
   for (int64_t blk = 0; blk < n / B; ++blk) {
     float v[E];
-    fwht_load<LOGB, SG, true>(xr + blk * B, SG ? signs + blk * B : nullptr, v);
-    const float sb = scale_b * fwht_transform<LOGB>(sm, v);   // the lane sign folded into the scale
+    fwht_load<LOGB, SG, true, fwht_tmax(LOGB)>(xr + blk * B, SG ? signs + blk * B : nullptr, v);
+    const float sb = scale_b * fwht_transform<LOGB, fwht_tmax(LOGB)>(sm, v);   // the lane sign folded into the scale
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       // columns 4 c .. 4 c + 3 of the row; lanes t .. t + 3 hold one 16-column group
@@ -119,10 +124,10 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T, FwhtShape<LOGB>::WAVES) void rq
 // 12 bytes of HBM traffic per element instead of 16, the same arithmetic as
 // the two launches above (so the same digits). Signs and u are present.
 template <int LOGB, int NB, int G, bool HN>
-__global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_row_kernel(
+__global__ __launch_bounds__((FS<LOGB>::T)) void rqm_row_kernel(
     const float* __restrict__ x, int64_t ldx, const int8_t* __restrict__ signs, float scale_b, int32_t qmax,
     const uint32_t* __restrict__ u, int64_t ldu, RngArgs noise, int8_t* out_dig, int64_t pitch, float* scale) {
-  using S = FwhtShape<LOGB>;
+  using S = FS<LOGB>;
   constexpr int T = S::T, E = S::E, NV = S::NV, B = S::B;
   constexpr int64_t n = (int64_t)NB * B;
   static_assert(NB % G == 0, "groups of G blocks");
@@ -134,11 +139,12 @@ __global__ __launch_bounds__(FwhtShape<LOGB>::T) void rqm_row_kernel(
 
   float v[NB][E];
 #pragma unroll
-  for (int k = 0; k < NB; ++k) fwht_load<LOGB, true, true>(xr + k * B, signs + k * B, v[k]);
+  for (int k = 0; k < NB; ++k) fwht_load<LOGB, true, true, fwht_tmax(LOGB)>(xr + k * B, signs + k * B, v[k]);
   float c = 1.0f;
 #pragma unroll
   for (int g = 0; g < NB; g += G) {
-    c = fwht_transform_blocks<LOGB, G>(sm, reinterpret_cast<float (&)[G][E]>(v[g]));   // same lane sign
+    // every group returns the same lane sign
+    c = fwht_transform_blocks<LOGB, G, fwht_tmax(LOGB)>(sm, reinterpret_cast<float (&)[G][E]>(v[g]));
     __syncthreads();
   }
   float m = 0.0f;
@@ -177,7 +183,7 @@ template <int LOGB, int NB, int G>
 hipError_t launch_rqm_row(const float* x, int64_t ldx, int64_t rows, const int8_t* signs, int32_t qmax,
                           const uint32_t* u, int64_t ldu, const RngArgs* noise, int8_t* out_dig, int64_t pitch,
                           float* scale, hipStream_t s) {
-  using S = FwhtShape<LOGB>;
+  using S = FS<LOGB>;
   const float scale_b = (float)(1.0 / sqrt((double)S::B));
   if (noise != nullptr)
     hipLaunchKernelGGL((rqm_row_kernel<LOGB, NB, G, true>), dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, signs,
@@ -192,7 +198,7 @@ template <int LOGB, bool SG, bool HU, bool HN>
 hipError_t launch_rqm_t(const float* x, int64_t ldx, int64_t rows, int64_t n, const int8_t* signs, int32_t qmax,
                         const uint32_t* u, int64_t ldu, const RngArgs* noise, int8_t* out_dig, int64_t pitch,
                         float* scale, hipStream_t s) {
-  using S = FwhtShape<LOGB>;
+  using S = FS<LOGB>;
   const float scale_b = (float)(1.0 / sqrt((double)S::B));
   hipLaunchKernelGGL((rqm_max_kernel<LOGB, SG>), dim3((unsigned)rows), dim3(S::T), 0, s, x, ldx, n, signs, scale_b,
                      scale);
