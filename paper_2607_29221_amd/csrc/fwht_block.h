@@ -9,7 +9,8 @@
 //    top bits from k);
 //  * the stages on index bits 2-7, the lane bits of t, exchange values
 //    between the lanes of a wave (DPP, swizzle and lane-swap instructions);
-//  * the stages on the wave bits of t (index bits 8-9, for b >= 512) go
+//  * the stages on the wave bits of t (index bits 8 .. 1 + log2 T: 8-9 for
+//    256 threads, 8-10 for 512; present for b >= 512) go
 //    through LDS in one pass: the block is written out, each thread gathers
 //    2 or 4 elements that differ in those bits, runs the stages and writes
 //    them back, and the result is read back in the load layout (register r
@@ -170,8 +171,8 @@ __device__ __forceinline__ void reg_stage(float (&v)[E]) {
 // stages on register bits run in registers. Those on lane bits 0-3 (index
 // bits 2-5) take the partner's value by DPP or swizzle; those on lane bits 4
 // and 5 (index bits 6, 7) exchange the lane bit with register bit 1 or 0 by
-// row swaps and run in registers. The stages on wave bits (index bits 8 and
-// 9, present for b >= 512) go through one LDS pass, whose write addresses
+// row swaps and run in registers. The stages on wave bits (index bits 8 ..
+// 1 + log2 T, present for b >= 512) go through one LDS pass, whose write addresses
 // undo the two exchanges; for b <= 256 the exchanges are swapped back.
 // The stages that stay inside the wave (registers, lanes), for one block;
 // returns the lane sign c. For b >= 512 the element layout is left with the
@@ -231,8 +232,8 @@ __device__ __forceinline__ float fwht_in_wave(FwhtRegs<LOGB, TMAX>& v, int lane)
 // stages on register bits run in registers. Those on lane bits 0-3 (index
 // bits 2-5) take the partner's value by DPP or swizzle; those on lane bits 4
 // and 5 (index bits 6, 7) exchange the lane bit with register bit 1 or 0 by
-// row swaps and run in registers. The stages on wave bits (index bits 8 and
-// 9, present for b >= 512) go through one LDS pass, whose write addresses
+// row swaps and run in registers. The stages on wave bits (index bits 8 ..
+// 1 + log2 T, present for b >= 512) go through one LDS pass, whose write addresses
 // undo the two exchanges; for b <= 256 the exchanges are swapped back.
 template <int LOGB, int NB, int TMAX = 256>
 __device__ __forceinline__ float fwht_transform_blocks(float* sm, FwhtRegs<LOGB, TMAX> (&v)[NB]) {
