@@ -12,7 +12,7 @@
 //  * the stages on the wave bits of t (index bits 8 .. 1 + log2 T: 8-9 for
 //    256 threads, 8-10 for 512; present for b >= 512) go
 //    through LDS in one pass: the block is written out, each thread gathers
-//    2 or 4 elements that differ in those bits, runs the stages and writes
+//    2, 4 or 8 elements that differ in those bits, runs the stages and writes
 //    them back, and the result is read back in the load layout (register r
 //    of thread t holds element 4 (t + T (r / 4)) + r % 4), unscaled.
 // LDS addresses are padded by one word per 32 (idx + idx / 32), which makes
