@@ -2,6 +2,7 @@
 // Every launcher assumes its arguments were validated by the ABI layer.
 #pragma once
 
+#include <atomic>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -79,15 +80,19 @@ hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s
 // kernel that streams B once and splits K inside each workgroup.
 constexpr int64_t SKINNY_MAX_M = 64;
 
-// Compute units of the current device (cached per device id).
+// Compute units of the current device (cached per device id; host threads
+// may call it concurrently).
 inline int compute_units() {
-  static int cached[64];
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) dev = 0;
-  if (dev >= 0 && dev < 64 && cached[dev] > 0) return cached[dev];
+  if (dev >= 0 && dev < 64) {
+    const int c = cached[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
   int v = 0;
   if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-  if (dev >= 0 && dev < 64) cached[dev] = v;
+  if (dev >= 0 && dev < 64) cached[dev].store(v, std::memory_order_relaxed);
   return v;
 }
 hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStream_t s);
