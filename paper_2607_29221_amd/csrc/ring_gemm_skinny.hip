@@ -405,9 +405,26 @@ __global__ __launch_bounds__(64 * W) void ring_gemm_skinny_unmask_kernel(GemmLau
   }
 }
 
+// Zeroes the M x N words at c (leading dimension ldc): block (x, y) covers
+// columns 1024 x .. 1024 x + 1023 of rows y, y + gridDim.y, ...; each thread
+// four consecutive words, one 16-byte store where the row allows it.
 __global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, int64_t M, int64_t N) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e < M * N) c[(e / N) * ldc + e % N] = 0u;
+  const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (j >= N) return;
+  for (int64_t row = blockIdx.y; row < M; row += gridDim.y) {
+    uint32_t* cr = c + row * ldc + j;
+    if (j + 4 <= N && ((uintptr_t)cr & 15) == 0) {
+      *(u32x4*)cr = u32x4{0u, 0u, 0u, 0u};
+    } else {
+      for (int q = 0; q < 4 && j + q < N; ++q) cr[q] = 0u;
+    }
+  }
+}
+
+void launch_clear_c(uint32_t* c, int64_t ldc, int64_t M, int64_t N, hipStream_t s) {
+  if (M <= 0 || N <= 0) return;
+  const dim3 grid((unsigned)((N + 1023) / 1024), (unsigned)(M < 65535 ? M : 65535));
+  hipLaunchKernelGGL(clear_c_kernel, grid, dim3(256), 0, s, c, ldc, M, N);
 }
 
 // Store and accumulate: the (tile, stage) units cut into one range per
@@ -418,9 +435,7 @@ hipError_t launch_shared_a(const GemmLaunch& g, EpilogueKind epi, hipStream_t s)
   const int64_t units = tiles * (g.Kp / 64);
   const int64_t cus = compute_units();
   const int64_t grid = cus < (units + 1) / 2 ? cus : (units + 1) / 2;
-  if (epi == EPI_STORE)
-    hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc, g.M,
-                       g.N);
+  if (epi == EPI_STORE) launch_clear_c(g.c, g.ldc, g.M, g.N, s);
   hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, WM>), dim3((unsigned)grid), dim3(64 * WM * SA_WN), 0, s, g, units);
   return hipGetLastError();
 }
@@ -476,9 +491,7 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
     // K = 0 leaves only the epilogue: C = 0, C unchanged, or the unmask of a
     // zero product
     if (epi == EPI_UNMASK) return launch_unmask_elementwise(g, s);
-    if (epi == EPI_STORE)
-      hipLaunchKernelGGL(clear_c_kernel, dim3((unsigned)((g.M * g.N + 255) / 256)), dim3(256), 0, s, g.c, g.ldc,
-                         g.M, g.N);
+    if (epi == EPI_STORE) launch_clear_c(g.c, g.ldc, g.M, g.N, s);
     return hipGetLastError();
   }
   if (epi == EPI_UNMASK) {
