@@ -13,7 +13,7 @@ which holds for honest outputs by associativity ((a^T W') X' = a^T (W' X'))
 and costs O((m + n) l t) instead of the O(m n l) of the product.
 
 Readings (each listed in the design notes):
-  * the box compares Y^chk X against a^T Y'; the server computes Y' = W' X',
+  * the protocol box compares Y^chk X against a^T Y'; the server computes Y' = W' X',
     so the comparison is made on the masked activations X' (otherwise it
     fails for honest outputs whenever U_x != 0);
   * the Q_i the server returns are covered too, with their own vectors (the

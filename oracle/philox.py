@@ -1,8 +1,8 @@
 """Philox counter-based generator (Salmon, Moraes, Dror, Shaw, "Parallel random
 numbers: as easy as 1, 2, 3", SC'11), restated from that paper.
 
-The MOSAIC paper does not name a generator for its mask material; both sides
-of this build draw it from Philox-4x32 with 10 rounds.
+The MOSAIC paper does not name a generator for its mask material; both the
+oracle and the GPU kernels draw it from Philox-4x32 with 10 rounds.
 
 Philox-4xW: the state is four W-bit words (c0, c1, c2, c3) (the counter) and a
 key of two W-bit words (k0, k1). One round multiplies c0 and c2 by fixed odd

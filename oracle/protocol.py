@@ -8,7 +8,7 @@ Y^T (l x m); ``run`` converts at the boundary only.
 Readings where the paper is ambiguous (listed with reasons in the design notes):
 * the sparse masks are S_{i+1} in Z^{m x r_i} and T_{i+1} in Z^{r_i x l}, the
   only dimensions under which S_{i+1} (M_i ... M_1) and N_1 ... N_i T_{i+1}
-  are defined (the box prints r_i x r_{i-1} and r_{i-1} x r_i);
+  are defined (the protocol box prints r_i x r_{i-1} and r_{i-1} x r_i);
 * the chains M_i ... M_1 and N_1 ... N_i start from M_1 in Z^{r_1 x n} and
   N_1 in Z^{n x r_1} (r_0 = n);
 * activation-side random matrices (R, E_x, T_i) are drawn element by element

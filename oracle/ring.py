@@ -11,7 +11,7 @@ Signed digits. The paper emulates one 32-bit multiply-accumulate with 8-bit
 multiply-accumulates by splitting each operand into four 8-bit limbs and
 recombining with shifts; because only residues mod 2^32 matter, the limb
 products a_i * b_j with i + j >= 4 vanish, leaving ten products (Section 6.1).
-This build uses balanced limbs: x = sum_{t<4} d_t 256^t (mod 2^32) with every
+Here the limbs are balanced: x = sum_{t<4} d_t 256^t (mod 2^32) with every
 d_t in [-128, 127]. That representation exists and is unique for every x
 (four base-256 digits shifted by -128 cover each residue exactly once).
 

@@ -2,10 +2,10 @@
 the C ABI. This module only allocates device buffers and orders the calls;
 every arithmetic step is a libmosaic kernel.
 
-Orientation (build layout): activations A are M x K (tokens x features),
+Orientation (row-major layout): activations A are M x K (tokens x features),
 weights W are N x K (out x in), outputs are M x N. In the paper's notation
 A = X^T and the output is (W X)^T; every product below is the transpose of
-the box's product and is computed as C = A B^T by mosaic_masked_matmul.
+the protocol box's product and is computed as C = A B^T by mosaic_masked_matmul.
 
 Factors of different levels are concatenated along the inner dimension, in
 the slot order (level d, level 1, ..., level d-1):

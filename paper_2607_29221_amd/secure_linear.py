@@ -10,7 +10,7 @@ Init W (once per weight matrix W, N x K fp32):
      (int8 weights: q_w = 127) with scale s_w = max |row| / q_w;
   3. Init W of Pi_Sec-Approx-MatMul on the integer codes.
 Online (activations A, M x K fp32, one row per token):
-  1. rotate every token, A~ = A R^T (the box's R X in build layout), and
+  1. rotate every token, A~ = A R^T (the protocol box's R X in the row-major layout), and
      quantise each token to q_x with scale s_x;
   2. Init X, mask, server product and unmask of Pi_Sec-Approx-MatMul;
   3. dequantise in the unmask epilogue: Y = s_x[m] s_w[n] Y^[m, n].
