@@ -6,7 +6,8 @@ computes, written from the paper's definitions (arxiv 2607.29221):
 * ``philox``    -- the counter-based generator (Salmon et al., SC'11) that both
                    sides use for the random mask material;
 * ``sampling``  -- uniform ring elements, the discrete Gaussian of Section 4.1
-                   ("Bounded protocol error"), LPN sparse noise (Background);
+                   ("Bounded protocol error"), LPN sparse noise of rate mu
+                   (Background) and of fixed row weight t (Example 4.1);
 * ``ring``      -- Z_{2^32} matrix arithmetic and the signed-digit encoding
                    used by the 8-bit emulation (Section 6.1, "Emulation
                    approach");

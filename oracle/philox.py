@@ -21,7 +21,9 @@ to W bits (the tests recompute them from those closed forms).
 ``philox_generic`` is the scalar reference for any W; ``philox4x32_np`` is the
 same function for W = 32 vectorised over numpy arrays. The tests pin the
 generic function's W = 64 instance against ``numpy.random.Philox`` (a
-Philox-4x64-10 implementation) and the vectorised one against the generic one.
+Philox-4x64-10 implementation), its W = 32 instance and the vectorised one
+against rocRAND's Philox4x32-10 block function (built on the host from
+rocRAND's open-source header), and the vectorised one against the generic one.
 """
 from __future__ import annotations
 

@@ -70,6 +70,30 @@ def _noise(params, rows, cols, seed, stream, instance, transposed=False):
                              sigma=nz.sigma, bound=nz.bound)
 
 
+def _lpn(params, level: int, rows: int, cols: int, seed: int, stream: int, instance: int) -> np.ndarray:
+    """The sparse LPN matrix of level ``level`` (S_level or T_level^T, rows x
+    cols): fixed row Hamming weight t_level when the parameters give one
+    (Example 4.1), else the rate-2^-s sampler."""
+    w = tuple(getattr(params, "lpn_weights", ()) or ())
+    if w:
+        return smp.sample_matrix("weight", rows, cols, seed, stream, instance, row_weight=w[level - 2])
+    return smp.sample_matrix("sparse", rows, cols, seed, stream, instance,
+                             log2_inv_density=params.sparse_log2_inv_density)
+
+
+def client_cost_per_row(params) -> int:
+    """The client's multiplications per output element of unmasking (and per
+    input element of masking), r_d + sum_{i=2}^{d} t_i: the dense level-d
+    factor plus one product per nonzero of each sparse level (Section 4.2
+    cost analysis, Table "lpn-tradeoff"). Requires fixed row weights for
+    d >= 2."""
+    r = list(params.ranks)
+    w = list(getattr(params, "lpn_weights", ()) or ())
+    if len(w) != len(r) - 1:
+        raise ValueError("the cost needs a row weight for every LPN level")
+    return r[-1] + sum(w)
+
+
 def init_w(W_plain: np.ndarray, params, seed: int, weight_id: int) -> WeightState:
     """Init W of the protocol box for a plaintext m x n weight matrix."""
     W = to_ring(W_plain)
@@ -86,8 +110,7 @@ def init_w(W_plain: np.ndarray, params, seed: int, weight_id: int) -> WeightStat
     E_w = _noise(params, m, n, seed, smp.STREAM_EW, weight_id)
     S: List[Optional[np.ndarray]] = [None] * d
     for i in range(1, d):
-        S[i] = smp.sample_matrix("sparse", m, r[i - 1], seed, smp.STREAM_S + i + 1, weight_id,
-                                 log2_inv_density=params.sparse_log2_inv_density)
+        S[i] = _lpn(params, i + 1, m, r[i - 1], seed, smp.STREAM_S + i + 1, weight_id)
     # chains M_i ... M_1 and N_1 ... N_i
     Mc = [M[0]]
     Nc = [N[0]]
@@ -117,8 +140,7 @@ def init_x(ws: WeightState, l: int, params, seed: int, call_id: int) -> CallStat
     E_x = _noise(params, n, l, seed, smp.STREAM_EX, call_id, transposed=True)
     T: List[Optional[np.ndarray]] = [None] * d
     for i in range(1, d):
-        T[i] = smp.sample_matrix("sparse", l, r[i - 1], seed, smp.STREAM_T + i + 1, call_id,
-                                 log2_inv_density=params.sparse_log2_inv_density).T.copy()
+        T[i] = _lpn(params, i + 1, l, r[i - 1], seed, smp.STREAM_T + i + 1, call_id).T.copy()
     # step 1b: U_x = N_1...N_d R + sum_{i=1}^{d-1} N_1...N_i T_{i+1} + E_x
     U_x = ring_matmul(ws.Nc[d - 1], R)
     for i in range(1, d):

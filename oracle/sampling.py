@@ -20,6 +20,16 @@ e = i * cols + j, and consumes words in that order:
 * sparse LPN noise S(.; mu) (Background, "LWE and LPN": sparse uniform with
   noise rate mu), mu = 2^-s: element e takes words 2e (gate) and 2e+1 (value)
   and is the value word if the top s bits of the gate word are zero, else 0;
+* LPN noise of fixed row Hamming weight t (Example 4.1 parameterises the
+  LPN levels by t = 80 nonzeros per noise vector): row i of a rows x cols
+  matrix consumes words 2 t i .. 2 t i + 2 t - 1. Its t nonzero columns are
+  the first t entries of a partial Fisher-Yates shuffle of 0 .. cols-1: step
+  j (j = 0 .. t-1) swaps entries j and j + floor(u_j (cols - j) / 2^32) of
+  the running permutation, u_j = word 2 t i + 2 j; the entry at the column
+  chosen in step j is word 2 t i + 2 j + 1 (a value of 0 is kept as drawn,
+  as in the rate-mu sampler). Every t-subset of columns is then chosen with
+  probability 1 / C(cols, t) up to the rounding of u_j (cols - j) / 2^32,
+  which moves each step's probabilities by less than cols / 2^32;
 * random signs d in {+1, -1}^n (Section 5, "Random Hadamard rotation"):
   d_j = +1 if bit 31 of word j is 0, else -1.
 """
@@ -126,9 +136,53 @@ def _elements(kind: str, e0: int, count: int, seed: int, stream: int, instance: 
     raise ValueError(f"unknown distribution {kind!r}")
 
 
+def weighted_rows(row_ids, cols: int, t: int, seed: int, stream: int, instance: int):
+    """Nonzero columns and values of rows ``row_ids`` of the fixed-weight LPN
+    matrix (t nonzeros per row, see the module notes): returns (positions,
+    values), two (len(row_ids), t) arrays; positions[:, j] is the column
+    chosen in step j of the row's partial shuffle and values[:, j] its
+    entry."""
+    row_ids = np.asarray(list(row_ids), dtype=np.int64)
+    n = row_ids.size
+    if not 0 <= t <= cols:
+        raise ValueError("row weight must satisfy 0 <= t <= cols")
+    if n == 0 or t == 0:
+        return np.zeros((n, t), dtype=np.int64), np.zeros((n, t), dtype=np.uint32)
+    if np.array_equal(row_ids, np.arange(row_ids[0], row_ids[0] + n)):    # consecutive rows: one range
+        words = stream_words(seed, stream, instance, 2 * t * int(row_ids[0]), 2 * t * n).reshape(n, 2 * t)
+    else:
+        words = np.stack([stream_words(seed, stream, instance, 2 * t * int(i), 2 * t) for i in row_ids])
+    u = words[:, 0::2].astype(np.uint64)
+    vals = words[:, 1::2].astype(np.uint32)
+    perm = np.tile(np.arange(cols, dtype=np.int64), (n, 1))
+    rix = np.arange(n)
+    for j in range(t):
+        k = j + ((u[:, j] * np.uint64(cols - j)) >> np.uint64(32)).astype(np.int64)
+        pj = perm[rix, j].copy()
+        perm[rix, j] = perm[rix, k]
+        perm[rix, k] = pj
+    return perm[:, :t].copy(), vals
+
+
+def sample_weighted(rows: int, cols: int, t: int, seed: int, stream: int, instance: int) -> np.ndarray:
+    """The rows x cols fixed-weight LPN matrix as a dense uint32 matrix."""
+    out = np.zeros((rows, cols), dtype=np.uint32)
+    chunk = 4096
+    for r0 in range(0, rows, chunk):
+        ids = range(r0, min(rows, r0 + chunk))
+        pos, val = weighted_rows(ids, cols, t, seed, stream, instance)
+        out[np.arange(r0, r0 + pos.shape[0])[:, None], pos] = val
+    return out
+
+
 def sample_matrix(kind: str, rows: int, cols: int, seed: int, stream: int, instance: int,
-                  sigma: float = 0.5, bound: int = 4, log2_inv_density: int = 6) -> np.ndarray:
-    """A logical rows x cols matrix over Z_{2^32} (uint32, two's complement)."""
+                  sigma: float = 0.5, bound: int = 4, log2_inv_density: int = 6,
+                  row_weight: int = 0) -> np.ndarray:
+    """A logical rows x cols matrix over Z_{2^32} (uint32, two's complement);
+    kind "weight" is the fixed-weight LPN matrix with ``row_weight`` nonzeros
+    per row."""
+    if kind == "weight":
+        return sample_weighted(rows, cols, row_weight, seed, stream, instance)
     return _elements(kind, 0, rows * cols, seed, stream, instance, sigma, bound,
                      log2_inv_density).reshape(rows, cols)
 

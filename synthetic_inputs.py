@@ -40,11 +40,14 @@ class ProtocolParams:
 
     ranks: (r_1, ..., r_d); depth d = len(ranks); r_1 > r_2 > ... > r_d.
     sparse_log2_inv_density: the LPN masks S_i, T_i have density 2^-k.
+    lpn_weights: (t_2, ..., t_d), the fixed row Hamming weight of S_{i+1}
+        and of each token's row of T_{i+1}; empty means the density rule.
     noise: the LWE error E_w / E_x.
     """
     ranks: Tuple[int, ...] = (128,)
     noise: NoiseSpec = field(default_factory=NoiseSpec)
     sparse_log2_inv_density: int = 6
+    lpn_weights: Tuple[int, ...] = ()
 
     @property
     def depth(self) -> int:
@@ -64,6 +67,16 @@ PARAMS_PAPER_D2_SPARSE = ProtocolParams(ranks=(1536, 1024), noise=NoiseSpec("zer
 # Depth 3 with the paper's ranks (1536, 1024, 652) (Section 4.2 example
 # parameterisation), sparse levels at density 1/64, no E.
 PARAMS_PAPER_D3_SPARSE = ProtocolParams(ranks=(1536, 1024, 652), noise=NoiseSpec("zero", 0.0, 0))
+# Example 4.1 in full: LWE r_1 = 1536 with sigma = 0.5, LPN-1 r_2 = 1024 and
+# LPN-2 r_3 = 652, both with row Hamming weight t = 80.
+PARAMS_PAPER_D3_T80 = ProtocolParams(ranks=(1536, 1024, 652), noise=NoiseSpec("dgauss", 0.5, 4),
+                                     lpn_weights=(80, 80))
+# Depth 2 with the paper's first two levels (r_2 = 1024, t_2 = 80) and sigma = 0.5.
+PARAMS_PAPER_D2_T80 = ProtocolParams(ranks=(1536, 1024), noise=NoiseSpec("dgauss", 0.5, 4),
+                                     lpn_weights=(80,))
+# Small fixed-weight instance for parity at the single-matmul size.
+PARAMS_D3_WEIGHT_SMALL = ProtocolParams(ranks=(192, 128, 64), noise=NoiseSpec("dgauss", 0.5, 4),
+                                        lpn_weights=(12, 9))
 
 
 # ---------------------------------------------------------------------------

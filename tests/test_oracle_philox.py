@@ -1,4 +1,7 @@
 """Pins for the oracle's Philox generator (CPU only)."""
+import os
+import shutil
+import subprocess
 from decimal import Decimal, getcontext
 
 import numpy as np
@@ -59,6 +62,61 @@ def test_weyl_constants_closed_form():
         w0, w1 = PHILOX_CONSTANTS[w]["W"]
         assert w0 == int(phi_frac * (2 ** w))
         assert w1 == int(s3_frac * (2 ** w))
+
+
+ROCRAND_HEADER = "/opt/rocm/include/rocrand/rocrand_philox4x32_10.h"
+
+
+@pytest.fixture(scope="module")
+def rocrand_block(tmp_path_factory):
+    """rocRAND's Philox-4x32-10 block function, built on the host from its
+    open-source header (an implementation independent of the oracle)."""
+    if not os.path.exists(ROCRAND_HEADER) or shutil.which("g++") is None:
+        pytest.skip("rocRAND header or g++ not available")
+    exe = str(tmp_path_factory.mktemp("rocrand") / "philox_ref")
+    src = os.path.join(os.path.dirname(__file__), "rocrand_philox_ref.cpp")
+    subprocess.run(["g++", "-O1", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", src, "-o", exe],
+                   check=True, capture_output=True)
+
+    def run(pairs):
+        text = "".join(" ".join(str(int(v)) for v in (*c, *k)) + "\n" for c, k in pairs)
+        out = subprocess.run([exe], input=text, capture_output=True, text=True, check=True).stdout
+        return [tuple(int(v) for v in line.split()) for line in out.strip().splitlines()]
+    return run
+
+
+def test_philox4x32_matches_rocrand(rocrand_block):
+    """The 4x32 instance (multipliers 0xD2511F53 / 0xCD9E8D57, ten rounds)
+    equals rocRAND's Philox4x32-10 on 64 random (counter, key) pairs and on
+    all-zero, all-one and digits-of-pi inputs; a wrong multiplier, Weyl
+    increment, round count or output permutation fails it."""
+    m = 2 ** 32 - 1
+    pairs = [((0, 0, 0, 0), (0, 0)), ((m, m, m, m), (m, m)),
+             ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0)),
+             ((1, 0, 0, 0), (0, 0)), ((0, 0, 0, 1), (0, 1))]
+    rng = np.random.default_rng(2024)
+    for _ in range(64):
+        c = tuple(int(v) for v in rng.integers(0, 2 ** 32, 4, dtype=np.uint64))
+        k = tuple(int(v) for v in rng.integers(0, 2 ** 32, 2, dtype=np.uint64))
+        pairs.append((c, k))
+    ref = rocrand_block(pairs)
+    assert len(ref) == len(pairs)
+    for (c, k), r in zip(pairs, ref):
+        assert philox_generic(c, k, width=32) == r
+    c = np.array([p[0] for p in pairs], dtype=np.uint64).T
+    for (c_, k), r in zip(pairs, ref):
+        out = philox4x32_np(*[np.array([v], dtype=np.uint64) for v in c_], k[0], k[1])
+        assert tuple(int(o[0]) for o in out) == r
+
+
+def test_stream_words_match_rocrand(rocrand_block):
+    """The oracle's stream (key = seed halves, counter = (block lo, block hi,
+    stream, instance)) built on rocRAND's block function."""
+    seed, st, inst = 0x0123_4567_89AB_CDEF, 0x51, 7
+    words = stream_words(seed, st, inst, 0, 64)
+    pairs = [((b, 0, st, inst), (seed & 0xFFFFFFFF, seed >> 32)) for b in range(16)]
+    ref = rocrand_block(pairs)
+    assert [int(w) for w in words] == [v for blk in ref for v in blk]
 
 
 def test_multipliers_odd():

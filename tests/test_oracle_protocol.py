@@ -146,3 +146,21 @@ def test_sampled_depth1_matches_full_run(noise):
     assert np.array_equal(s["A_masked"], full.X_masked.T[I])
     assert np.array_equal(s["K_c"], full.cs.K.T[np.ix_(I, J)])
     assert np.array_equal(s["Y"], s["identity"])
+
+
+@pytest.mark.parametrize("weights", [(3,), (5, 2)])
+def test_fixed_weight_levels(weights):
+    """With fixed row weights (Example 4.1's parameterisation) S_{i+1} has t
+    nonzeros in every row, T_{i+1} in every column (one token's noise
+    vector), and unmasking still returns (W + E_w)(X + E_x) exactly."""
+    ranks = (12, 8, 6)[: len(weights) + 1]
+    A, W = _plain(5, 12, 10, seed=11)
+    p = ProtocolParams(ranks=ranks, noise=SMALL, lpn_weights=weights)
+    res = proto.run(A, W, p, seed=77, weight_id=1, call_id=2)
+    for i, t in enumerate(weights, start=1):
+        assert np.all(np.count_nonzero(res.ws.S[i], axis=1) == t)
+        assert np.all(np.count_nonzero(res.cs.T[i], axis=0) == t)
+    X = A.T.astype(np.int64)
+    lhs = W.astype(np.int64) + lift(res.ws.E_w).astype(np.int64)
+    rhs = X + lift(res.cs.E_x).astype(np.int64)
+    assert np.array_equal(res.Y, _int_matmul(lhs & 0xFFFFFFFF, rhs & 0xFFFFFFFF))

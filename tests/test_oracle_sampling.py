@@ -100,3 +100,64 @@ def test_signs_balanced():
     d = smp.sample_signs(1 << 16, 3)
     assert set(np.unique(d)) == {-1, 1}
     assert abs(d.mean()) < 5 / math.sqrt(d.size)
+
+
+# --- fixed-weight LPN noise (Example 4.1: t nonzeros per noise vector) ---
+
+def test_weighted_rows_exact_weight_and_range():
+    """Every row has exactly t distinct columns in [0, cols) (also t = cols,
+    a full permutation, and t = 0)."""
+    for cols, t in [(1536, 80), (1024, 80), (7, 7), (64, 1), (33, 0)]:
+        pos, val = smp.weighted_rows(range(200), cols, t, 11, 0x44, 2)
+        assert pos.shape == (200, t) and val.shape == (200, t)
+        for row in pos:
+            assert len(set(row.tolist())) == t
+            assert all(0 <= p < cols for p in row)
+        if t == cols:
+            assert all(sorted(row.tolist()) == list(range(cols)) for row in pos)
+    S = smp.sample_matrix("weight", 300, 1536, 5, 0x43, 1, row_weight=80)
+    assert np.all(np.count_nonzero(S, axis=1) == 80)     # a zero value has probability 80 * 2^-32
+
+
+def test_weighted_subsets_uniform():
+    """All C(5, 2) = 10 column pairs (and all 4! orders of a full shuffle of
+    4) appear equally often: a partial shuffle that picked from the wrong
+    range or swapped the wrong entries biases these counts."""
+    pos, _ = smp.weighted_rows(range(30000), 5, 2, 3, 0x45, 0)
+    keys = np.sort(pos, axis=1)
+    codes = keys[:, 0] * 5 + keys[:, 1]
+    counts = np.bincount(codes, minlength=25)
+    cells = counts[[a * 5 + b for a in range(5) for b in range(a + 1, 5)]]
+    assert cells.sum() == 30000
+    exp = 3000.0
+    assert float(((cells - exp) ** 2 / exp).sum()) < 33.7          # chi2, 9 dof, p ~ 1e-4
+    perm, _ = smp.weighted_rows(range(24000), 4, 4, 4, 0x46, 0)
+    codes = perm[:, 0] * 64 + perm[:, 1] * 16 + perm[:, 2] * 4 + perm[:, 3]
+    _, counts = np.unique(codes, return_counts=True)
+    assert counts.size == 24
+    assert float(((counts - 1000.0) ** 2 / 1000.0).sum()) < 49.7     # chi2, 23 dof, p ~ 1e-3
+
+
+def test_weighted_positions_uniform_at_paper_size():
+    """At r = 1536, t = 80 each column is chosen with probability t / r."""
+    pos, val = smp.weighted_rows(range(3000), 1536, 80, 8, 0x47, 0)
+    counts = np.bincount(pos.ravel(), minlength=1536)
+    exp = 3000 * 80 / 1536
+    chi2 = float(((counts - exp) ** 2 / exp).sum())
+    assert abs(chi2 - 1535) < 6 * math.sqrt(2 * 1535)
+    by = np.frombuffer(val.tobytes(), dtype=np.uint8)
+    bc = np.bincount(by, minlength=256)
+    assert float(((bc - by.size / 256) ** 2 / (by.size / 256)).sum()) < 400
+
+
+def test_weighted_row_uses_its_own_words():
+    """Row i is a function of words 2 t i .. 2 t i + 2 t - 1 only: the same row
+    drawn alone or inside a range agrees, and the first step's column is
+    floor(u_0 cols / 2^32)."""
+    t, cols = 80, 1024
+    a, va = smp.weighted_rows([17], cols, t, 9, 0x48, 3)
+    b, vb = smp.weighted_rows(range(10, 30), cols, t, 9, 0x48, 3)
+    assert np.array_equal(a[0], b[7]) and np.array_equal(va[0], vb[7])
+    w = smp.stream_words(9, 0x48, 3, 2 * t * 17, 2 * t)
+    assert a[0, 0] == (int(w[0]) * cols) >> 32
+    assert np.array_equal(va[0], w[1::2])
