@@ -42,6 +42,15 @@
  *            truncated to [-B, B]);
  *   SPARSE   element e is word 2e+1 if the top s bits of word 2e are zero,
  *            else 0 (LPN noise of rate 2^-s, Section 3);
+ *   WEIGHT   LPN noise with t entries per row (Example 4.1's
+ *            parameterisation by the Hamming weight t): row i uses words
+ *            2ti .. 2ti+2t-1. Starting from the identity permutation of the
+ *            columns, step j (j = 0 .. t-1) swaps entries j and
+ *            j + floor(u_j (cols - j) / 2^32), u_j = word 2ti + 2j; the column
+ *            then at entry j holds word 2ti + 2j + 1 and every other
+ *            column holds 0 (a partial Fisher-Yates shuffle: the t columns
+ *            form a uniformly random subset up to the rounding of that
+ *            product; a drawn value of 0 is kept, as for SPARSE);
  *   ZERO     element e is 0.
  *
  * Memory. Every pointer argument except ``mosaic_rng`` structs and the
@@ -69,7 +78,7 @@
 extern "C" {
 #endif
 
-#define MOSAIC_ABI_VERSION 1
+#define MOSAIC_ABI_VERSION 2
 
 typedef enum mosaic_status {
   MOSAIC_OK = 0,
@@ -82,7 +91,8 @@ typedef enum mosaic_dist {
   MOSAIC_DIST_ZERO = 0,
   MOSAIC_DIST_UNIFORM = 1,
   MOSAIC_DIST_DGAUSS = 2,
-  MOSAIC_DIST_SPARSE = 3
+  MOSAIC_DIST_SPARSE = 3,
+  MOSAIC_DIST_WEIGHT = 4
 } mosaic_dist;
 
 typedef enum mosaic_dtype {
@@ -104,13 +114,16 @@ typedef struct mosaic_rng {
   double sigma;             /* DGAUSS: parameter sigma >= 0 */
   int32_t log2_inv_density; /* SPARSE: density 2^-s, 0 <= s <= 31 */
   int32_t transposed;
+  int32_t row_weight;       /* WEIGHT: nonzeros per row t, 0 <= t <= cols */
 } mosaic_rng;
 
 /* ABI version (MOSAIC_ABI_VERSION of the built library). */
 int32_t mosaic_abi_version(void);
 
-/* Message for the last error on the calling thread ("" if none). */
+/* Message for the last error on the calling thread ("" if none).
+ * mosaic_last_error_string is the same function under a second name. */
 const char* mosaic_last_error_message(void);
+const char* mosaic_last_error_string(void);
 
 /* Host-only. Discrete Gaussian thresholds T_0 .. T_{2B-1} (Section 4.1,
  * "Bounded protocol error": Pr[k] proportional to exp(-k^2 / (2 sigma^2)),
@@ -123,7 +136,9 @@ mosaic_status mosaic_dgauss_thresholds(double sigma, int32_t bound, uint64_t* ou
  * step 1 and Init X step 1a: uniform L, M_i, N_i, R; discrete Gaussian E_w,
  * E_x; sparse S_i, T_i). Writes ring elements to ``out`` (leading dimension
  * ``ldo`` elements) and/or digits to ``out_dig`` (row pitch ``dig_pitch``
- * bytes); each output may be NULL but not both. */
+ * bytes); each output may be NULL but not both. WEIGHT streams need
+ * transposed = 0, cols <= 8192 and 0 <= row_weight <= cols (else
+ * MOSAIC_ERR_UNSUPPORTED / MOSAIC_ERR_INVALID_ARG). */
 mosaic_status mosaic_sample(const mosaic_rng* rng, int64_t rows, int64_t cols,
                             uint32_t* out, int64_t ldo,
                             int8_t* out_dig, int64_t dig_pitch, void* stream);
@@ -134,8 +149,9 @@ mosaic_status mosaic_sample(const mosaic_rng* rng, int64_t rows, int64_t cols,
  * x: plaintext of type ``x_dtype`` at x[i * x_rs + j * x_cs] (element
  * strides; NULL means 0); u: ring matrix, leading dimension ``ldu`` (NULL
  * means 0); e: drawn from ``noise`` (NULL means 0), so the Init X error can be
- * generated in the same pass. Outputs as in mosaic_sample. With x and noise
- * NULL this converts a ring matrix to digit layout. */
+ * generated in the same pass (any distribution but WEIGHT, whose rows are
+ * drawn by mosaic_sample only). Outputs as in mosaic_sample. With x and
+ * noise NULL this converts a ring matrix to digit layout. */
 mosaic_status mosaic_mask(const void* x, int32_t x_dtype, int64_t x_rs, int64_t x_cs,
                           const uint32_t* u, int64_t ldu, const mosaic_rng* noise,
                           int64_t rows, int64_t cols,
@@ -197,16 +213,22 @@ mosaic_status mosaic_rotate_quantize_mask(const float* x, int64_t ldx, int64_t r
                                           float* scale, void* stream);
 
 /* Sparse LPN matrices in compressed-row form (Section 4.2 protocol box:
- * S_{i+1} and T_{i+1} are sparse with noise rate 2^-s; the client's products
- * with them then cost O(nonzeros) per output row, Section 4.2 cost analysis
- * and Table "lpn-tradeoff").
+ * S_{i+1} and T_{i+1} are sparse, with noise rate 2^-s or with t nonzeros
+ * per row as in Example 4.1; the client's products with them then cost
+ * O(nonzeros) per output row, Section 4.2 cost analysis and Table
+ * "lpn-tradeoff").
  *
- * The matrix is the rows x cols SPARSE stream matrix of ``rng`` (rng->dist
- * must be MOSAIC_DIST_SPARSE, rng->transposed 0). Its compressed rows are
+ * The matrix is the rows x cols SPARSE or WEIGHT stream matrix of ``rng``
+ * (rng->transposed 0; WEIGHT: cols <= 8192, row_weight <= 2048). Its
+ * compressed rows are
  *   row_ptr[0 .. rows]     int64, row_ptr[0] = 0, row i owns
- *                          entries row_ptr[i] .. row_ptr[i+1]-1;
- *   col_idx[nnz], values[nnz]  column (int32, increasing within a row) and
- *                          ring value (uint32) of each nonzero.
+ *                          entries row_ptr[i] .. row_ptr[i+1]-1
+ *                          (WEIGHT: row_ptr[i] = i t);
+ *   col_idx[nnz], values[nnz]  column (int32) and ring value (uint32) of
+ *                          each entry: SPARSE lists a row's nonzeros in
+ *                          increasing column order, WEIGHT lists its t
+ *                          entries in the order of the shuffle's steps (a
+ *                          drawn value may be 0).
  * mosaic_sparse_csr_count writes row_ptr (rows + 1 entries); the caller
  * then sizes col_idx / values to at least row_ptr[rows] entries (reading it
  * back, or using the bound rows * cols) and calls mosaic_sparse_csr_fill. */
@@ -231,10 +253,10 @@ mosaic_status mosaic_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, co
                                         const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
                                         uint32_t* c, int64_t ldc, int32_t subtract, void* stream);
 /* mosaic_sparse_stream_gather_rows: as mosaic_sparse_gather_rows with P the
- *   rows x rcols SPARSE stream matrix of ``rng`` itself (same validity rules
- *   as mosaic_sparse_csr_count): each row's nonzeros are drawn inside the
- *   call, so no compressed form is stored (T_{i+1} of Init X, drawn afresh
- *   for every call). */
+ *   rows x rcols SPARSE or WEIGHT stream matrix of ``rng`` itself (same
+ *   validity rules as mosaic_sparse_csr_count): each row's nonzeros are
+ *   drawn inside the call, so no compressed form is stored (T_{i+1} of
+ *   Init X, drawn afresh for every call). */
 mosaic_status mosaic_sparse_stream_gather_rows(const mosaic_rng* rng, int64_t rows, int64_t rcols, const uint32_t* d,
                                                int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc,
                                                int32_t subtract, void* stream);

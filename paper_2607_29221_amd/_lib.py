@@ -31,6 +31,7 @@ class MosaicRng(ctypes.Structure):
         ("sigma", ctypes.c_double),
         ("log2_inv_density", c_i32),
         ("transposed", c_i32),
+        ("row_weight", c_i32),
     ]
 
 
@@ -38,6 +39,7 @@ class MosaicRng(ctypes.Structure):
 _SIGNATURES = {
     "mosaic_abi_version": ([], c_i32),
     "mosaic_last_error_message": ([], ctypes.c_char_p),
+    "mosaic_last_error_string": ([], ctypes.c_char_p),
     "mosaic_dgauss_thresholds": ([ctypes.c_double, c_i32, ctypes.POINTER(c_u64)], c_i32),
     "mosaic_sample": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr], c_i32),
     "mosaic_mask": ([c_ptr, c_i32, c_i64, c_i64, c_ptr, c_i64, ctypes.POINTER(MosaicRng), c_i64, c_i64,

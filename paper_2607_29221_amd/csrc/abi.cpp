@@ -97,6 +97,10 @@ mosaic_status rng_args(const mosaic_rng* r, RngArgs* a) {
         return fail(MOSAIC_ERR_INVALID_ARG, "sparse log2_inv_density %d outside [0, 31]", r->log2_inv_density);
       a->sparse_shift = 32 - r->log2_inv_density;
       break;
+    case MOSAIC_DIST_WEIGHT:
+      if (r->row_weight < 0) return fail(MOSAIC_ERR_INVALID_ARG, "row_weight %d is negative", r->row_weight);
+      a->row_weight = r->row_weight;
+      break;
     default:
       return fail(MOSAIC_ERR_INVALID_ARG, "unknown distribution %d", r->dist);
   }
@@ -117,6 +121,28 @@ mosaic_status check_digits(const int8_t* p, int64_t pitch, int64_t rows, int64_t
   return MOSAIC_OK;
 }
 
+// A WEIGHT stream matrix of rows x cols that the row kernels can draw.
+mosaic_status check_weighted(const mosaic_rng* r, int64_t cols) {
+  if (r->transposed) return fail(MOSAIC_ERR_UNSUPPORTED, "WEIGHT streams cannot be transposed");
+  if (r->row_weight < 0 || r->row_weight > cols)
+    return fail(MOSAIC_ERR_INVALID_ARG, "row_weight %d outside [0, cols = %lld]", r->row_weight, (long long)cols);
+  if (cols > WEIGHT_MAX_COLS || r->row_weight > WEIGHT_MAX_T)
+    return fail(MOSAIC_ERR_UNSUPPORTED, "WEIGHT needs cols <= %lld and row_weight <= %lld",
+                (long long)WEIGHT_MAX_COLS, (long long)WEIGHT_MAX_T);
+  return MOSAIC_OK;
+}
+
+// rng of the compressed-row calls: a non-transposed SPARSE or WEIGHT stream.
+mosaic_status check_lpn_rng(const mosaic_rng* r, int64_t cols, RngArgs* a) {
+  if (r == nullptr || (r->dist != MOSAIC_DIST_SPARSE && r->dist != MOSAIC_DIST_WEIGHT) || r->transposed)
+    return fail(MOSAIC_ERR_INVALID_ARG, "rng must be a non-transposed SPARSE or WEIGHT stream");
+  if (r->dist == MOSAIC_DIST_WEIGHT) {
+    const mosaic_status st = check_weighted(r, cols);
+    if (st != MOSAIC_OK) return st;
+  }
+  return rng_args(r, a);
+}
+
 }  // namespace
 
 extern "C" {
@@ -124,6 +150,8 @@ extern "C" {
 int32_t mosaic_abi_version(void) { return MOSAIC_ABI_VERSION; }
 
 const char* mosaic_last_error_message(void) { return g_last_error.c_str(); }
+
+const char* mosaic_last_error_string(void) { return g_last_error.c_str(); }
 
 mosaic_status mosaic_dgauss_thresholds(double sigma, int32_t bound, uint64_t* out) {
   if (out == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "out is NULL");
@@ -157,6 +185,8 @@ mosaic_status mosaic_mask(const void* x, int32_t x_dtype, int64_t x_rs, int64_t 
   a.ldu = ldu;
   a.has_noise = 0;
   if (noise != nullptr) {
+    if (noise->dist == MOSAIC_DIST_WEIGHT)
+      return fail(MOSAIC_ERR_UNSUPPORTED, "WEIGHT streams are drawn by mosaic_sample, not inside the mask pass");
     const mosaic_status st = rng_args(noise, &a.noise);
     if (st != MOSAIC_OK) return st;
     a.has_noise = noise->dist != MOSAIC_DIST_ZERO;
@@ -175,7 +205,24 @@ mosaic_status mosaic_mask(const void* x, int32_t x_dtype, int64_t x_rs, int64_t 
 mosaic_status mosaic_sample(const mosaic_rng* rng, int64_t rows, int64_t cols, uint32_t* out, int64_t ldo,
                             int8_t* out_dig, int64_t dig_pitch, void* stream) {
   if (rng == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "rng is NULL");
-  return mosaic_mask(nullptr, MOSAIC_U32, 0, 0, nullptr, 0, rng, rows, cols, out, ldo, out_dig, dig_pitch, stream);
+  if (rng->dist != MOSAIC_DIST_WEIGHT)
+    return mosaic_mask(nullptr, MOSAIC_U32, 0, 0, nullptr, 0, rng, rows, cols, out, ldo, out_dig, dig_pitch, stream);
+  if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (rows == 0 || cols == 0) return MOSAIC_OK;
+  if (out == nullptr && out_dig == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "no output given");
+  if (out != nullptr && ldo < cols) return fail(MOSAIC_ERR_INVALID_ARG, "ldo < cols");
+  if (out_dig != nullptr) {
+    const mosaic_status st = check_digits(out_dig, dig_pitch, rows, cols, "out_dig");
+    if (st != MOSAIC_OK) return st;
+  }
+  mosaic_status st = check_weighted(rng, cols);
+  if (st != MOSAIC_OK) return st;
+  RngArgs a{};
+  st = rng_args(rng, &a);
+  if (st != MOSAIC_OK) return st;
+  if (rows > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  return hip_status(launch_weighted_sample(a, rows, cols, out, ldo, out_dig, dig_pitch, (hipStream_t)stream),
+                    "weighted sample launch");
 }
 
 mosaic_status mosaic_sample_signs(const mosaic_rng* rng, int64_t n, int8_t* out, void* stream) {
@@ -270,12 +317,13 @@ mosaic_status mosaic_sparse_csr_count(const mosaic_rng* rng, int64_t rows, int64
   if (rows < 0 || cols < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
   if (cols > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "cols must fit int32");
   if (row_ptr == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "row_ptr is NULL");
-  if (rng == nullptr || rng->dist != MOSAIC_DIST_SPARSE || rng->transposed)
-    return fail(MOSAIC_ERR_INVALID_ARG, "rng must be a non-transposed SPARSE stream");
   RngArgs a{};
-  mosaic_status st = rng_args(rng, &a);
+  mosaic_status st = check_lpn_rng(rng, cols, &a);
   if (st != MOSAIC_OK) return st;
   if (rows > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  if (rng->dist == MOSAIC_DIST_WEIGHT)
+    return hip_status(launch_weighted_csr_count(rows, a.row_weight, row_ptr, (hipStream_t)stream),
+                      "weighted count launch");
   return hip_status(launch_sparse_csr_count(a, rows, cols, row_ptr, (hipStream_t)stream), "sparse count launch");
 }
 
@@ -286,12 +334,13 @@ mosaic_status mosaic_sparse_csr_fill(const mosaic_rng* rng, int64_t rows, int64_
   if (rows == 0 || cols == 0) return MOSAIC_OK;
   if (row_ptr == nullptr || col_idx == nullptr || values == nullptr)
     return fail(MOSAIC_ERR_INVALID_ARG, "row_ptr, col_idx or values is NULL");
-  if (rng == nullptr || rng->dist != MOSAIC_DIST_SPARSE || rng->transposed)
-    return fail(MOSAIC_ERR_INVALID_ARG, "rng must be a non-transposed SPARSE stream");
   RngArgs a{};
-  mosaic_status st = rng_args(rng, &a);
+  mosaic_status st = check_lpn_rng(rng, cols, &a);
   if (st != MOSAIC_OK) return st;
   if (rows > 0x7FFFFFFF) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
+  if (rng->dist == MOSAIC_DIST_WEIGHT)
+    return hip_status(launch_weighted_csr_fill(a, rows, cols, row_ptr, col_idx, values, (hipStream_t)stream),
+                      "weighted fill launch");
   return hip_status(launch_sparse_csr_fill(a, rows, cols, row_ptr, col_idx, values, (hipStream_t)stream),
                     "sparse fill launch");
 }
@@ -316,10 +365,8 @@ mosaic_status mosaic_sparse_stream_gather_rows(const mosaic_rng* rng, int64_t ro
   if (rows == 0 || ncols == 0) return MOSAIC_OK;
   if (c == nullptr || (rcols > 0 && d == nullptr)) return fail(MOSAIC_ERR_INVALID_ARG, "NULL operand");
   if (ldd < ncols || ldc < ncols) return fail(MOSAIC_ERR_INVALID_ARG, "leading dimension < ncols");
-  if (rng == nullptr || rng->dist != MOSAIC_DIST_SPARSE || rng->transposed)
-    return fail(MOSAIC_ERR_INVALID_ARG, "rng must be a non-transposed SPARSE stream");
   RngArgs a{};
-  mosaic_status st = rng_args(rng, &a);
+  mosaic_status st = check_lpn_rng(rng, rcols, &a);
   if (st != MOSAIC_OK) return st;
   if (rows > 0x7FFFFFFF || (ncols + 255) / 256 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
   return hip_status(launch_sparse_stream_gather_rows(a, rows, rcols, d, ldd, ncols, c, ldc, subtract != 0,

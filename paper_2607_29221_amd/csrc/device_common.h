@@ -23,6 +23,7 @@ struct RngArgs {
   int32_t bound;          // DGAUSS support [-bound, bound]
   int32_t sparse_shift;   // SPARSE: 32 - s (gate kept when gate >> shift == 0); 32 keeps all
   int32_t transposed;
+  int32_t row_weight;     // WEIGHT: entries per row
   // DGAUSS inverse-CDF table. Of the 2 bound thresholds T_k (ascending, in
   // [0, 2^32]) those equal to 0 count for every word and those equal to 2^32
   // for none: they are folded into dg_base = -bound + #{T_k = 0}; the

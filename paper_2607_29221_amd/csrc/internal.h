@@ -41,6 +41,17 @@ hipError_t launch_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_pt
                                      const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
                                      int64_t ldc, int subtract, hipStream_t s);
 
+// Fixed-row-weight (WEIGHT) streams: at most WEIGHT_MAX_COLS columns (the
+// row's permutation lives in LDS) and, where a row is staged whole in LDS,
+// WEIGHT_MAX_T entries.
+constexpr int64_t WEIGHT_MAX_COLS = 8192;
+constexpr int64_t WEIGHT_MAX_T = 2048;
+hipError_t launch_weighted_sample(const RngArgs& r, int64_t rows, int64_t cols, uint32_t* out, int64_t ldo,
+                                  int8_t* dig, int64_t pitch, hipStream_t s);
+hipError_t launch_weighted_csr_count(int64_t rows, int64_t t, int64_t* row_ptr, hipStream_t s);
+hipError_t launch_weighted_csr_fill(const RngArgs& r, int64_t rows, int64_t cols, const int64_t* row_ptr,
+                                    int32_t* col_idx, uint32_t* values, hipStream_t s);
+
 hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb, int64_t rows,
                                    int64_t cols, int64_t* count, hipStream_t s);
 

@@ -7,11 +7,107 @@
 // The matrices are the SPARSE streams of mosaic.h: element (i, j) of a
 // rows x cols matrix is e = i cols + j, nonzero iff the top s bits of word 2e
 // are zero, and then equal to word 2e + 1. Compressed rows list the nonzeros
-// of each row in increasing column order.
+// of each row in increasing column order. Or they are WEIGHT streams (the
+// fixed Hamming weight t of Example 4.1): row i holds t entries chosen by a
+// partial Fisher-Yates shuffle driven by words 2ti .. 2ti+2t-1, listed in
+// the order of the shuffle's steps.
 #include "internal.h"
 
 namespace mosaic {
 namespace {
+
+// Entries of row ``row`` of a WEIGHT stream matrix, computed by one wave
+// (the calling workgroup's first 64 threads; every thread of the workgroup
+// must call it, the others only wait). perm: LDS scratch of ``cols``
+// uint16, u: LDS scratch of t words; pos / val (LDS, t entries) receive the
+// chosen column and the value of each step. The permutation is stored as
+// perm[k] ^ k so that zero-filled memory is the identity. Ends with a
+// workgroup barrier, after which pos and val are visible to all threads.
+__device__ void weighted_row(const RngArgs& r, int64_t row, int cols, uint16_t* perm, uint32_t* u, int32_t* pos,
+                             uint32_t* val) {
+  const int t = r.row_weight;
+  const int tid = threadIdx.x;
+  if (tid < 64) {
+    for (int k = tid; k < cols; k += 64) perm[k] = 0;
+    const uint64_t w0 = 2 * (uint64_t)t * (uint64_t)row;   // even: each (u, value) pair is one half block
+    for (int j = tid; j < t; j += 64) {
+      const uint64_t w = w0 + 2 * (uint64_t)j;
+      const uint4 blk = philox_block(r, w >> 2);
+      const bool hi = ((w >> 1) & 1) != 0;
+      u[j] = hi ? blk.z : blk.x;
+      val[j] = hi ? blk.w : blk.y;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int j = 0; j < t; ++j) {
+      const uint32_t k = (uint32_t)j + (uint32_t)(((uint64_t)u[j] * (uint64_t)(uint32_t)(cols - j)) >> 32);
+      const uint32_t a = perm[j] ^ (uint32_t)j;     // entries j and k of the running permutation
+      const uint32_t b = perm[k] ^ k;
+      perm[j] = (uint16_t)(b ^ (uint32_t)j);
+      perm[k] = (uint16_t)(a ^ k);
+      pos[j] = (int32_t)b;
+    }
+  }
+  __syncthreads();
+}
+
+// Dynamic LDS of the WEIGHT kernels: u (t words), pos (t), val (t), then
+// perm (cols uint16).
+inline size_t weighted_lds_bytes(int64_t cols, int64_t t) { return (size_t)(12 * t + 2 * cols + 16); }
+
+// One 64-thread workgroup per row: the row of a WEIGHT matrix as ring words
+// and/or digits (zeros, then the t entries).
+__global__ __launch_bounds__(64) void weighted_sample_kernel(RngArgs r, int64_t cols, uint32_t* out, int64_t ldo,
+                                                             int8_t* dig, int64_t pitch) {
+  extern __shared__ uint32_t wlds[];
+  const int t = r.row_weight;
+  uint32_t* u = wlds;
+  int32_t* pos = (int32_t*)(wlds + t);
+  uint32_t* val = wlds + 2 * t;
+  uint16_t* perm = (uint16_t*)(wlds + 3 * t);
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  if (out != nullptr)
+    for (int64_t k = tid; k < cols; k += 64) out[row * ldo + k] = 0u;
+  if (dig != nullptr) {
+    const int64_t bytes = 4 * (64 * ((cols + 63) / 64));   // the padded row, zero digits
+    for (int64_t k = 16 * tid; k < bytes; k += 16 * 64) *(uint4*)(dig + row * pitch + k) = make_uint4(0, 0, 0, 0);
+  }
+  weighted_row(r, row, (int)cols, perm, u, pos, val);   // its barriers also order the zero stores first
+  for (int j = tid; j < t; j += 64) {
+    const int64_t c = pos[j];
+    const uint32_t v = val[j];
+    if (out != nullptr) out[row * ldo + c] = v;
+    if (dig != nullptr) {
+      const uint32_t w = digit_word(v);
+      int8_t* g = dig + row * pitch + 64 * (c >> 4) + (c & 15);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) g[16 * q] = (int8_t)(w >> (8 * q));
+    }
+  }
+}
+
+// row_ptr[i] = i t for a WEIGHT matrix (rows + 1 entries).
+__global__ __launch_bounds__(256) void weighted_count_kernel(int64_t rows, int64_t t, int64_t* row_ptr) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i <= rows) row_ptr[i] = i * t;
+}
+
+// One 64-thread workgroup per row: the row's t entries into its compressed
+// row (at row_ptr[row]).
+__global__ __launch_bounds__(64) void weighted_fill_kernel(RngArgs r, int64_t cols, const int64_t* row_ptr,
+                                                           int32_t* col_idx, uint32_t* values) {
+  extern __shared__ uint32_t wlds[];
+  const int t = r.row_weight;
+  const int64_t row = blockIdx.x;
+  weighted_row(r, row, (int)cols, (uint16_t*)(wlds + 3 * t), wlds, (int32_t*)(wlds + t), wlds + 2 * t);
+  const int64_t base = row_ptr[row];
+  for (int j = threadIdx.x; j < t; j += 64) {
+    col_idx[base + j] = (int32_t)wlds[t + j];
+    values[base + j] = wlds[2 * t + j];
+  }
+}
 
 // gate and value of element e (words 2e and 2e + 1 share a Philox block)
 __device__ __forceinline__ bool sparse_elem(const RngArgs& r, uint64_t e, uint32_t* val) {
@@ -86,11 +182,13 @@ __global__ __launch_bounds__(256) void sparse_fill_kernel(RngArgs r, int64_t row
 
 // c[i][k] +-= sum_j P(i, j) d[j][k] for k < ncols. A workgroup owns 256
 // consecutive k of one row i. The row's nonzeros are staged in LDS in chunks
-// of CH entries -- copied from compressed rows (STREAM = 0) or drawn from the
+// of CH entries -- copied from compressed rows (STREAM = 0), drawn from the
 // SPARSE stream of rng over the row's rcols columns (STREAM = 1: each wave
 // appends its nonzeros through an LDS counter; the ring sum does not depend
-// on their order) -- and every thread then runs over the staged entries,
-// which are LDS broadcasts, with several independent loads of d in flight.
+// on their order) or drawn as the t entries of a WEIGHT row (STREAM = 2, one
+// chunk: t <= CH; the shuffle's scratch is dynamic LDS) -- and every thread
+// then runs over the staged entries, which are LDS broadcasts, with several
+// independent loads of d in flight.
 template <int STREAM>
 __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rcols, const int64_t* row_ptr,
                                                           const int32_t* col_idx, const uint32_t* values,
@@ -106,12 +204,16 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rco
   const bool active = k < ncols;
   const uint32_t* dk = d + (active ? k : 0);
   const int64_t lo = STREAM ? 0 : row_ptr[i];
-  const int64_t hi = STREAM ? rcols : row_ptr[i + 1];
+  const int64_t hi = STREAM == 2 ? r.row_weight : STREAM ? rcols : row_ptr[i + 1];
   uint32_t acc = 0;
   for (int64_t base = lo; base < hi; base += CH) {
     const int64_t end = (base + CH < hi) ? base + CH : hi;
     int n;
-    if (STREAM) {
+    if (STREAM == 2) {
+      extern __shared__ uint32_t wlds[];
+      weighted_row(r, i, (int)rcols, (uint16_t*)wlds + 0, wlds + ((rcols + 1) >> 1), scol, sval);
+      n = r.row_weight;
+    } else if (STREAM == 1) {
       if (tid == 0) scount = 0;
       __syncthreads();
       for (int64_t j0 = base; j0 < end; j0 += 256) {
@@ -213,9 +315,39 @@ hipError_t launch_sparse_stream_gather_rows(const RngArgs& r, int64_t rows, int6
                                             int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc, int subtract,
                                             hipStream_t s) {
   if (rows == 0 || ncols == 0 || rcols == 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_rows_kernel<1>, dim3((unsigned)rows, (unsigned)((ncols + 255) / 256)), dim3(256), 0, s,
-                     r, rcols, (const int64_t*)nullptr, (const int32_t*)nullptr, (const uint32_t*)nullptr, d, ldd,
-                     ncols, c, ldc, subtract);
+  const dim3 grid((unsigned)rows, (unsigned)((ncols + 255) / 256));
+  if (r.dist == 4) {
+    if (r.row_weight == 0) return hipSuccess;
+    // perm (rcols uint16, rounded up to words), then u (t words)
+    const size_t lds = (size_t)(4 * ((rcols + 1) / 2) + 4 * r.row_weight);
+    hipLaunchKernelGGL(gather_rows_kernel<2>, grid, dim3(256), lds, s, r, rcols, (const int64_t*)nullptr,
+                       (const int32_t*)nullptr, (const uint32_t*)nullptr, d, ldd, ncols, c, ldc, subtract);
+  } else {
+    hipLaunchKernelGGL(gather_rows_kernel<1>, grid, dim3(256), 0, s, r, rcols, (const int64_t*)nullptr,
+                       (const int32_t*)nullptr, (const uint32_t*)nullptr, d, ldd, ncols, c, ldc, subtract);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_weighted_sample(const RngArgs& r, int64_t rows, int64_t cols, uint32_t* out, int64_t ldo,
+                                  int8_t* dig, int64_t pitch, hipStream_t s) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  hipLaunchKernelGGL(weighted_sample_kernel, dim3((unsigned)rows), dim3(64), weighted_lds_bytes(cols, r.row_weight), s,
+                     r, cols, out, ldo, dig, pitch);
+  return hipGetLastError();
+}
+
+hipError_t launch_weighted_csr_count(int64_t rows, int64_t t, int64_t* row_ptr, hipStream_t s) {
+  hipLaunchKernelGGL(weighted_count_kernel, dim3((unsigned)((rows + 1 + 255) / 256)), dim3(256), 0, s, rows, t,
+                     row_ptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_weighted_csr_fill(const RngArgs& r, int64_t rows, int64_t cols, const int64_t* row_ptr,
+                                    int32_t* col_idx, uint32_t* values, hipStream_t s) {
+  if (rows == 0 || cols == 0 || r.row_weight == 0) return hipSuccess;
+  hipLaunchKernelGGL(weighted_fill_kernel, dim3((unsigned)rows), dim3(64), weighted_lds_bytes(cols, r.row_weight), s,
+                     r, cols, row_ptr, col_idx, values);
   return hipGetLastError();
 }
 

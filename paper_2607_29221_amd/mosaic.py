@@ -19,7 +19,7 @@ import torch
 
 from . import _lib
 
-DIST_ZERO, DIST_UNIFORM, DIST_DGAUSS, DIST_SPARSE = 0, 1, 2, 3
+DIST_ZERO, DIST_UNIFORM, DIST_DGAUSS, DIST_SPARSE, DIST_WEIGHT = 0, 1, 2, 3, 4
 DT_I8, DT_I16, DT_I32, DT_U32 = 0, 1, 2, 3
 STATUS_OK, STATUS_INVALID_ARG, STATUS_UNSUPPORTED, STATUS_HIP = 0, -1, -2, -3
 _TORCH_DT = {torch.int8: DT_I8, torch.int16: DT_I16, torch.int32: DT_I32}
@@ -89,10 +89,10 @@ class Digits:
 
 
 def rng(seed: int, stream: int, instance: int, dist: int, sigma: float = 0.5, bound: int = 4,
-        log2_inv_density: int = 6, transposed: bool = False) -> _lib.MosaicRng:
+        log2_inv_density: int = 6, transposed: bool = False, row_weight: int = 0) -> _lib.MosaicRng:
     return _lib.MosaicRng(seed=seed & 0xFFFFFFFFFFFFFFFF, stream=stream, instance=instance, dist=dist,
                           bound=bound, sigma=sigma, log2_inv_density=log2_inv_density,
-                          transposed=1 if transposed else 0)
+                          transposed=1 if transposed else 0, row_weight=row_weight)
 
 
 def mosaic_abi_version() -> int:
@@ -174,13 +174,17 @@ class SparseRows:
 
 
 def mosaic_sparse_csr(r: _lib.MosaicRng, rows: int, cols: int, exact: bool = True, device="cuda") -> SparseRows:
-    """Compressed rows of the SPARSE stream matrix of ``r``. With ``exact``
-    the arrays are sized to the nonzero count (one device-to-host read);
-    otherwise to the bound rows * cols (no synchronisation)."""
+    """Compressed rows of the SPARSE or WEIGHT stream matrix of ``r``. With
+    ``exact`` the arrays are sized to the nonzero count (one device-to-host
+    read for SPARSE; rows * t for WEIGHT); otherwise to the bound rows * cols
+    (no synchronisation)."""
     row_ptr = torch.empty(rows + 1, dtype=torch.int64, device=device)
     _check(_lib.load().mosaic_sparse_csr_count(ctypes.byref(r), rows, cols, row_ptr.data_ptr(), _stream()),
            "mosaic_sparse_csr_count")
-    cap = int(row_ptr[rows].item()) if exact else rows * cols
+    if r.dist == DIST_WEIGHT:
+        cap = rows * r.row_weight
+    else:
+        cap = int(row_ptr[rows].item()) if exact else rows * cols
     col_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
     values = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
     _check(_lib.load().mosaic_sparse_csr_fill(ctypes.byref(r), rows, cols, row_ptr.data_ptr(), col_idx.data_ptr(),

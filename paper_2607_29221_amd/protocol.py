@@ -54,6 +54,23 @@ def _noise_rng(params, seed: int, stream: int, instance: int):
     return m.rng(seed, stream, instance, m.DIST_DGAUSS, sigma=nz.sigma, bound=nz.bound)
 
 
+def _lpn_rng(params, level: int, seed: int, stream: int, instance: int):
+    """Stream of the sparse LPN matrix of ``level`` (S_level, or T_level^T):
+    fixed row weight t_level when the parameters give one (Example 4.1),
+    else noise rate 2^-s."""
+    weights = tuple(getattr(params, "lpn_weights", ()) or ())
+    if weights:
+        return m.rng(seed, stream, instance, m.DIST_WEIGHT, row_weight=int(weights[level - 2]))
+    return m.rng(seed, stream, instance, m.DIST_SPARSE, log2_inv_density=params.sparse_log2_inv_density)
+
+
+# Token counts up to which a call with both LPN forms available uses the
+# sparse gathers: their bytes grow with the token count and reach those of
+# the dense slot products at about 64 tokens (measured: sparse 6-19% faster
+# at 1 and 8 tokens, 12-30% slower at 64).
+SPARSE_LPN_MAX_TOKENS = 16
+
+
 def _ring_empty(rows: int, cols: int, device) -> torch.Tensor:
     return torch.empty((rows, cols), dtype=torch.int32, device=device)
 
@@ -70,12 +87,14 @@ class MaskedWeight:
     digit layout by the client. One vector misses an error in the top bit
     with probability 1/2 over Z_{2^32}; t vectors bound that by 2^-t.
 
-    With ``sparse_lpn`` (the default at depth >= 2) the LPN matrices stay sparse on the
-    client: S_{i+1} is kept in compressed rows and multiplied by gathering
-    (U_w at Init W, S_{i+1} Q_i at unmasking), T_{i+1} is compressed per
-    call and gathered into U_a and K_c, so their cost per output follows the
-    nonzero count instead of r_i. The dense products then run over the
-    level-d slot only. Results are identical to the dense path."""
+    At depth >= 2 the LPN matrices can also stay sparse on the client:
+    S_{i+1} is kept in compressed rows and multiplied by gathering (S_{i+1}
+    Q_i at unmasking), T_{i+1} is drawn inside the gathers into U_a and K_c,
+    so their cost per output follows the nonzero count instead of r_i; the
+    dense products then run over the level-d slot only. ``sparse_lpn`` None
+    (the default) keeps both forms and picks per call from the token count
+    (sparse up to SPARSE_LPN_MAX_TOKENS), True keeps only the sparse form,
+    False only the dense one. Results are identical either way."""
 
     def __init__(self, W: torch.Tensor, params, seed: int, weight_id: int = 0, check_vectors: int = 0,
                  sparse_lpn: Optional[bool] = None):
@@ -88,8 +107,11 @@ class MaskedWeight:
         self.slot_levels = [d] + list(range(1, d))            # level of each slot
         self.slot_ranks = [r[lv - 1] for lv in self.slot_levels]
         self.R = sum(padded_k(c) for c in self.slot_ranks)    # padded inner width
-        self.sparse = (True if sparse_lpn is None else bool(sparse_lpn)) and d >= 2
-        self.Rd = padded_k(r[d - 1]) if self.sparse else self.R   # width of the dense products
+        self.sparse_mode = sparse_lpn
+        self.keep_sparse = d >= 2 and sparse_lpn is not False  # compressed S, D_i
+        self.keep_dense = not (d >= 2 and sparse_lpn is True)  # every slot in Lcat / Bx
+        self.sparse = self.keep_sparse and not self.keep_dense  # sparse-only weight
+        self.Rd = padded_k(r[d - 1])                          # width of the sparse calls' products
         U = m.DIST_UNIFORM
         s = seed
 
@@ -123,23 +145,25 @@ class MaskedWeight:
         # for the levels i < d that meet a sparse matrix
         self.D: dict = {}
         Mc32: dict = {}
-        if self.sparse:
+        if self.keep_sparse:
             for i in range(1, d):
                 self.D[i] = _ring_empty(r[i - 1], K + N, dev)
-                Mc32[i] = _ring_empty(r[i - 1], K, dev)
+                if not self.keep_dense:                       # U_w then needs S_{i+1} Mc_i by gathering
+                    Mc32[i] = _ring_empty(r[i - 1], K, dev)
 
         NcT: List[Digits] = []                # (N_1 ... N_i)^T (r_i x K)
         for i in range(1, d + 1):
             ri = r[i - 1]
             nct = Digits.empty(ri, K, dev)
-            keep = i in self.D
+            keep = i in Mc32
+            keep_d = i in self.D
             if i == 1:
                 m.mosaic_sample(m.rng(s, STREAM_M + 1, weight_id, U), ri, K, out_dig=mc_dst(1),
                                 out=Mc32[1] if keep else None)
                 m.mosaic_sample(m.rng(s, STREAM_M + 1, weight_id, U, transposed=True), K, ri, out_dig=mct_dst(1))
                 m.mosaic_sample(m.rng(s, STREAM_N + 1, weight_id, U), K, ri, out_dig=nc_dst(1))
                 m.mosaic_sample(m.rng(s, STREAM_N + 1, weight_id, U, transposed=True), ri, K, out_dig=nct,
-                                out=self.D[1][:, :K] if keep else None)
+                                out=self.D[1][:, :K] if keep_d else None)
             else:
                 rp = r[i - 2]
                 Mi = Digits.empty(ri, rp, dev)                  # M_i (r_i x r_{i-1})
@@ -151,20 +175,19 @@ class MaskedWeight:
                 self._product_to_digits(mct_dst(i - 1), Mi, K, ri, rp, mct_dst(i))   # McT_{i-1} M_i^T
                 self._product_to_digits(nc_dst(i - 1), NiT, K, ri, rp, nc_dst(i))    # Nc_{i-1} N_i
                 self._product_to_digits(NiT, nc_dst(i - 1), ri, K, rp, nct,
-                                        self.D[i][:, :K] if keep else None)            # N_i^T Nc_{i-1}^T
+                                        self.D[i][:, :K] if keep_d else None)          # N_i^T Nc_{i-1}^T
             NcT.append(nct)
 
-        # client: Lcat = [L | S_2 | ... | S_d] (sparse mode: L only, S_{i+1} as
-        # compressed rows)
-        self.Lcat = Digits.concat(N, self.slot_ranks[:1] if self.sparse else self.slot_ranks, dev)
+        # client: Lcat = [L | S_2 | ... | S_d] (sparse-only: L alone), and
+        # S_{i+1} as compressed rows when the sparse form is kept
+        self.Lcat = Digits.concat(N, self.slot_ranks if self.keep_dense else self.slot_ranks[:1], dev)
         m.mosaic_sample(m.rng(s, STREAM_L, weight_id, U), N, r[d - 1], out_dig=self.Lcat[0])
         self.S: dict = {}
         for slot, lv in enumerate(self.slot_levels[1:], start=1):
-            srng = m.rng(s, STREAM_S + lv + 1, weight_id, m.DIST_SPARSE,
-                         log2_inv_density=params.sparse_log2_inv_density)
-            if self.sparse:
+            srng = _lpn_rng(params, lv + 1, s, STREAM_S + lv + 1, weight_id)
+            if self.keep_sparse:
                 self.S[lv] = m.mosaic_sparse_csr(srng, N, r[lv - 1], exact=True, device=dev)
-            else:
+            if self.keep_dense:
                 m.mosaic_sample(srng, N, r[lv - 1], out_dig=self.Lcat[slot])
 
         # integrity check vectors (slots of a_Q in the order of Q's columns)
@@ -181,9 +204,12 @@ class MaskedWeight:
 
         # U_w = Lcat McTcat^T (= L Mc_d + sum S_{i+1} Mc_i); W' = W + U_w + E_w
         U_w = _ring_empty(N, K, dev)
-        m.mosaic_masked_matmul(self.Lcat[0].whole(self.Rd), McTcat[0].whole(self.Rd), N, K, self.Rd, U_w)
-        for lv, S in self.S.items():
-            m.mosaic_sparse_gather_rows(S, Mc32[lv], K, U_w)
+        if self.keep_dense:
+            m.mosaic_masked_matmul(self.Lcat[0].whole(self.R), McTcat[0].whole(self.R), N, K, self.R, U_w)
+        else:
+            m.mosaic_masked_matmul(self.Lcat[0].whole(self.Rd), McTcat[0].whole(self.Rd), N, K, self.Rd, U_w)
+            for lv, S in self.S.items():
+                m.mosaic_sparse_gather_rows(S, Mc32[lv], K, U_w)
         del McTcat, Mc32
         ew = _noise_rng(params, s, STREAM_EW, weight_id)
         Wm = _ring_empty(N, K, dev) if self.t > 0 else None
@@ -212,7 +238,15 @@ class MaskedWeight:
             if lv in self.D:                                  # J_i^T next to (N_1..N_i)^T
                 m.mosaic_masked_matmul(NcT[lv - 1], WE, ri, N, K, self.D[lv][:, K:])
         del WE, NcT
-        self.Bx_dense = Digits(bx, r[d - 1]) if self.sparse else self.Bx
+        self.Bx_dense = Digits(bx, r[d - 1])     # the level-d slot (sparse calls)
+
+    def sparse_call(self, M: int) -> bool:
+        """Whether a call with M tokens uses the sparse LPN form."""
+        if not self.keep_sparse:
+            return False
+        if not self.keep_dense:
+            return True
+        return M <= SPARSE_LPN_MAX_TOKENS
 
     @staticmethod
     def _product_to_digits(a: Digits, b: Digits, rows: int, cols: int, inner: int, out: Digits,
@@ -250,11 +284,9 @@ def init_x(w: MaskedWeight, M: int, call_id: int, buf: CallBuffers) -> None:
     product (E_x is drawn later, inside the mask pass)."""
     p, s, r = w.params, w.seed, list(w.params.ranks)
     m.mosaic_sample(m.rng(s, STREAM_R, call_id, m.DIST_UNIFORM), M, r[w.d - 1], out_dig=buf.rho[0])
-    if not w.sparse:
+    if not w.sparse_call(M):
         for slot, lv in enumerate(w.slot_levels[1:], start=1):
-            m.mosaic_sample(m.rng(s, STREAM_T + lv + 1, call_id, m.DIST_SPARSE,
-                                  log2_inv_density=p.sparse_log2_inv_density),
-                            M, r[lv - 1], out_dig=buf.rho[slot])
+            m.mosaic_sample(_lpn_rng(p, lv + 1, s, STREAM_T + lv + 1, call_id), M, r[lv - 1], out_dig=buf.rho[slot])
         m.mosaic_masked_matmul(buf.rho[0].whole(w.R), w.Bx, M, w.K + w.N, w.R, buf.UK)
         return
     # sparse mode: the level-d slot as a product, then each T_{i+1}^T (M x r_i,
@@ -262,8 +294,7 @@ def init_x(w: MaskedWeight, M: int, call_id: int, buf: CallBuffers) -> None:
     # D_i = [(N_1..N_i)^T | J_i^T]
     m.mosaic_masked_matmul(buf.rho[0].whole(w.Rd), w.Bx_dense.whole(w.Rd), M, w.K + w.N, w.Rd, buf.UK)
     for lv, D in w.D.items():
-        m.mosaic_sparse_stream_gather_rows(m.rng(s, STREAM_T + lv + 1, call_id, m.DIST_SPARSE,
-                                                 log2_inv_density=p.sparse_log2_inv_density),
+        m.mosaic_sparse_stream_gather_rows(_lpn_rng(p, lv + 1, s, STREAM_T + lv + 1, call_id),
                                            M, r[lv - 1], D, w.K + w.N, buf.UK)
 
 
@@ -285,11 +316,12 @@ def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tens
     mode the product covers the level-d slot (L Q_d) and each S_{i+1} Q_i is
     subtracted by gathering from Q_i's ring words."""
     r = list(w.params.ranks)
-    slots = w.slot_levels[:1] if w.sparse else w.slot_levels
+    sparse = w.sparse_call(M)
+    slots = w.slot_levels[:1] if sparse else w.slot_levels
     for slot, lv in enumerate(slots):
         c0 = w.q_cols[slot]
         m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
-    if not w.sparse:
+    if not sparse:
         m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
                         M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
         return

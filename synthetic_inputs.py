@@ -74,6 +74,9 @@ PARAMS_PAPER_D3_T80 = ProtocolParams(ranks=(1536, 1024, 652), noise=NoiseSpec("d
 # Depth 2 with the paper's first two levels (r_2 = 1024, t_2 = 80) and sigma = 0.5.
 PARAMS_PAPER_D2_T80 = ProtocolParams(ranks=(1536, 1024), noise=NoiseSpec("dgauss", 0.5, 4),
                                      lpn_weights=(80,))
+# Decode workload rerun with the paper's small LWE error (sigma = 0.5) on
+# top of the depth-2 sparse masks (density 2^-6).
+PARAMS_DECODE_D2_NOISY = ProtocolParams(ranks=(1536, 1024), noise=NoiseSpec("dgauss", 0.5, 4))
 # Small fixed-weight instance for parity at the single-matmul size.
 PARAMS_D3_WEIGHT_SMALL = ProtocolParams(ranks=(192, 128, 64), noise=NoiseSpec("dgauss", 0.5, 4),
                                         lpn_weights=(12, 9))

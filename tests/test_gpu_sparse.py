@@ -173,3 +173,129 @@ def test_sparse_mode_dequantised_output():
         outs.append((buf.Y.cpu().numpy(), yf.cpu().numpy()))
     assert np.array_equal(outs[0][0], outs[1][0])
     assert np.array_equal(outs[0][1], outs[1][1])
+
+
+# --- fixed row weight (Example 4.1: t nonzeros per row) ---
+
+@pytest.mark.parametrize("rows,cols,t", [(5, 1536, 80), (64, 1024, 80), (33, 70, 70), (4, 8192, 2048),
+                                         (3, 5, 0), (1, 1, 1), (130, 652, 80)])
+def test_weighted_sample_matches_oracle(rows, cols, t):
+    """mosaic_sample with a WEIGHT stream: ring words and digits equal the
+    oracle's partial-shuffle matrix (zeros elsewhere, padding digits zero)."""
+    seed, stream, inst = 77, 0x44, 5
+    r = m.rng(seed, stream, inst, m.DIST_WEIGHT, row_weight=t)
+    out = torch.full((rows, cols + 3), -1, dtype=torch.int32, device="cuda")
+    dig = m.Digits(torch.full((rows, 4 * m.padded_k(cols)), 7, dtype=torch.int8, device="cuda"), cols)
+    m.mosaic_sample(r, rows, cols, out=out[:, :cols], out_dig=dig)
+    torch.cuda.synchronize()
+    ref = smp.sample_matrix("weight", rows, cols, seed, stream, inst, row_weight=t)
+    got = to_np_u32(out)
+    assert np.array_equal(got[:, :cols], ref)
+    assert np.all(got[:, cols:] == 0xFFFFFFFF)
+    from tests.gpu_util import pad_is_zero, unpack_digits
+    assert np.array_equal(unpack_digits(dig), ref)
+    assert pad_is_zero(dig)
+
+
+@pytest.mark.parametrize("rows,cols,t", [(300, 1536, 80), (17, 1024, 80), (9, 40, 40), (2, 8192, 2048)])
+def test_weighted_csr_matches_oracle(rows, cols, t):
+    """Compressed rows of a WEIGHT stream: row_ptr = i t, and each row lists
+    the oracle's columns and values in the order of the shuffle's steps."""
+    seed, stream, inst = 8, 0x45, 1
+    p = m.mosaic_sparse_csr(m.rng(seed, stream, inst, m.DIST_WEIGHT, row_weight=t), rows, cols)
+    torch.cuda.synchronize()
+    pos, val = smp.weighted_rows(range(rows), cols, t, seed, stream, inst)
+    assert np.array_equal(p.row_ptr.cpu().numpy(), np.arange(rows + 1) * t)
+    assert np.array_equal(p.col_idx.cpu().numpy()[: rows * t].reshape(rows, t), pos)
+    assert np.array_equal(p.values.cpu().numpy().view(np.uint32)[: rows * t].reshape(rows, t), val)
+
+
+@pytest.mark.parametrize("rows,r,ncols,t", [(9, 1536, 517, 80), (64, 1024, 8192, 80), (3, 300, 70, 300),
+                                            (1, 1, 1, 1), (5, 2048, 300, 2048)])
+@pytest.mark.parametrize("subtract", [False, True])
+def test_weighted_stream_gather(rows, r, ncols, t, subtract):
+    """T_{i+1} terms with WEIGHT rows drawn inside the gather, and the same
+    through compressed rows, equal ring products with the oracle's matrix."""
+    rng = np.random.default_rng(rows + r + t)
+    seed, stream, inst = 13, 0x63, 9
+    P = smp.sample_matrix("weight", rows, r, seed, stream, inst, row_weight=t)
+    D = rng.integers(0, 2 ** 32, (r, ncols), dtype=np.uint32)
+    C0 = rng.integers(0, 2 ** 32, (rows, ncols), dtype=np.uint32)
+    prod = ring_matmul(P, D)
+    want = ring_sub(C0, prod) if subtract else ring_add(C0, prod)
+    rr = m.rng(seed, stream, inst, m.DIST_WEIGHT, row_weight=t)
+    c = to_dev_ring(C0)
+    m.mosaic_sparse_stream_gather_rows(rr, rows, r, to_dev_ring(D), ncols, c, subtract=subtract)
+    c2 = to_dev_ring(C0)
+    m.mosaic_sparse_gather_rows(m.mosaic_sparse_csr(rr, rows, r), to_dev_ring(D), ncols, c2, subtract=subtract)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_u32(c), want)
+    assert np.array_equal(to_np_u32(c2), want)
+
+
+def test_weighted_rejected_where_unsupported():
+    r = m.rng(1, 2, 3, m.DIST_WEIGHT, row_weight=5)
+    out = torch.empty((4, 4), dtype=torch.int32, device="cuda")
+    with pytest.raises(m.MosaicError):                           # t > cols
+        m.mosaic_sample(r, 4, 4, out=out)
+    with pytest.raises(m.MosaicError):                           # not drawn inside the mask pass
+        m.mosaic_mask(None, out, r, 4, 4, out=out)
+    rt = m.rng(1, 2, 3, m.DIST_WEIGHT, row_weight=1, transposed=True)
+    with pytest.raises(m.MosaicError):
+        m.mosaic_sample(rt, 4, 4, out=out)
+
+
+@pytest.mark.parametrize("mode", [False, True, None], ids=["dense", "sparse", "auto"])
+@pytest.mark.parametrize("shape", [(64, 512, 512), (70, 130, 200), (5, 256, 96)], ids=["small", "ragged", "few"])
+def test_weighted_protocol_modes(mode, shape):
+    """Depth 3 with fixed row weights, every LPN form: U_a, K_c, Y', Y equal
+    the oracle bit for bit."""
+    from synthetic_inputs import PARAMS_D3_WEIGHT_SMALL
+    M, K, N = shape
+    A, W = int8_operands(M, K, N, 4)
+    seed = 4242
+    ref = oproto.run(A, W, PARAMS_D3_WEIGHT_SMALL, seed, weight_id=2, call_id=3)
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), PARAMS_D3_WEIGHT_SMALL, seed, 2, sparse_lpn=mode)
+    buf = gproto.run_call(w, torch.from_numpy(A).cuda(), 3)
+    torch.cuda.synchronize()
+    UK, YQ = to_np_u32(buf.UK), to_np_u32(buf.YQ)
+    cs = ref.cs
+    assert np.array_equal(UK[:, :K], ring_sub(cs.U_x, cs.E_x).T)
+    assert np.array_equal(UK[:, K:], cs.K.T)
+    assert np.array_equal(YQ[:, :N], ref.Y_masked.T)
+    assert np.array_equal(buf.Y.cpu().numpy(), lift(ref.Y).T)
+
+
+def _noisy_identity(A, W, params, seed, weight_id, call_id):
+    """(A + E_a)(W + E_w)^T over Z_{2^32}, E drawn by the oracle's sampler;
+    exact in float64 (entries below 2^53)."""
+    nz = params.noise
+    M, K = A.shape
+    N = W.shape[0]
+    Ea = smp.sample_matrix("dgauss", M, K, seed, smp.STREAM_EX, call_id, sigma=nz.sigma, bound=nz.bound)
+    Ew = smp.sample_matrix("dgauss", N, K, seed, smp.STREAM_EW, weight_id, sigma=nz.sigma, bound=nz.bound)
+    a = A.astype(np.float64) + lift(Ea).astype(np.float64)
+    b = W.astype(np.float64) + lift(Ew).astype(np.float64)
+    y = a @ b.T
+    return (y.astype(np.int64) & 0xFFFFFFFF).astype(np.uint32)
+
+
+@pytest.mark.parametrize("shape_id", range(len(DECODE_KN)), ids=[f"{k}x{n}" for k, n in DECODE_KN])
+@pytest.mark.parametrize("which", ["d2-noisy", "paper-d3-t80"])
+def test_decode_noisy_exact(shape_id, which):
+    """Decode shapes with the paper's LWE error sigma = 0.5: depth 2 (1536,
+    1024) at density 2^-6, and Example 4.1 in full (1536, 1024, 652 with
+    t = 80). Every output of Y equals (A + E_a)(W + E_w)^T mod 2^32 for
+    1, 8 and 64 tokens (sparse calls below 17 tokens, dense above)."""
+    from synthetic_inputs import PARAMS_DECODE_D2_NOISY, PARAMS_PAPER_D3_T80
+    params = PARAMS_DECODE_D2_NOISY if which == "d2-noisy" else PARAMS_PAPER_D3_T80
+    K, N = DECODE_KN[shape_id]
+    A, W = int8_operands(max(DECODE_M), K, N, DECODE_SEED)
+    seed = 0xDEC0DE50 + shape_id
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), params, seed, shape_id)
+    for Mi in DECODE_M:
+        Ai = np.ascontiguousarray(A[:Mi])
+        buf = gproto.run_call(w, torch.from_numpy(Ai).cuda(), call_id=100 + Mi)
+        torch.cuda.synchronize()
+        want = _noisy_identity(Ai, W, params, seed, shape_id, 100 + Mi)
+        assert np.array_equal(to_np_u32(buf.Y), want), (which, K, N, Mi)
