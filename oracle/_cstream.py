@@ -16,7 +16,7 @@ _lib = None
 
 def build() -> str:
     tmp = _LIB + f".tmp{os.getpid()}"
-    subprocess.run(["gcc", "-O2", "-shared", "-fPIC", "-o", tmp, _SRC], check=True)
+    subprocess.run(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", tmp, _SRC], check=True)
     os.replace(tmp, _LIB)
     return _LIB
 

@@ -27,19 +27,26 @@ static void philox_block(uint64_t b, uint32_t stream, uint32_t instance, uint32_
   out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
 }
 
-/* words t0 .. t0 + count - 1 of stream (seed, stream, instance) */
+/* words t0 .. t0 + count - 1 of stream (seed, stream, instance); ranges of
+ * words are independent, so OpenMP threads take consecutive slices */
 void oracle_stream_words(uint64_t seed, uint32_t stream, uint32_t instance, uint64_t t0, uint64_t count,
                          uint32_t* out) {
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  uint32_t blk[4];
-  uint64_t have = ~(uint64_t)0;
-  for (uint64_t i = 0; i < count; ++i) {
-    const uint64_t t = t0 + i;
-    const uint64_t b = t >> 2;
-    if (b != have) {
-      philox_block(b, stream, instance, k0, k1, blk);
-      have = b;
+  const int64_t slices = (int64_t)((count + 65535) >> 16);
+#pragma omp parallel for schedule(static)
+  for (int64_t sl = 0; sl < slices; ++sl) {
+    const uint64_t i0 = (uint64_t)sl << 16;
+    const uint64_t i1 = (i0 + 65536 < count) ? i0 + 65536 : count;
+    uint32_t blk[4];
+    uint64_t have = ~(uint64_t)0;
+    for (uint64_t i = i0; i < i1; ++i) {
+      const uint64_t t = t0 + i;
+      const uint64_t b = t >> 2;
+      if (b != have) {
+        philox_block(b, stream, instance, k0, k1, blk);
+        have = b;
+      }
+      out[i] = blk[t & 3];
     }
-    out[i] = blk[t & 3];
   }
 }

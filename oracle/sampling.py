@@ -120,11 +120,11 @@ def _elements(kind: str, e0: int, count: int, seed: int, stream: int, instance: 
     if kind == "uniform":
         return stream_words(seed, stream, instance, e0, count)
     if kind == "dgauss":
+        # -B + #{k : T_k <= word}: the count of thresholds at or below the
+        # word, which is its right insertion point in the ascending table
         u = stream_words(seed, stream, instance, e0, count).astype(np.uint64)
-        th = dgauss_thresholds(sigma, bound)
-        v = np.full(count, -bound, dtype=np.int64)
-        for t in th:
-            v += (u >= np.uint64(t)).astype(np.int64)
+        th = np.array(dgauss_thresholds(sigma, bound), dtype=np.uint64)
+        v = np.searchsorted(th, u, side="right").astype(np.int64) - bound
         return v.astype(np.int32).view(np.uint32)
     if kind == "sparse":
         w = stream_words(seed, stream, instance, 2 * e0, 2 * count)

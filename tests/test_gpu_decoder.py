@@ -22,6 +22,7 @@ from oracle.sampling import sample_signs
 from paper_2607_29221_amd import decoder as dec
 from paper_2607_29221_amd import protocol as gproto
 from paper_2607_29221_amd.secure_linear import SecureLinear, activation_window, rotation_block
+from tests.gpu_util import code_validity, noisy_identity
 from synthetic_inputs import (DECODER, DECODER_LINEARS, DECODER_RING_KN, DECODER_RING_SEED, DECODER_SEED,
                               PARAMS_D1_SMALL_R128, PARAMS_PAPER_D1, decoder_input, decoder_weight, int_codes)
 
@@ -71,25 +72,10 @@ def test_decoder_ring_products_sampled(shape_id):
     exact = (A[I].astype(np.int64) + ref["E_x"].view(np.int32)) @ \
             (W[J].astype(np.int64) + ref["E_w"].view(np.int32)).T
     assert np.array_equal(Y.view(np.int32).astype(np.int64), exact)
-
-
-def _code_validity(codes_gpu, scales_gpu, x64, signs, block, qmax, tol=0.02):
-    """Checks GPU codes of rows x64 (float64, unrotated) against the oracle's
-    float64 rotation and quantisation."""
-    xr = ohad.rotate(x64, signs, block)
-    amax = np.max(np.abs(xr), axis=1)
-    s64 = amax / qmax
-    assert np.all(np.abs(scales_gpu.astype(np.float64) - s64) <= 1e-5 * s64)
-    v = xr / s64[:, None]
-    ref = np.rint(v)
-    frac = np.abs(v - np.floor(v) - 0.5)
-    clear = frac > tol
-    got = codes_gpu.astype(np.int64)
-    assert np.array_equal(got[clear], ref[clear].astype(np.int64))
-    amb = ~clear
-    assert np.all((got[amb] == np.floor(v[amb])) | (got[amb] == np.ceil(v[amb])))
-    assert np.max(np.abs(got)) <= qmax
-    return float(np.mean(amb))
+    # every output equals that product (no wrap-around anywhere: the window)
+    print(f"decoder ring full-output check K={K} N={N}", flush=True)
+    want = noisy_identity(A, W, p, RING_SEED, shape_id, 7)
+    assert np.array_equal(buf.Y.cpu().numpy().view(np.uint32), want)
 
 
 def test_first_layer_codes_valid():
@@ -108,13 +94,13 @@ def test_first_layer_codes_valid():
     J = [0, 17, 5000, W.shape[0] - 1]
     Jt = torch.tensor(J, device=dev)
     wrows = W.index_select(0, Jt).cpu().numpy().astype(np.float64)
-    amb_w = _code_validity(lin.weight_codes.index_select(0, Jt).cpu().numpy(),
+    amb_w = code_validity(lin.weight_codes.index_select(0, Jt).cpu().numpy(),
                            lin.s_w.index_select(0, Jt).cpu().numpy(), wrows, signs, lin.block, 127)
     I = [0, 1, 1023, 4095]
     It = torch.tensor(I, device=dev)
     x64 = x.index_select(0, It).cpu().numpy().astype(np.float64)
     a64 = x64 / np.sqrt(np.mean(x64 ** 2, axis=1, keepdims=True) + 1e-5)     # RMSNorm, gain 1
-    amb_x = _code_validity(codes.index_select(0, It).cpu().numpy(), s_x.index_select(0, It).cpu().numpy(),
+    amb_x = code_validity(codes.index_select(0, It).cpu().numpy(), s_x.index_select(0, It).cpu().numpy(),
                            a64, signs, lin.block, lin.q_x)
     assert lin.q_x == 1997 and rotation_block(28672) == 4096
     assert amb_w < 0.1 and amb_x < 0.1

@@ -1,7 +1,8 @@
 """Parity at the full workload sizes, in the launch configuration bench.py
-times, on outputs the oracle can compute one by one (prefill), on every
-output where a closed form gives them (decode, no LWE error), and on sampled
-rows of the rotation."""
+times: every intermediate on outputs the oracle computes one by one, and
+every output of Y against (A + E_a)(W + E_w)^T (prefill, with the paper's
+small LWE error) or A W^T (decode, no LWE error); the rotation on sampled
+rows."""
 import numpy as np
 import pytest
 import torch
@@ -15,7 +16,7 @@ from paper_2607_29221_amd.mosaic import Digits
 from synthetic_inputs import (DECODE_KN, DECODE_M, DECODE_SEED, HADAMARD_SEED, HADAMARD_SHAPE,
                               PARAMS_PAPER_D1, PARAMS_PAPER_D2_SPARSE, PREFILL_KN, PREFILL_M, PREFILL_SEED,
                               int8_operands, outlier_activations)
-from tests.gpu_util import to_np_u32, unpack_digits
+from tests.gpu_util import noisy_identity, to_np_u32, unpack_digits
 
 pytestmark = pytest.mark.gpu
 
@@ -23,7 +24,7 @@ PREFILL_PROTOCOL_SEED = 0x6D6F736169630000 | PREFILL_SEED   # the seed bench.py 
 
 
 @pytest.mark.parametrize("shape_id", range(len(PREFILL_KN)), ids=[f"{k}x{n}" for k, n in PREFILL_KN])
-def test_prefill_sampled_outputs(shape_id):
+def test_prefill_outputs(shape_id):
     K, N = PREFILL_KN[shape_id]
     M = PREFILL_M
     p = PARAMS_PAPER_D1
@@ -58,6 +59,9 @@ def test_prefill_sampled_outputs(shape_id):
     assert np.array_equal(unpack_digits(a_rows), ref["A_masked"])
     w_rows = Digits(w.Bext.buf.index_select(0, Jt), K)
     assert np.array_equal(unpack_digits(w_rows), ref["W_masked"])
+    # every output: Y = (A + E_a)(W + E_w)^T mod 2^32
+    print(f"prefill full-output check K={K} N={N}", flush=True)
+    assert np.array_equal(to_np_u32(buf.Y), noisy_identity(A, W, p, PREFILL_PROTOCOL_SEED, shape_id, call_id))
     # the protocol error stays within the bound of Theorem 4.2 at these rows
     err = Y.astype(np.int64) - A[I].astype(np.int64) @ W[J].astype(np.int64).T
     scale = 0.5 * np.sqrt((A[I].astype(np.float64) ** 2).sum(1)[:, None]
@@ -96,7 +100,7 @@ def test_rotation_full_size():
     torch.cuda.synchronize()
     d = sample_signs(n, HADAMARD_SEED, 0)
     assert np.array_equal(signs.cpu().numpy(), d)
-    rows_s = np.arange(0, rows, 7)                     # 586 rows spread over the matrix
+    rows_s = np.arange(rows)                           # every row
     ref = ohad.rotate(x[rows_s].astype(np.float64), d)
     got = y.cpu().numpy()[rows_s].astype(np.float64)
     err = np.max(np.abs(got - ref), axis=1) / np.max(np.abs(ref), axis=1)

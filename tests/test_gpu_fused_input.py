@@ -1,7 +1,8 @@
-"""Fused rotate + quantise + mask of Pi_Sec-Linear's input against the
-three separate passes (rotation, quantisation, mask) through the C ABI:
-digits and scales are bit-identical, and shapes outside the fused kernel's
-limits are refused with MOSAIC_ERR_UNSUPPORTED."""
+"""Fused rotate + quantise + mask of Pi_Sec-Linear's input through the C ABI:
+against the oracle (codes recovered as A' - U - E and checked against the
+float64 rotation and quantisation), against the three separate passes
+(rotation, quantisation, mask: digits and scales bit-identical), and shapes
+outside the fused kernel's limits refused with MOSAIC_ERR_UNSUPPORTED."""
 import numpy as np
 import pytest
 import torch
@@ -11,7 +12,7 @@ from paper_2607_29221_amd import protocol as gproto
 from paper_2607_29221_amd.mosaic import Digits
 from paper_2607_29221_amd.secure_linear import SecureLinear
 from synthetic_inputs import PARAMS_PAPER_D1, decoder_weight, outlier_activations
-from tests.gpu_util import digits_np
+from tests.gpu_util import code_validity, digits_np, unpack_digits
 
 pytestmark = pytest.mark.gpu
 
@@ -75,3 +76,33 @@ def test_secure_linear_fused_equals_separate():
     y_sep = lin(x, call_id=5)
     torch.cuda.synchronize()
     assert np.array_equal(y_fused.cpu().numpy(), y_sep.cpu().numpy())
+
+
+@pytest.mark.parametrize("rows,n,block,qmax", [(64, 8192, 8192, 1997), (48, 28672, 4096, 567),
+                                               (16, 16384, 16384, 1000), (32, 8192, 1024, 1997)],
+                         ids=["one-launch-8192", "two-launch-28672", "one-launch-16384", "blocks-1024"])
+def test_fused_against_oracle(rows, n, block, qmax):
+    """Codes = A' - U - E_a (U and E_a from the oracle's streams) equal the
+    oracle's float64 rotation and quantisation wherever rounding is not
+    ambiguous at float32 precision; scales within 1e-5."""
+    from oracle import sampling as smp
+    from oracle.ring import lift, ring_sub
+    x = outlier_activations(rows, n, 7 * rows + n)
+    x[3] = 0.0
+    signs_np = smp.sample_signs(n, 21, 1)
+    U = smp.sample_matrix("uniform", rows, n, 22, 0x51, 6)
+    E = smp.sample_matrix("dgauss", rows, n, 23, gproto.STREAM_EX, 6, sigma=0.5, bound=4)
+    from tests.gpu_util import to_dev_ring
+    xd = torch.from_numpy(x).cuda()
+    d = Digits.empty(rows, n)
+    sc = torch.empty(rows, dtype=torch.float32, device="cuda")
+    m.mosaic_rotate_quantize_mask(xd, qmax, d, block=block, signs=torch.from_numpy(signs_np).cuda(),
+                                  u=to_dev_ring(U), scale=sc,
+                                  noise=m.rng(23, gproto.STREAM_EX, 6, m.DIST_DGAUSS, sigma=0.5, bound=4))
+    torch.cuda.synchronize()
+    codes = lift(ring_sub(ring_sub(unpack_digits(d), U), E))
+    s = sc.cpu().numpy()
+    assert s[3] == 1.0 and np.all(codes[3] == 0)
+    keep = np.array([i for i in range(rows) if i != 3])
+    amb = code_validity(codes[keep], s[keep], x[keep].astype(np.float64), signs_np, block, qmax)
+    assert amb < 0.1

@@ -14,7 +14,7 @@ from paper_2607_29221_amd import protocol as gproto
 from synthetic_inputs import (PARAMS_D2_SPARSE, PARAMS_D3_SPARSE_SMALL, PARAMS_PAPER_D2_SPARSE,
                               PARAMS_PAPER_D3_SPARSE, DECODE_KN, DECODE_M, DECODE_SEED, NoiseSpec, ProtocolParams,
                               int8_operands)
-from tests.gpu_util import to_dev_ring, to_np_u32
+from tests.gpu_util import noisy_identity, to_dev_ring, to_np_u32
 
 pytestmark = pytest.mark.gpu
 
@@ -266,20 +266,6 @@ def test_weighted_protocol_modes(mode, shape):
     assert np.array_equal(buf.Y.cpu().numpy(), lift(ref.Y).T)
 
 
-def _noisy_identity(A, W, params, seed, weight_id, call_id):
-    """(A + E_a)(W + E_w)^T over Z_{2^32}, E drawn by the oracle's sampler;
-    exact in float64 (entries below 2^53)."""
-    nz = params.noise
-    M, K = A.shape
-    N = W.shape[0]
-    Ea = smp.sample_matrix("dgauss", M, K, seed, smp.STREAM_EX, call_id, sigma=nz.sigma, bound=nz.bound)
-    Ew = smp.sample_matrix("dgauss", N, K, seed, smp.STREAM_EW, weight_id, sigma=nz.sigma, bound=nz.bound)
-    a = A.astype(np.float64) + lift(Ea).astype(np.float64)
-    b = W.astype(np.float64) + lift(Ew).astype(np.float64)
-    y = a @ b.T
-    return (y.astype(np.int64) & 0xFFFFFFFF).astype(np.uint32)
-
-
 @pytest.mark.parametrize("shape_id", range(len(DECODE_KN)), ids=[f"{k}x{n}" for k, n in DECODE_KN])
 @pytest.mark.parametrize("which", ["d2-noisy", "paper-d3-t80"])
 def test_decode_noisy_exact(shape_id, which):
@@ -297,5 +283,5 @@ def test_decode_noisy_exact(shape_id, which):
         Ai = np.ascontiguousarray(A[:Mi])
         buf = gproto.run_call(w, torch.from_numpy(Ai).cuda(), call_id=100 + Mi)
         torch.cuda.synchronize()
-        want = _noisy_identity(Ai, W, params, seed, shape_id, 100 + Mi)
+        want = noisy_identity(Ai, W, params, seed, shape_id, 100 + Mi)
         assert np.array_equal(to_np_u32(buf.Y), want), (which, K, N, Mi)
