@@ -198,6 +198,7 @@ def run_gpu(steps: int, warmup: int, extras: bool):
     if extras:
         out["extras"] = run_extras(dev)
         out["extras"]["decode"] = run_decode(dev)
+        out["extras"]["lpn_client_cost"] = run_lpn_client_cost(dev)
         out["extras"]["decoder_stack"] = run_decoder_stack(dev)
         out["extras"]["integrity_check"] = run_integrity(dev)
         out["extras"]["matvec_sweep"] = run_matvec_sweep(dev)
@@ -568,8 +569,8 @@ def run_decode(dev):
     import torch
 
     from paper_2607_29221_amd import protocol as gp
-    from synthetic_inputs import (DECODE_KN, DECODE_M, DECODE_SEED, PARAMS_PAPER_D2_SPARSE, PARAMS_PAPER_D3_SPARSE,
-                                  int8_operands)
+    from synthetic_inputs import (DECODE_KN, DECODE_M, DECODE_SEED, PARAMS_DECODE_D2_NOISY, PARAMS_PAPER_D2_SPARSE,
+                                  PARAMS_PAPER_D3_SPARSE, PARAMS_PAPER_D3_T80, int8_operands)
 
     res = []
     reps = 20
@@ -583,19 +584,31 @@ def run_decode(dev):
             return [gp.MaskedWeight(Wd, params, 0xDEC0DE00 + 0x100 * j + idx, weight_id=idx, sparse_lpn=sparse)
                     for j in range(nrot)]
 
-        wl = weights(PARAMS_PAPER_D2_SPARSE, False)
+        wl = weights(PARAMS_PAPER_D2_SPARSE, False)        # dense LPN form only (the server loop)
+        wal = weights(PARAMS_PAPER_D2_SPARSE, None)        # both forms, chosen per call by token count
         wsl = weights(PARAMS_PAPER_D2_SPARSE, True)
         w3l = weights(PARAMS_PAPER_D3_SPARSE, True)
+        wnl = weights(PARAMS_DECODE_D2_NOISY, None)         # the same with sigma = 0.5 LWE error
+        wtl = weights(PARAMS_PAPER_D3_T80, None)            # Example 4.1 in full (t = 80)
         w = wl[0]
         for M in DECODE_M:
             Ad = torch.from_numpy(A[:M].copy()).to(dev)
             bl = [gp.alloc_call(x, M, dev) for x in wl]
+            bal = [gp.alloc_call(x, M, dev) for x in wal]
             bsl = [gp.alloc_call(x, M, dev) for x in wsl]
             b3l = [gp.alloc_call(x, M, dev) for x in w3l]
-            for ws_, bs_ in ((wl, bl), (wsl, bsl), (w3l, b3l)):
+            bnl = [gp.alloc_call(x, M, dev) for x in wnl]
+            btl = [gp.alloc_call(x, M, dev) for x in wtl]
+            lists = ((wl, bl), (wal, bal), (wsl, bsl), (w3l, b3l), (wnl, bnl), (wtl, btl))
+            for ws_, bs_ in lists:
                 for j in range(nrot):
                     gp.run_call(ws_[j], Ad, 10_000 + j, bs_[j])
             torch.cuda.synchronize()
+            extra_graph = {}
+            for key, (ws_, bs_) in (("call_us_auto_lpn_graph", lists[1]), ("call_us_d2_noisy_graph", lists[4]),
+                                    ("call_us_d3_t80_graph", lists[5])):
+                extra_graph[key] = round(_graph_ms(lambda i: gp.run_call(ws_[i % nrot], Ad, 50_000 + i,
+                                                                         bs_[i % nrot]), reps) * 1e3, 2)
             # the loops once more as replayed graphs: device time without the
             # host's per-launch cost (which bounds the eager whole-call loops)
             server_graph_ms = _graph_ms(lambda i: gp.server(wl[i % nrot], M, bl[i % nrot]), reps)
@@ -651,10 +664,59 @@ def run_decode(dev):
                         "call_us_sparse_lpn_graph": round(call_sparse_graph_ms * 1e3, 2),
                         "call_us_d3_sparse_lpn_graph": round(call_d3_graph_ms * 1e3, 2),
                         "init_x_us_sparse_lpn": round(init_x_ms * 1e3, 2),
-                        "online_us_sparse_lpn": round(online_ms * 1e3, 2), "weights_rotated": nrot})
-            del bl, bsl, b3l
-        del w, wl, wsl, w3l
+                        "online_us_sparse_lpn": round(online_ms * 1e3, 2), "weights_rotated": nrot,
+                        **extra_graph})
+            del bl, bal, bsl, b3l, bnl, btl
+        del w, wl, wal, wsl, w3l, wnl, wtl
     return res
+
+
+def run_lpn_client_cost(dev):
+    """The client's share of a decode call for the three mask depths of
+    Example 4.1 -- LWE only (r = 1536), + LPN-1 (r_2 = 1024, t_2 = 80),
+    + LPN-2 (r_3 = 652, t_3 = 80), all with sigma = 0.5 -- at (K, N) = (4096,
+    14336): Init X, mask and unmask (no server product), sparse LPN form,
+    device time of 20 calls replayed as a HIP graph, calls cycling through
+    distinct masked weights. Table "lpn-tradeoff" puts the client's
+    multiplications per (m + n) l at r_1 = 1536, r_2 + t_2 = 1104 and
+    r_3 + t_2 + t_3 = 812 (ratios 1, 0.719, 0.529)."""
+    import torch
+
+    from paper_2607_29221_amd import protocol as gp
+    from synthetic_inputs import (DECODE_SEED, PARAMS_PAPER_D1, PARAMS_PAPER_D2_T80, PARAMS_PAPER_D3_T80,
+                                  int8_operands)
+
+    K, N, reps = 4096, 14336, 20
+    A, W = int8_operands(64, K, N, DECODE_SEED)
+    Wd = torch.from_numpy(W).to(dev)
+    cfgs = (("lwe_only", PARAMS_PAPER_D1), ("lpn1_t80", PARAMS_PAPER_D2_T80), ("lpn2_t80", PARAMS_PAPER_D3_T80))
+    table = {"lwe_only": 1536, "lpn1_t80": 1104, "lpn2_t80": 812}
+    rows = []
+    for M in (8, 64):
+        Ad = torch.from_numpy(A[:M].copy()).to(dev)
+        entry = {"M": M}
+        for name, params in cfgs:
+            nrot = _rotation(4 * K * (N + sum(params.ranks)))
+            wl = [gp.MaskedWeight(Wd, params, 0xC11E0000 + 0x100 * j, weight_id=1, sparse_lpn=True)
+                  for j in range(nrot)]
+            bl = [gp.alloc_call(x, M, dev) for x in wl]
+            for j in range(nrot):
+                gp.run_call(wl[j], Ad, 60_000 + j, bl[j])
+
+            def client(i):
+                gp.init_x(wl[i % nrot], M, 70_000 + i, bl[i % nrot])
+                gp.mask(wl[i % nrot], Ad, 70_000 + i, bl[i % nrot])
+                gp.unmask(wl[i % nrot], M, bl[i % nrot])
+            entry[name + "_us"] = round(_graph_ms(client, reps) * 1e3, 2)
+            del wl, bl
+        base = entry["lwe_only_us"]
+        entry["ratio"] = [round(entry[n + "_us"] / base, 3) for n, _ in cfgs]
+        rows.append(entry)
+    return {"K": K, "N": N, "rows": rows,
+            "table_per_row": [table[n] for n, _ in cfgs],
+            "table_ratio": [round(table[n] / 1536, 3) for n, _ in cfgs],
+            "summary": {"table_ratio": [round(table[n] / 1536, 3) for n, _ in cfgs],
+                        **{f"M{r['M']}_ratio": r["ratio"] for r in rows}}}
 
 
 def run_decoder_stack(dev):
@@ -725,6 +787,62 @@ def _shape(name):
     return decoder_linear_shape(name)
 
 
+def run_mfma_ceiling():
+    """The ceiling the server product runs under: the register-only MFMA
+    probe (v_mfma_i32_32x32x32_i8, operands in registers, no memory traffic)
+    on zero, constant and uniformly random operands, each timed for about
+    0.3 s after 0.5 s of the same load; then the server product itself at
+    the 8192 x 30208 x 8192 prefill server shape on uniform and on all-zero
+    digits. int8 TOP/s."""
+    import torch
+
+    from paper_2607_29221_amd import mosaic as m
+    from paper_2607_29221_amd.mosaic import Digits
+
+    dev = torch.device("cuda", 0)
+    out = torch.zeros(1, dtype=torch.int32, device=dev)
+    res = {}
+    iters = 8192
+    for mode, name in ((0, "zero"), (1, "constant"), (2, "random")):
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 0.5:
+            m.mosaic_probe_mfma_i8(mode, iters, out)
+            torch.cuda.synchronize()
+        e0, e1 = _events(2)
+        e0.record()
+        ops, n = 0, 0
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 0.3 or n < 3:
+            ops += m.mosaic_probe_mfma_i8(mode, iters, out)
+            n += 1
+        e1.record()
+        torch.cuda.synchronize()
+        res[f"register_{name}_tops"] = round(ops / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+    M, K, Np = 2048, 8192, 30208
+    A, B = Digits.empty(M, K, dev), Digits.empty(Np, K, dev)
+    C = torch.empty((M, Np), dtype=torch.int32, device=dev)
+    for name in ("uniform", "zero"):
+        if name == "uniform":
+            m.mosaic_sample(m.rng(1, 1, 0, m.DIST_UNIFORM), M, K, out_dig=A)
+            m.mosaic_sample(m.rng(1, 2, 0, m.DIST_UNIFORM), Np, K, out_dig=B)
+        else:
+            A.buf.zero_()
+            B.buf.zero_()
+        for _ in range(20):
+            m.mosaic_masked_matmul(A, B, M, Np, K, C)
+        e0, e1 = _events(2)
+        e0.record()
+        for _ in range(10):
+            m.mosaic_masked_matmul(A, B, M, Np, K, C)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 10
+        res[f"server_{name}_digits_tops"] = round(20.0 * M * K * Np / ms / 1e9, 1)
+    res["server_over_register_random"] = round(res["server_uniform_digits_tops"] / res["register_random_tops"], 3)
+    res["server_over_register_zero"] = round(res["server_zero_digits_tops"] / res["register_zero_tops"], 3)
+    return res
+
+
 def run_product_only():
     """The server product alone (mosaic_masked_matmul) at the prefill server
     shapes, M = 2048, (N + 1536, K), on uniformly sampled digit operands:
@@ -758,37 +876,120 @@ def run_product_only():
     return out
 
 
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def run_cpu_baseline():
-    """The oracle on a bounded sample of the same workload: 384 tokens x 128
-    output columns of the (K, N) = (8192, 8192) shape, full per-call path
-    (Init X, mask, server product incl. Q, unmask; 10-25 s of CPU work on the
-    hosts seen so far);
-    Init W for those 128 weight rows is prepared outside the timed region.
-    At this output width the rank-1536 mask products (U_a and Q, M K r ring
-    MACs each) dominate the oracle's work, so its rate per plaintext ring op
-    is lower than it would be at the full width."""
+    """The oracle on the GPU machine's host cores (its plain C leg, OpenMP over
+    output rows; ``cores`` is the thread count OpenMP uses), on bounded
+    samples:
+
+    * the prefill call at K = 8192, rank 1536, for 1024 of the 2048 tokens
+      and 2048 of the 8192 output columns: Init X, mask, server product with
+      Q, unmasking (Init W of those weight rows prepared outside the timed
+      region, as on the GPU). ``value`` counts every ring multiply-accumulate
+      the call does (U_a, K_c, Y', Q and the unmask product) as two ring
+      operations, so the counted operations equal the work done;
+      ``plaintext_ring_tops`` counts only the 2 M K N of the plaintext product
+      (the GPU line's definition; at this width the rank-1536 products are a
+      larger share of the work than at N = 8192);
+    * the rotation of 4096 x 8192 float64 rows, forward and inverse, on all
+      threads, and of 512 rows on one thread;
+    * the single masked matmul (64 x 512 x 512, depth 1, rank 128) on one
+      thread."""
+    import os as _os
+
     import numpy as np
 
+    from oracle import _cring
     from oracle import protocol as op
-    from synthetic_inputs import PARAMS_PAPER_D1, PREFILL_SEED, int8_operands
+    from oracle.sampling import sample_signs
+    from synthetic_inputs import (PARAMS_D1_SMALL_R128, PARAMS_PAPER_D1, PREFILL_SEED, int8_operands,
+                                  outlier_activations)
 
-    K, N, Ms, Ns = 8192, 8192, 384, 128
+    threads = _cring.threads()
+    K, N, Ms, Ns, r = 8192, 8192, 1024, 2048, PARAMS_PAPER_D1.ranks[0]
     A, W = int8_operands(2048, K, N, PREFILL_SEED)
     seed = 0x6D6F736169630000 | PREFILL_SEED
-    ws = op.init_w(W[:Ns], PARAMS_PAPER_D1, seed, 0)
-    X = A[:Ms].T
     t0 = time.perf_counter()
-    cs = op.init_x(ws, Ms, PARAMS_PAPER_D1, seed, 0)
-    Xm = op.mask(X, cs)
-    Ym, Q = op.server(ws, Xm)
-    Y = op.unmask(ws, cs, Ym, Q)
+    w = op.init_w_depth1_c(W[:Ns], PARAMS_PAPER_D1, seed, 0)
+    init_w_s = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    res = op.call_depth1_c(w, A[:Ms], PARAMS_PAPER_D1, seed, 1)
     dt = time.perf_counter() - t0
-    assert Y.shape == (Ns, Ms)
-    ops = 2.0 * Ms * K * Ns
-    return {"value": ops / dt / 1e12, "unit": "ring-TOPS", "cores": 1, "kind": "oracle",
-            "seconds": round(dt, 2),
-            "sample": f"{Ms} tokens x {Ns} output columns of (K, N) = ({K}, {N}), rank 1536, full per-call "
-                      "path (Init X, mask, server incl. Q, unmask); numpy integer matmul, single-threaded"}
+    assert res["Y"].shape == (Ms, Ns)
+    macs = Ms * (r * K + r * Ns + K * (Ns + r) + r * Ns)
+
+    x = outlier_activations(4096, 8192, 3)
+    d = sample_signs(8192, 3, 0)
+    t0 = time.perf_counter()
+    y = _cring.rotate_rows(x, d)
+    xb = _cring.rotate_rows(y, d, inverse=True)
+    rot_s = time.perf_counter() - t0
+    assert np.max(np.abs(xb - x)) < 1e-9 * np.max(np.abs(x))
+
+    prev = _os.environ.get("OMP_NUM_THREADS")
+    one = {}
+    try:
+        import ctypes
+        ctypes.CDLL("libgomp.so.1").omp_set_num_threads(1)
+        t0 = time.perf_counter()
+        y1 = _cring.rotate_rows(x[:512], d)
+        _cring.rotate_rows(y1, d, inverse=True)
+        one["rotation_512x8192_fwd_inv_s"] = round(time.perf_counter() - t0, 3)
+        A1, W1 = int8_operands(64, 512, 512, 0)
+        t0 = time.perf_counter()
+        w1 = op.init_w_depth1_c(W1, PARAMS_D1_SMALL_R128, 1234, 0)
+        op.call_depth1_c(w1, A1, PARAMS_D1_SMALL_R128, 1234, 0)
+        one["single_matmul_64x512x512_s"] = round(time.perf_counter() - t0, 4)
+        one["threads"] = _cring.threads()
+    finally:
+        ctypes.CDLL("libgomp.so.1").omp_set_num_threads(threads)
+        if prev is not None:
+            _os.environ["OMP_NUM_THREADS"] = prev
+    return {"value": round(2.0 * macs / dt / 1e12, 5), "unit": "ring-TOPS", "cores": threads,
+            "kind": "oracle", "seconds": round(dt, 2),
+            "plaintext_ring_tops": round(2.0 * Ms * K * Ns / dt / 1e12, 5),
+            "sample": f"{Ms} of 2048 tokens x {Ns} of {N} output columns at K = {K}, rank {r}: Init X, mask, "
+                      f"server with Q, unmask ({macs:.3g} ring MACs, all counted); plain C ring loops "
+                      f"(gcc -O2, OpenMP over rows); Init W {init_w_s:.1f} s untimed",
+                      "host_cpus": _os.cpu_count(), "cpu_model": _cpu_model(),
+            "rotation_4096x8192_fwd_inv_s": round(rot_s, 3),
+            "rotation_gbs": round(2 * 4096 * 8192 * 16 / rot_s / 1e9, 2),
+            "one_thread": one}
+
+
+def _compact(ex):
+    """The figures of the extras that the roofline targets name, as short
+    top-level keys of the JSON line (the full extras go to a side file)."""
+    out = {}
+    p = {}
+    p["fwht_4096x8192"] = {"us": ex["fwht_4096x8192_us"], "gbs": ex["fwht_gbs"], "hbm_frac": ex["fwht_hbm_frac"]}
+    for key, name in (("mask", "mask_2048x28672"), ("mask_in_pass_noise", "mask_noise_2048x28672")):
+        p[name] = {"us": ex[key + "_us"], "gbs": ex[key + "_gbs"], "hbm_frac": ex[key + "_hbm_frac"]}
+    for si in ex.get("secure_input", []):
+        p[f"fused_input_{si['rows']}x{si['n']}"] = {"us": si["fused_us"], "gbs": si["fused_gbs"],
+                                                      "hbm_frac": round(si["fused_gbs"] / HBM_PEAK_GBS, 3)}
+    out["passes"] = p
+    if "decode" in ex:
+        out["decode"] = [{"K": d["K"], "N": d["N"], "M": d["M"], "server_hbm_frac": d["server_hbm_frac"],
+                          "call_us_graph": d["call_us_auto_lpn_graph"]} for d in ex["decode"]]
+    if "lpn_client_cost" in ex:
+        out["lpn_client_cost"] = ex["lpn_client_cost"]["summary"]
+    if "integrity_check" in ex:
+        out["integrity_check_over_server"] = [c["check_over_server"] for c in ex["integrity_check"]]
+    if "decoder_stack" in ex:
+        ds = ex["decoder_stack"]
+        out["decoder_stack"] = {"secure_ms": ds["secure_forward_ms"], "plaintext_fp32_ms": ds["plaintext_fp32_forward_ms"],
+                                "rel_l2_per_layer": [v["rel_l2"] for v in ds["per_layer"]]}
+    return out
 
 
 def main():
@@ -805,6 +1006,8 @@ def main():
                          "pass; for counter runs)")
     ap.add_argument("--decode-only", action="store_true",
                     help="only time the decode-shaped calls (for kernel traces)")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="only the register-only MFMA probe and the server product on uniform and zero digits")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device three times (scale for HBM byte counters)")
     args = ap.parse_args()
@@ -817,6 +1020,10 @@ def main():
         print(json.dumps({"product_only": run_product_only()}))
         return
 
+    if args.mfma_ceiling:
+        print(json.dumps({"mfma_ceiling": run_mfma_ceiling()}))
+        return
+
     if args.passes_only:
         import torch
         _warm_up(torch.device("cuda:0"))
@@ -826,7 +1033,8 @@ def main():
     if args.decode_only:
         import torch
         _warm_up(torch.device("cuda:0"))
-        print(json.dumps({"decode": run_decode(torch.device("cuda:0"))}))
+        print(json.dumps({"decode": run_decode(torch.device("cuda:0")),
+                          "lpn_client_cost": run_lpn_client_cost(torch.device("cuda:0"))}))
         return
 
     if args.copy_calibration:
@@ -861,7 +1069,15 @@ def main():
         "per_shape": gpu["per_shape"],
     }
     if "extras" in gpu:
-        line["extras"] = gpu["extras"]
+        line.update(_compact(gpu["extras"]))
+        path = os.path.join(ROOT, "gpurun_out", "bench_extras.json")
+        try:
+            os.makedirs(os.path.dirname(path), exist_ok=True)
+            with open(path, "w") as f:
+                json.dump(gpu["extras"], f, indent=1)
+            line["extras_file"] = os.path.relpath(path, ROOT)
+        except OSError:
+            pass
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = run_cpu_baseline()
     print(json.dumps(line), flush=True)

@@ -243,3 +243,50 @@ def sampled_depth1(A_rows: np.ndarray, W_rows: np.ndarray, I, J, K: int, params,
     ident = ring_matmul(ring_add(to_ring(A_rows), Ex_I), WE.T)
     return dict(W_masked=Wm, U_a=Ua_noE, A_masked=Am, Y_masked=Ym, Q=Q, K_c=Kc, Y=Y, identity=ident,
                 E_w=Ew_J, E_x=Ex_I)
+
+
+# ---------------------------------------------------------------------------
+# Depth 1 (Section 4.1) in the build's row-major orientation, with the ring
+# products of the plain C leg (oracle/c/ring_oracle.c, all host cores): the
+# same streams and the same sums as init_w / init_x / mask / server / unmask
+# above, for the CPU baseline at workload sizes.
+# ---------------------------------------------------------------------------
+@dataclass
+class Depth1Weight:
+    W_masked: np.ndarray    # W' = W + E_w + L M     (N x K)
+    M: np.ndarray           # M_1                    (r x K)
+    N: np.ndarray           # N_1                    (K x r)
+    L: np.ndarray           # L                      (N x r)
+    J: np.ndarray           # J_1 = (W + E_w) N_1    (N x r)
+
+
+def init_w_depth1_c(W_plain: np.ndarray, params, seed: int, weight_id: int) -> Depth1Weight:
+    """Init W (box steps 1-5 at d = 1) for W (N x K)."""
+    from . import _cring
+    N_, K = W_plain.shape
+    r = params.ranks[0]
+    L = smp.sample_matrix("uniform", N_, r, seed, smp.STREAM_L, weight_id)
+    M = smp.sample_matrix("uniform", r, K, seed, smp.STREAM_M + 1, weight_id)
+    Nm = smp.sample_matrix("uniform", K, r, seed, smp.STREAM_N + 1, weight_id)
+    WE = ring_add(to_ring(W_plain), _noise(params, N_, K, seed, smp.STREAM_EW, weight_id))
+    Wm = ring_add(WE, _cring.ring_matmul_nt(L, np.ascontiguousarray(M.T)))
+    J = _cring.ring_matmul_nt(WE, np.ascontiguousarray(Nm.T))
+    return Depth1Weight(W_masked=Wm, M=M, N=Nm, L=L, J=J)
+
+
+def call_depth1_c(w: Depth1Weight, A_plain: np.ndarray, params, seed: int, call_id: int) -> dict:
+    """Init X, mask, server product and unmasking for A (M x K tokens):
+        U_a = R^T N^T,  K_c = R^T J^T,  A' = A + U_a + E_a,
+        Y' = A' W'^T,  Q^T = A' M^T,  Y = Y' - K_c - Q^T L^T."""
+    from . import _cring
+    Mt, K = A_plain.shape
+    r = w.M.shape[0]
+    Rt = smp.sample_matrix("uniform", Mt, r, seed, smp.STREAM_R, call_id)
+    Ea = _noise(params, Mt, K, seed, smp.STREAM_EX, call_id)
+    Ua = _cring.ring_matmul_nt(Rt, w.N)
+    Kc = _cring.ring_matmul_nt(Rt, w.J)
+    Am = ring_add(to_ring(A_plain), Ua, Ea)
+    Ym = _cring.ring_matmul_nt(Am, w.W_masked)
+    Qt = _cring.ring_matmul_nt(Am, w.M)
+    Y = ring_sub(ring_sub(Ym, Kc), _cring.ring_matmul_nt(Qt, w.L))
+    return dict(U_a=Ua, K_c=Kc, A_masked=Am, Y_masked=Ym, Q=Qt, Y=Y, E_a=Ea)

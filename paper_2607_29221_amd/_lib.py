@@ -61,6 +61,7 @@ _SIGNATURES = {
                                   c_i32),
     "mosaic_hadamard_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
     "mosaic_hadamard28_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
+    "mosaic_probe_mfma_i8": ([c_i32, c_i64, c_ptr, ctypes.POINTER(c_i64), c_ptr], c_i32),
     "mosaic_quantize_rows": ([c_ptr, c_i64, c_i64, c_i64, c_i32, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_ptr],
                              c_i32),
 }

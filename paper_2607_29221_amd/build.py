@@ -26,7 +26,7 @@ ARCH = os.environ.get("MOSAIC_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["abi.cpp", "elementwise.hip", "ring_gemm.hip", "ring_gemm_skinny.hip", "hadamard.hip", "quantize.hip",
-           "sparse.hip", "secure_input.hip", "hadamard28.hip"]
+           "sparse.hip", "secure_input.hip", "hadamard28.hip", "probe.hip"]
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-x", "hip",
          # keep the compiler from forming packed fp32 instructions
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

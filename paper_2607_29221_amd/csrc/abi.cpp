@@ -10,6 +10,7 @@
 #include <string>
 
 #include "../../include/mosaic.h"
+#include "../../include/mosaic_probe.h"
 #include "internal.h"
 
 using namespace mosaic;
@@ -514,6 +515,13 @@ mosaic_status mosaic_quantize_rows(const float* x, int64_t ldx, int64_t rows, in
   if (rows >= (int64_t(1) << 31)) return fail(MOSAIC_ERR_UNSUPPORTED, "too many rows");
   return hip_status(launch_quantize_rows(x, ldx, rows, n, qmax, q, ldq, q_dig, q_pitch, scale, (hipStream_t)stream),
                     "quantize launch");
+}
+
+mosaic_status mosaic_probe_mfma_i8(int32_t mode, int64_t iters, int32_t* out, int64_t* ops, void* stream) {
+  if (mode < 0 || mode > 2) return fail(MOSAIC_ERR_INVALID_ARG, "mode %d outside {0, 1, 2}", mode);
+  if (iters < 1) return fail(MOSAIC_ERR_INVALID_ARG, "iters must be >= 1");
+  if (out == nullptr || ops == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "out or ops is NULL");
+  return hip_status(launch_mfma_probe(mode, iters, out, ops, (hipStream_t)stream), "mfma probe launch");
 }
 
 }  // extern "C"

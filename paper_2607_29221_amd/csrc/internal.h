@@ -52,6 +52,8 @@ hipError_t launch_weighted_csr_count(int64_t rows, int64_t t, int64_t* row_ptr, 
 hipError_t launch_weighted_csr_fill(const RngArgs& r, int64_t rows, int64_t cols, const int64_t* row_ptr,
                                     int32_t* col_idx, uint32_t* values, hipStream_t s);
 
+hipError_t launch_mfma_probe(int mode, int64_t iters, int32_t* out, int64_t* ops, hipStream_t s);
+
 hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb, int64_t rows,
                                    int64_t cols, int64_t* count, hipStream_t s);
 

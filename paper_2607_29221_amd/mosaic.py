@@ -258,3 +258,12 @@ def mosaic_quantize_rows(x: torch.Tensor, qmax: int, q: Optional[torch.Tensor] =
                                             q.stride(0) if q is not None else 0,
                                             q_dig.ptr if q_dig else None, q_dig.pitch if q_dig else 0,
                                             _ptr(scale), _stream()), "mosaic_quantize_rows")
+
+
+def mosaic_probe_mfma_i8(mode: int, iters: int, out: torch.Tensor) -> int:
+    """Launches the register-only MFMA probe (measurement aid); returns the
+    int8 operations launched. ``out`` is a one-element int32 device tensor."""
+    ops = ctypes.c_int64(0)
+    _check(_lib.load().mosaic_probe_mfma_i8(mode, iters, out.data_ptr(), ctypes.byref(ops), _stream()),
+           "mosaic_probe_mfma_i8")
+    return int(ops.value)
