@@ -891,15 +891,13 @@ def run_cpu_baseline():
     output rows; ``cores`` is the thread count OpenMP uses), on bounded
     samples:
 
-    * the prefill call at K = 8192, rank 1536, for 1024 of the 2048 tokens
-      and 2048 of the 8192 output columns: Init X, mask, server product with
-      Q, unmasking (Init W of those weight rows prepared outside the timed
-      region, as on the GPU). ``value`` counts every ring multiply-accumulate
-      the call does (U_a, K_c, Y', Q and the unmask product) as two ring
-      operations, so the counted operations equal the work done;
-      ``plaintext_ring_tops`` counts only the 2 M K N of the plaintext product
-      (the GPU line's definition; at this width the rank-1536 products are a
-      larger share of the work than at N = 8192);
+    * the whole prefill call at the first shape, M = 2048, (K, N) = (8192,
+      8192), rank 1536: Init X, mask, server product with Q, unmasking (Init
+      W prepared outside the timed region, as on the GPU). ``value`` counts
+      every ring multiply-accumulate the call does (U_a, K_c, Y', Q and the
+      unmask product) as two ring operations, so the counted operations
+      equal the work done; ``plaintext_ring_tops`` counts only the 2 M K N of
+      the plaintext product (the GPU line's definition);
     * the rotation of 4096 x 8192 float64 rows, forward and inverse, on all
       threads, and of 512 rows on one thread;
     * the single masked matmul (64 x 512 x 512, depth 1, rank 128) on one
@@ -915,7 +913,7 @@ def run_cpu_baseline():
                                   outlier_activations)
 
     threads = _cring.threads()
-    K, N, Ms, Ns, r = 8192, 8192, 1024, 2048, PARAMS_PAPER_D1.ranks[0]
+    K, N, Ms, Ns, r = 8192, 8192, 2048, 8192, PARAMS_PAPER_D1.ranks[0]
     A, W = int8_operands(2048, K, N, PREFILL_SEED)
     seed = 0x6D6F736169630000 | PREFILL_SEED
     t0 = time.perf_counter()
@@ -957,7 +955,7 @@ def run_cpu_baseline():
     return {"value": round(2.0 * macs / dt / 1e12, 5), "unit": "ring-TOPS", "cores": threads,
             "kind": "oracle", "seconds": round(dt, 2),
             "plaintext_ring_tops": round(2.0 * Ms * K * Ns / dt / 1e12, 5),
-            "sample": f"{Ms} of 2048 tokens x {Ns} of {N} output columns at K = {K}, rank {r}: Init X, mask, "
+            "sample": f"the whole call at M = {Ms}, (K, N) = ({K}, {Ns}), rank {r}: Init X, mask, "
                       f"server with Q, unmask ({macs:.3g} ring MACs, all counted); plain C ring loops "
                       f"(gcc -O2, OpenMP over rows); Init W {init_w_s:.1f} s untimed",
                       "host_cpus": _os.cpu_count(), "cpu_model": _cpu_model(),

@@ -49,6 +49,48 @@ def padded_k(k: int) -> int:
     return 64 * ((k + 63) // 64)
 
 
+# Host-side shape checks before any launch: the C ABI sees only pointers and
+# sizes, so a tensor smaller than the sizes passed would be read or written
+# past its end on the GPU. These raise ValueError instead.
+def _need(t: Optional[torch.Tensor], rows: int, cols: int, name: str, dtypes=None, optional: bool = True) -> None:
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if rows == 0 or cols == 0:
+        return
+    if t.dim() == 1:
+        if rows * cols > t.numel() or (rows > 1 and cols > 1):
+            raise ValueError(f"{name} holds {t.numel()} elements, needs {rows} x {cols}")
+        return
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be a matrix")
+    if t.shape[0] < rows or t.shape[1] < cols:
+        raise ValueError(f"{name} is {tuple(t.shape)}, needs at least ({rows}, {cols})")
+    if cols > 1 and t.stride(1) != 1:
+        raise ValueError(f"{name} must have contiguous rows")
+
+
+def _need_dig(d: Optional["Digits"], rows: int, cols: int, name: str, optional: bool = True) -> None:
+    if d is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not d.buf.is_cuda or d.buf.dtype != torch.int8 or d.buf.dim() != 2 or d.buf.stride(1) != 1:
+        raise ValueError(f"{name} must be a row-contiguous int8 device matrix")
+    if rows == 0 or cols == 0:
+        return
+    if d.rows < rows or d.col0 % 64 or 4 * (d.col0 + padded_k(cols)) > d.pitch:
+        raise ValueError(f"{name} ({d.rows} rows, pitch {d.pitch}, column {d.col0}) cannot hold {rows} x {cols} digits")
+
+
+_INT = (torch.int32,)
+
+
 @dataclass
 class Digits:
     """rows x cols ring matrix in digit layout, at column ``col0`` of ``buf``."""
@@ -107,6 +149,8 @@ def mosaic_dgauss_thresholds(sigma: float, bound: int) -> List[int]:
 
 def mosaic_sample(r: _lib.MosaicRng, rows: int, cols: int, out: Optional[torch.Tensor] = None,
                   out_dig: Optional[Digits] = None) -> None:
+    _need(out, rows, cols, "out", _INT)
+    _need_dig(out_dig, rows, cols, "out_dig")
     ldo = out.stride(0) if out is not None else 0
     _check(_lib.load().mosaic_sample(ctypes.byref(r), rows, cols, _ptr(out), ldo,
                                      out_dig.ptr if out_dig else None, out_dig.pitch if out_dig else 0,
@@ -119,10 +163,18 @@ def mosaic_mask(x: Optional[torch.Tensor], u: Optional[torch.Tensor], noise: Opt
     """out = x + u + noise (mod 2^32). ``x_transposed`` reads x[j, i] for
     element (i, j) (x then has shape (cols, rows))."""
     if x is not None:
+        if x.dtype not in _TORCH_DT or not x.is_cuda or x.dim() != 2:
+            raise ValueError("x must be an int8/int16/int32 device matrix")
+        xr, xc = (cols, rows) if x_transposed else (rows, cols)
+        if x.shape[0] < xr or x.shape[1] < xc:
+            raise ValueError(f"x is {tuple(x.shape)}, needs at least ({xr}, {xc})")
         dt = _TORCH_DT[x.dtype]   # int32 and uint32 embed identically into the ring
         rs, cs = (x.stride(1), x.stride(0)) if x_transposed else (x.stride(0), x.stride(1))
     else:
         dt, rs, cs = DT_U32, 0, 0
+    _need(u, rows, cols, "u", _INT)
+    _need(out, rows, cols, "out", _INT)
+    _need_dig(out_dig, rows, cols, "out_dig")
     ldu = u.stride(0) if u is not None else 0
     ldo = out.stride(0) if out is not None else 0
     _check(_lib.load().mosaic_mask(_ptr(x), dt, rs, cs, _ptr(u), ldu,
@@ -133,6 +185,9 @@ def mosaic_mask(x: Optional[torch.Tensor], u: Optional[torch.Tensor], noise: Opt
 
 def mosaic_masked_matmul(a: Digits, b: Digits, M: int, N: int, K: int, c: torch.Tensor) -> None:
     """c[:M, :N] = A B^T over Z_{2^32} (c is an int32 tensor holding ring words)."""
+    _need_dig(a, M, K, "a", optional=False)
+    _need_dig(b, N, K, "b", optional=False)
+    _need(c, M, N, "c", _INT, optional=False)
     _check(_lib.load().mosaic_masked_matmul(a.ptr, a.pitch, b.ptr, b.pitch, M, N, K, c.data_ptr(),
                                             c.stride(0), _stream()), "mosaic_masked_matmul")
 
@@ -141,6 +196,16 @@ def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digi
                   M: int, N: int, R: int, y: Optional[torch.Tensor] = None,
                   s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,
                   y_f32: Optional[torch.Tensor] = None) -> None:
+    _need(ym, M, N, "ym", _INT, optional=False)
+    _need(kc, M, N, "kc", _INT)
+    if R > 0:
+        _need_dig(q, M, R, "q", optional=False)
+        _need_dig(l, N, R, "l", optional=False)
+    _need(y, M, N, "y", _INT)
+    _need(y_f32, M, N, "y_f32", (torch.float32,))
+    if y_f32 is not None:
+        _need(s_rows, 1, M, "s_rows", (torch.float32,), optional=False)
+        _need(s_cols, 1, N, "s_cols", (torch.float32,), optional=False)
     _check(_lib.load().mosaic_unmask(ym.data_ptr(), ym.stride(0), _ptr(kc), kc.stride(0) if kc is not None else 0,
                                      q.ptr if q else None, q.pitch if q else 0,
                                      l.ptr if l else None, l.pitch if l else 0, M, N, R,
@@ -156,6 +221,11 @@ def mosaic_rotate_quantize_mask(x: torch.Tensor, qmax: int, out_dig: Digits, blo
     """Fused rotate + quantise + mask of Pi_Sec-Linear's input: digits of
     round(R x / s) + u + noise for every row of x, and the row scales."""
     rows, n = x.shape
+    _need(x, rows, n, "x", (torch.float32,), optional=False)
+    _need_dig(out_dig, rows, n, "out_dig", optional=False)
+    _need(u, rows, n, "u", _INT)
+    _need(scale, 1, rows, "scale", (torch.float32,))
+    _need(signs, 1, n, "signs", (torch.int8,))
     _check(_lib.load().mosaic_rotate_quantize_mask(x.data_ptr(), x.stride(0), rows, n, n if block is None else block,
                                                    _ptr(signs), qmax, _ptr(u), u.stride(0) if u is not None else 0,
                                                    ctypes.byref(noise) if noise is not None else None,
@@ -195,6 +265,8 @@ def mosaic_sparse_csr(r: _lib.MosaicRng, rows: int, cols: int, exact: bool = Tru
 def mosaic_sparse_gather_rows(p: SparseRows, d: torch.Tensor, ncols: int, c: torch.Tensor,
                               subtract: bool = False) -> None:
     """c[i, :ncols] +-= sum_j P[i, j] d[j, :ncols] (P: rows x r sparse)."""
+    _need(d, p.cols, ncols, "d", _INT, optional=False)
+    _need(c, p.rows, ncols, "c", _INT, optional=False)
     _check(_lib.load().mosaic_sparse_gather_rows(p.rows, p.row_ptr.data_ptr(), p.col_idx.data_ptr(),
                                                  p.values.data_ptr(), d.data_ptr(), d.stride(0), ncols,
                                                  c.data_ptr(), c.stride(0), 1 if subtract else 0, _stream()),
@@ -205,6 +277,8 @@ def mosaic_sparse_stream_gather_rows(r: _lib.MosaicRng, rows: int, rcols: int, d
                                      c: torch.Tensor, subtract: bool = False) -> None:
     """c[i, :ncols] +-= sum_j P[i, j] d[j, :ncols], P the rows x rcols SPARSE
     stream matrix of ``r`` (drawn inside the call)."""
+    _need(d, rcols, ncols, "d", _INT, optional=False)
+    _need(c, rows, ncols, "c", _INT, optional=False)
     _check(_lib.load().mosaic_sparse_stream_gather_rows(ctypes.byref(r), rows, rcols, d.data_ptr(), d.stride(0), ncols,
                                                         c.data_ptr(), c.stride(0), 1 if subtract else 0, _stream()),
            "mosaic_sparse_stream_gather_rows")
@@ -213,6 +287,8 @@ def mosaic_sparse_stream_gather_rows(r: _lib.MosaicRng, rows: int, rcols: int, d
 def mosaic_sparse_gather_cols(p: SparseRows, d: torch.Tensor, M: int, c: torch.Tensor,
                               subtract: bool = False) -> None:
     """c[m, n] +-= sum_j d[m, j] P[n, j] for m < M, n < P.rows."""
+    _need(d, M, p.cols, "d", _INT, optional=False)
+    _need(c, M, p.rows, "c", _INT, optional=False)
     _check(_lib.load().mosaic_sparse_gather_cols(M, p.rows, p.row_ptr.data_ptr(), p.col_idx.data_ptr(),
                                                  p.values.data_ptr(), d.data_ptr(), d.stride(0), c.data_ptr(),
                                                  c.stride(0), 1 if subtract else 0, _stream()),
@@ -232,12 +308,16 @@ def mosaic_count_mismatches(a: torch.Tensor, b: torch.Tensor, count: torch.Tenso
 
 
 def mosaic_sample_signs(r: _lib.MosaicRng, n: int, out: torch.Tensor) -> None:
+    _need(out, 1, n, "out", (torch.int8,), optional=False)
     _check(_lib.load().mosaic_sample_signs(ctypes.byref(r), n, out.data_ptr(), _stream()), "mosaic_sample_signs")
 
 
 def mosaic_hadamard_rotate(x: torch.Tensor, y: torch.Tensor, block: Optional[int] = None,
                            signs: Optional[torch.Tensor] = None, inverse: bool = False) -> None:
     rows, n = x.shape
+    _need(x, rows, n, "x", (torch.float32,), optional=False)
+    _need(y, rows, n, "y", (torch.float32,), optional=False)
+    _need(signs, 1, n, "signs", (torch.int8,))
     _check(_lib.load().mosaic_hadamard_rotate(x.data_ptr(), x.stride(0), y.data_ptr(), y.stride(0), rows, n,
                                               n if block is None else block, _ptr(signs), 1 if inverse else 0,
                                               _stream()), "mosaic_hadamard_rotate")
@@ -246,6 +326,9 @@ def mosaic_hadamard_rotate(x: torch.Tensor, y: torch.Tensor, block: Optional[int
 def mosaic_hadamard28_rotate(x: torch.Tensor, y: torch.Tensor, signs: Optional[torch.Tensor] = None,
                              inverse: bool = False) -> None:
     rows, n = x.shape
+    _need(x, rows, n, "x", (torch.float32,), optional=False)
+    _need(y, rows, n, "y", (torch.float32,), optional=False)
+    _need(signs, 1, n, "signs", (torch.int8,))
     _check(_lib.load().mosaic_hadamard28_rotate(x.data_ptr(), x.stride(0), y.data_ptr(), y.stride(0), rows, n,
                                                 _ptr(signs), 1 if inverse else 0, _stream()),
            "mosaic_hadamard28_rotate")
@@ -254,6 +337,10 @@ def mosaic_hadamard28_rotate(x: torch.Tensor, y: torch.Tensor, signs: Optional[t
 def mosaic_quantize_rows(x: torch.Tensor, qmax: int, q: Optional[torch.Tensor] = None,
                          q_dig: Optional[Digits] = None, scale: Optional[torch.Tensor] = None) -> None:
     rows, n = x.shape
+    _need(x, rows, n, "x", (torch.float32,), optional=False)
+    _need(q, rows, n, "q", _INT)
+    _need_dig(q_dig, rows, n, "q_dig")
+    _need(scale, 1, rows, "scale", (torch.float32,))
     _check(_lib.load().mosaic_quantize_rows(x.data_ptr(), x.stride(0), rows, n, qmax, _ptr(q),
                                             q.stride(0) if q is not None else 0,
                                             q_dig.ptr if q_dig else None, q_dig.pitch if q_dig else 0,

@@ -26,3 +26,34 @@ def test_activation_window_values(K, q_x):
 
 def test_activation_window_without_noise():
     assert activation_window(8192, 127, 0) == (2 ** 31 - 1) // (8192 * 127)
+
+
+def test_binding_rejects_undersized_tensors():
+    """The binding checks tensor sizes against the sizes it passes, before
+    any call reaches the library (no GPU needed: the checks raise first)."""
+    import pytest
+    import torch
+
+    from paper_2607_29221_amd import mosaic as m
+
+    class FakeCuda(torch.Tensor):
+        @property
+        def is_cuda(self):
+            return True
+
+    small = torch.zeros((4, 8), dtype=torch.int32).as_subclass(FakeCuda)
+    r = m.rng(1, 2, 3, m.DIST_UNIFORM)
+    with pytest.raises(ValueError):
+        m.mosaic_sample(r, 5, 8, out=small)
+    with pytest.raises(ValueError):
+        m.mosaic_sample(r, 4, 9, out=small)
+    dig = m.Digits(torch.zeros((4, 256), dtype=torch.int8).as_subclass(FakeCuda), 64)
+    with pytest.raises(ValueError):
+        m.mosaic_masked_matmul(dig, dig, 4, 4, 65, small)          # K beyond the digit buffer
+    with pytest.raises(ValueError):
+        m.mosaic_masked_matmul(dig, dig, 5, 4, 64, small)          # M beyond the rows
+    with pytest.raises(ValueError):
+        m.mosaic_unmask(small, None, dig, dig, 4, 9, 64, y=small)  # N beyond ym
+    cpu = torch.zeros((4, 8), dtype=torch.int32)
+    with pytest.raises(ValueError):
+        m.mosaic_sample(r, 4, 8, out=cpu)                           # host memory
