@@ -171,6 +171,22 @@ mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch,
                                    int64_t M, int64_t N, int64_t K,
                                    uint32_t* c, int64_t ldc, void* stream);
 
+/* The same product with B given as ring words, for short A: C = A B^T over
+ * Z_{2^32} (accumulate != 0: C += A B^T), A: M x K digits (a_pitch), B: N x K
+ * uint32 with leading dimension ldb >= K, C: M x N (ldc >= N). This is the
+ * client's side of the integrity check (Freivalds' test; Appendix
+ * "Computational integrity", online step 4 of the Section 4.2 box): the
+ * check vectors times the server's outputs [Y' | Q], which arrive as ring
+ * words and are read once here instead of being converted to digits first.
+ * Requirements: M <= 64, b 16-byte aligned and ldb a multiple of 4 (else
+ * MOSAIC_ERR_UNSUPPORTED); A's digits past column K must be zero (the digit
+ * layout's padding), because the words read past column K within a row are
+ * whatever follows in memory. */
+mosaic_status mosaic_masked_matmul_words(const int8_t* a_dig, int64_t a_pitch,
+                                         const uint32_t* b, int64_t ldb,
+                                         int64_t M, int64_t N, int64_t K,
+                                         uint32_t* c, int64_t ldc, int32_t accumulate, void* stream);
+
 /* a6. Unmask (protocol box, online step 5, in the build's orientation:
  * Y = Y' - K - Q_d L^T - sum_i Q_i S_{i+1}^T):
  *     y(i, j) = ym(i, j) - kc(i, j) - sum_{r < R} q(i, r) l(j, r)  (mod 2^32)
@@ -270,12 +286,37 @@ mosaic_status mosaic_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row
  * honestly. This call counts the entries where two uint32 matrices differ:
  *     *count = #{(i, j) : a(i, j) != b(i, j)},  0 <= i < rows, 0 <= j < cols
  * a and b are device matrices with leading dimensions lda, ldb >= cols;
- * ``count`` is a device int64 written by the call (0 for an empty matrix).
- * One workgroup does the whole count, so the call is meant for the check's
- * small matrices (t x M). Fails with MOSAIC_ERR_INVALID_ARG for NULL
- * pointers or leading dimensions < cols. */
+ * ``count`` is a device int64 written by the call (0 for an empty matrix):
+ * a first launch clears it, a second adds the workgroups' partial counts to
+ * it atomically, so two calls that share ``count`` on different streams
+ * race. Fails with MOSAIC_ERR_INVALID_ARG for NULL pointers or leading
+ * dimensions < cols. */
 mosaic_status mosaic_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb,
                                       int64_t rows, int64_t cols, int64_t* count, void* stream);
+
+/* The whole integrity check of one call (online step 4 of the Section 4.2
+ * protocol box; Appendix "Computational integrity"): with t check vectors,
+ *     d = c^T A'^T - V [Y' | Q]^T   (t x M, over Z_{2^32}),
+ *     *count = #{(j, i) : d(j, i) != 0},
+ * where c^T (t x K, digit layout ct_dig / ct_pitch) is the client's key,
+ * A' (M x K, a_dig / a_pitch) the masked activations the server received,
+ * V = [a_W | a_Q] (t x NR, v_dig / v_pitch) the check vectors laid out like
+ * the columns of [Y' | Q], and [Y' | Q] (M x NR uint32 ring words, leading
+ * dimension ldyq) the server's output. count = 0 accepts the call; an
+ * output the server changed by delta in column k is caught by the vectors
+ * j with V(j, k) delta != 0. d (leading dimension ldd >= M) and count are
+ * written by the call; d tells which tokens failed which vectors.
+ * Constraints: 0 <= t <= 64; yq 16-byte aligned and ldyq a multiple of 4
+ * (else MOSAIC_ERR_UNSUPPORTED), ldyq >= NR; digit pitches as for
+ * mosaic_masked_matmul; row pitches at most 8 MiB. Columns of [Y' | Q]
+ * past NR up to the next multiple of 64 are read (within each row's ldyq
+ * words, and up to the 16-byte boundary past the last row's NR-th word)
+ * and cancelled by V's zero padding digits. Four launches on the stream:
+ * clear d and count, d += c^T A'^T, d -= V [Y' | Q]^T, count. */
+mosaic_status mosaic_integrity_check(const int8_t* ct_dig, int64_t ct_pitch, const int8_t* a_dig, int64_t a_pitch,
+                                     const int8_t* v_dig, int64_t v_pitch, const uint32_t* yq, int64_t ldyq,
+                                     int64_t t, int64_t M, int64_t K, int64_t NR, uint32_t* d, int64_t ldd,
+                                     int64_t* count, void* stream);
 
 /* a1 (signs). Random sign vector of the rotation (Section 5: d drawn
  * uniformly from {+1, -1}^n): out[j] = +1 if bit 31 of word j of the stream

@@ -280,6 +280,107 @@ mosaic_status mosaic_masked_matmul(const int8_t* a_dig, int64_t a_pitch, const i
   return MOSAIC_OK;
 }
 
+mosaic_status mosaic_masked_matmul_words(const int8_t* a_dig, int64_t a_pitch, const uint32_t* b, int64_t ldb,
+                                         int64_t M, int64_t N, int64_t K, uint32_t* c, int64_t ldc,
+                                         int32_t accumulate, void* stream) {
+  if (M < 0 || N < 0 || K < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (M == 0 || N == 0) return MOSAIC_OK;
+  if (c == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "c is NULL");
+  if (ldc < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldc < N");
+  if (M > SKINNY_MAX_M) return fail(MOSAIC_ERR_UNSUPPORTED, "A must have at most %lld rows", (long long)SKINNY_MAX_M);
+  mosaic_status st = check_digits(a_dig, a_pitch, M, K, "a_dig");
+  if (st != MOSAIC_OK) return st;
+  if (K > 0) {
+    if (b == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "b is NULL");
+    if (ldb < K) return fail(MOSAIC_ERR_INVALID_ARG, "ldb < K");
+    if (!aligned16(b) || ldb % 4 != 0) return fail(MOSAIC_ERR_UNSUPPORTED, "b must be 16-byte aligned, ldb a multiple of 4");
+  }
+  if (a_pitch > (int64_t(1) << 23) || 4 * ldb > (int64_t(1) << 23))
+    return fail(MOSAIC_ERR_UNSUPPORTED, "row pitch above 8 MiB");
+  GemmLaunch g{};
+  g.a_pitch = a_pitch;
+  g.b_pitch = 4 * ldb;
+  g.M = M;
+  g.N = N;
+  g.c = c;
+  g.ldc = ldc;
+  const int64_t Kp = padded_k(K);
+  int64_t k0 = 0;
+  do {
+    const int64_t kc = (Kp - k0 < MAX_K_CHUNK) ? Kp - k0 : MAX_K_CHUNK;
+    g.a = a_dig + 4 * k0;
+    g.b = (const int8_t*)(b + k0);
+    g.Kp = kc;
+    g.b_last = 16 * ((K - k0 + 3) / 4) < 4 * kc ? 16 * ((K - k0 + 3) / 4) : 4 * kc;
+    const EpilogueKind epi = (k0 == 0 && accumulate == 0) ? EPI_STORE : EPI_ACCUM;
+    const mosaic_status ls = hip_status(launch_ring_gemm_words_b(g, epi, (hipStream_t)stream), "ring product launch");
+    if (ls != MOSAIC_OK) return ls;
+    k0 += kc;
+  } while (k0 < Kp);
+  return MOSAIC_OK;
+}
+
+mosaic_status mosaic_integrity_check(const int8_t* ct_dig, int64_t ct_pitch, const int8_t* a_dig, int64_t a_pitch,
+                                     const int8_t* v_dig, int64_t v_pitch, const uint32_t* yq, int64_t ldyq,
+                                     int64_t t, int64_t M, int64_t K, int64_t NR, uint32_t* d, int64_t ldd,
+                                     int64_t* count, void* stream) {
+  if (t < 0 || M < 0 || K < 0 || NR < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (count == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "count is NULL");
+  if (t > SKINNY_MAX_M) return fail(MOSAIC_ERR_UNSUPPORTED, "at most %lld check vectors", (long long)SKINNY_MAX_M);
+  const bool work = t > 0 && M > 0;
+  if (work) {
+    if (d == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "d is NULL");
+    if (ldd < M) return fail(MOSAIC_ERR_INVALID_ARG, "ldd < M");
+    mosaic_status st = check_digits(ct_dig, ct_pitch, t, K, "ct_dig");
+    if (st == MOSAIC_OK) st = check_digits(a_dig, a_pitch, M, K, "a_dig");
+    if (st == MOSAIC_OK) st = check_digits(v_dig, v_pitch, t, NR, "v_dig");
+    if (st != MOSAIC_OK) return st;
+    if (NR > 0) {
+      if (yq == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "yq is NULL");
+      if (ldyq < NR) return fail(MOSAIC_ERR_INVALID_ARG, "ldyq < NR");
+      if (!aligned16(yq) || ldyq % 4 != 0)
+        return fail(MOSAIC_ERR_UNSUPPORTED, "yq must be 16-byte aligned, ldyq a multiple of 4");
+    }
+    if (ct_pitch > (int64_t(1) << 23) || a_pitch > (int64_t(1) << 23) || v_pitch > (int64_t(1) << 23) ||
+        4 * ldyq > (int64_t(1) << 23))
+      return fail(MOSAIC_ERR_UNSUPPORTED, "row pitch above 8 MiB");
+  }
+  const hipStream_t s = (hipStream_t)stream;
+  mosaic_status st = hip_status(launch_clear_check(d, ldd, work ? t : 0, work ? M : 0, count, s), "check clear launch");
+  if (st != MOSAIC_OK || !work) return st;
+  GemmLaunch g{};
+  g.M = t;
+  g.N = M;
+  g.c = d;
+  g.ldc = ldd;
+  // d += c^T A'^T, in inner chunks that fit the accumulators
+  g.a_pitch = ct_pitch;
+  g.b_pitch = a_pitch;
+  const int64_t Kp = padded_k(K);
+  for (int64_t k0 = 0; k0 < Kp; k0 += MAX_K_CHUNK) {
+    g.a = ct_dig + 4 * k0;
+    g.b = a_dig + 4 * k0;
+    g.Kp = (Kp - k0 < MAX_K_CHUNK) ? Kp - k0 : MAX_K_CHUNK;
+    st = hip_status(launch_ring_gemm(g, EPI_ACCUM, s), "check product launch");
+    if (st != MOSAIC_OK) return st;
+  }
+  // d -= V [Y' | Q]^T, B read as ring words
+  g.negate = true;
+  g.a_pitch = v_pitch;
+  g.b_pitch = 4 * ldyq;
+  const int64_t NRp = padded_k(NR);
+  for (int64_t k0 = 0; k0 < NRp; k0 += MAX_K_CHUNK) {
+    const int64_t kc = (NRp - k0 < MAX_K_CHUNK) ? NRp - k0 : MAX_K_CHUNK;
+    g.a = v_dig + 4 * k0;
+    g.b = (const int8_t*)(yq + k0);
+    g.Kp = kc;
+    g.b_last = 16 * ((NR - k0 + 3) / 4) < 4 * kc ? 16 * ((NR - k0 + 3) / 4) : 4 * kc;
+    st = hip_status(launch_ring_gemm_words_b(g, EPI_ACCUM, s), "check product launch");
+    if (st != MOSAIC_OK) return st;
+  }
+  return hip_status(launch_count_mismatches(d, ldd, nullptr, 0, t, M, count, s, false), "check count launch");
+}
+
 mosaic_status mosaic_rotate_quantize_mask(const float* x, int64_t ldx, int64_t rows, int64_t n, int64_t block,
                                           const int8_t* signs, int32_t qmax, const uint32_t* u, int64_t ldu,
                                           const mosaic_rng* noise, int8_t* out_dig, int64_t dig_pitch,

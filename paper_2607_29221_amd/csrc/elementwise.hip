@@ -213,27 +213,36 @@ __global__ __launch_bounds__(256) void signs_kernel(RngArgs r, int64_t n, int8_t
     if (e0 + q < n) out[e0 + q] = (ww[q] >> 31) ? (int8_t)-1 : (int8_t)1;
 }
 
-// One workgroup of 1024 threads counts differing entries: each thread scans
-// a strided share of the elements, then wave shuffles and one LDS word per
-// wave reduce the counts, and thread 0 writes the total.
-__global__ __launch_bounds__(1024) void count_mismatches_kernel(const uint32_t* a, int64_t lda, const uint32_t* b,
-                                                                int64_t ldb, int64_t rows, int64_t cols,
-                                                                int64_t* count) {
-  __shared__ unsigned long long part[16];
-  unsigned long long n = 0;
-  const int64_t total = rows * cols;
-  for (int64_t e = threadIdx.x; e < total; e += 1024) {
-    const int64_t i = e / cols, j = e - i * cols;
-    n += (a[i * lda + j] != b[i * ldb + j]) ? 1ull : 0ull;
+// count = 0, ahead of the workgroups that add their partial counts.
+__global__ void zero_count_kernel(int64_t* count) { *count = 0; }
+
+// Differing entries of two rows x cols matrices (b null: nonzero entries
+// of a): each thread compares
+// 4-column groups (grid-stride), a wave and then the workgroup sum their
+// counts, and one atomic per workgroup adds the sum to count.
+__global__ __launch_bounds__(256) void count_mismatches_kernel(const uint32_t* a, int64_t lda, const uint32_t* b,
+                                                               int64_t ldb, int64_t rows, int64_t cols,
+                                                               int64_t* count) {
+  __shared__ unsigned part[4];
+  unsigned n = 0;
+  const int64_t per_row = (cols + 3) / 4;
+  const int64_t groups = rows * per_row;
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < groups; q += (int64_t)gridDim.x * 256) {
+    const int64_t i = q / per_row;
+    const int64_t j = (q - i * per_row) * 4;
+    const uint32_t* ar = a + i * lda + j;
+    const uint32_t* br = b != nullptr ? b + i * ldb + j : nullptr;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (j + c < cols) n += ar[c] != (b != nullptr ? br[c] : 0u) ? 1u : 0u;
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) n += __shfl_xor(n, off);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = n;
   __syncthreads();
   if (threadIdx.x == 0) {
-    unsigned long long t = 0;
-    for (int w = 0; w < 16; ++w) t += part[w];
-    *count = (int64_t)t;
+    const unsigned t = part[0] + part[1] + part[2] + part[3];
+    if (t != 0) atomicAdd((unsigned long long*)count, (unsigned long long)t);
   }
 }
 
@@ -291,8 +300,15 @@ hipError_t launch_signs(const RngArgs& r, int64_t n, int8_t* out, hipStream_t s)
 }
 
 hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb, int64_t rows,
-                                   int64_t cols, int64_t* count, hipStream_t s) {
-  hipLaunchKernelGGL(count_mismatches_kernel, dim3(1), dim3(1024), 0, s, a, lda, b, ldb, rows, cols, count);
+                                   int64_t cols, int64_t* count, hipStream_t s, bool clear_count) {
+  if (clear_count) hipLaunchKernelGGL(zero_count_kernel, dim3(1), dim3(1), 0, s, count);
+  const int64_t groups = rows * ((cols + 3) / 4);
+  if (groups == 0) return hipGetLastError();
+  // about 2 groups per thread, at most 1024 workgroups
+  int64_t grid = (groups + 511) / 512;
+  if (grid > 1024) grid = 1024;
+  hipLaunchKernelGGL(count_mismatches_kernel, dim3((unsigned)grid), dim3(256), 0, s, a, lda, b, ldb, rows, cols,
+                     count);
   return hipGetLastError();
 }
 

@@ -54,8 +54,11 @@ hipError_t launch_weighted_csr_fill(const RngArgs& r, int64_t rows, int64_t cols
 
 hipError_t launch_mfma_probe(int mode, int64_t iters, int32_t* out, int64_t* ops, hipStream_t s);
 
+// count = #{(i, j) : a(i, j) != b(i, j)}, or != 0 when b is null; with
+// clear_count false the entries are added to a count some earlier launch on
+// the stream has cleared.
 hipError_t launch_count_mismatches(const uint32_t* a, int64_t lda, const uint32_t* b, int64_t ldb, int64_t rows,
-                                   int64_t cols, int64_t* count, hipStream_t s);
+                                   int64_t cols, int64_t* count, hipStream_t s, bool clear_count = true);
 
 // Ring product C = A B^T with an epilogue.
 // EPI_ACCUM adds the product to c (c += A B^T over the ring): long inner
@@ -71,6 +74,11 @@ struct GemmLaunch {
   const int8_t* b;
   int64_t b_pitch;
   int64_t M, N, Kp;       // Kp: K padded to 64
+  // B given as ring words: bytes of B's last row that may be read from
+  // b (its valid words from b on, rounded up to 16 bytes)
+  int64_t b_last;
+  // decode kernel, EPI_ACCUM: subtract the product from c instead of adding
+  bool negate;
   // EPI_STORE
   uint32_t* c;
   int64_t ldc;
@@ -109,6 +117,12 @@ inline int compute_units() {
   return v;
 }
 hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStream_t s);
+// C = A B^T for A of at most SKINNY_MAX_M rows (digits) and B given as ring
+// words (b = first word, b_pitch = row pitch in bytes, a multiple of 16);
+// EPI_STORE or EPI_ACCUM.
+hipError_t launch_ring_gemm_words_b(const GemmLaunch& g, EpilogueKind epi, hipStream_t s);
+// d = 0 (rows x cols, leading dimension ldd) and *count = 0 in one launch.
+hipError_t launch_clear_check(uint32_t* d, int64_t ldd, int64_t rows, int64_t cols, int64_t* count, hipStream_t s);
 
 // Writes one recombined ring value of C = A B^T at (m, n) through the
 // epilogue: EPI_STORE stores it; EPI_UNMASK forms y = ym - val - kc and

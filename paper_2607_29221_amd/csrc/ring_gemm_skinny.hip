@@ -111,7 +111,16 @@ __device__ __forceinline__ void wait_vm() {
 // tiles x stages (column tile, stage) pairs, tile-major, with WM x 4 waves:
 // wave (wm, wn) multiplies A row tiles wm MT / WM .. +MT / WM with B row tiles
 // 2 wn, 2 wn + 1 of the column tile. K must be non-zero.
-template <int MT, int WM>
+// BW: B arrives as ring words (row pitch b_pitch bytes) instead of digits. A
+// stage's 64 words of a row occupy 256 bytes, the size of its digit row, so
+// the direct loads and the fragment reads are unchanged: the four 16-byte
+// slots a lane reads for a B tile hold the 16 words of one column group,
+// and the lane turns them into that group's four digit planes in registers.
+// Columns past K read whatever follows in B's rows;
+// A's zero digits there cancel them. The stage offset then travels in the
+// per-lane offset, which the buffer range check covers, and the range ends
+// b_last bytes into B's last row, so that no load leaves the words B holds.
+template <int MT, int WM, bool BW = false>
 __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(GemmLaunch g, int64_t units) {
   constexpr int NW = WM * SA_WN;
   constexpr int MTW = MT / WM;                     // A row tiles per wave
@@ -155,13 +164,17 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
   auto fetch = [&](int slot) {
     const int64_t n0 = lt * SA_BN;
     const int64_t rows_b = (g.N - n0) < SA_BN ? (g.N - n0) : SA_BN;
-    const v4i rsb = make_rsrc(g.b + n0 * g.b_pitch, rows_b * g.b_pitch);
+    const int64_t bbytes = BW ? (rows_b - 1) * g.b_pitch + g.b_last : rows_b * g.b_pitch;
+    const v4i rsb = make_rsrc(g.b + n0 * g.b_pitch, bbytes);
     const int soff = (int)lst * ROWB;
     const uint32_t base = lds0 + (uint32_t)slot * STG;
 #pragma unroll
     for (int q = 0; q < QA; ++q) dma16(rsa, base + (wave * 4 * QA + 4 * q) * ROWB, va[q], soff);
 #pragma unroll
-    for (int q = 0; q < QB; ++q) dma16(rsb, base + ASZ + (wave * 4 * QB + 4 * q) * ROWB, vb[q], soff);
+    for (int q = 0; q < QB; ++q) {
+      if (BW) dma16(rsb, base + ASZ + (wave * 4 * QB + 4 * q) * ROWB, vb[q] + soff, 0);
+      else dma16(rsb, base + ASZ + (wave * 4 * QB + 4 * q) * ROWB, vb[q], soff);
+    }
     if (++lst == stages) {
       lst = 0;
       ++lt;
@@ -206,6 +219,25 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
     for (int j = 0; j < SA_NTW; ++j)
 #pragma unroll
       for (int t = 0; t < 4; ++t) fb[j][t] = *(const v4i*)(sb + j * 16 * ROWB + fo[t]);
+    if (BW) {
+      // the four slots a lane reads hold the 16 words of its column group;
+      // turn them into the group's four digit planes in registers
+#pragma unroll
+      for (int j = 0; j < SA_NTW; ++j) {
+        uint32_t pl[4][4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t w4[4] = {digit_word((uint32_t)fb[j][c][0]), digit_word((uint32_t)fb[j][c][1]),
+                                  digit_word((uint32_t)fb[j][c][2]), digit_word((uint32_t)fb[j][c][3])};
+          uint32_t p4[4];
+          digit_transpose4(w4, p4);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) pl[t][c] = p4[t];
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) fb[j][t] = v4i{(int)pl[t][0], (int)pl[t][1], (int)pl[t][2], (int)pl[t][3]};
+      }
+    }
 #pragma unroll
     for (int i = 0; i < MTW; ++i)
 #pragma unroll
@@ -235,7 +267,7 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
                                  ((uint32_t)acc[i][j][2][v] << 16) + ((uint32_t)acc[i][j][3][v] << 24);
             const int64_t m = (wm * MTW + i) * 16 + 4 * h + v;
             const int64_t n = n0 + j * 16 + r;
-            if (m < g.M && n < g.N) atomicAdd(&g.c[m * g.ldc + n], val);
+            if (m < g.M && n < g.N) atomicAdd(&g.c[m * g.ldc + n], g.negate ? 0u - val : val);
 #pragma unroll
             for (int c = 0; c < 4; ++c) acc[i][j][c][v] = 0;
           }
@@ -408,7 +440,9 @@ __global__ __launch_bounds__(64 * W) void ring_gemm_skinny_unmask_kernel(GemmLau
 // Zeroes the M x N words at c (leading dimension ldc): block (x, y) covers
 // columns 1024 x .. 1024 x + 1023 of rows y, y + gridDim.y, ...; each thread
 // four consecutive words, one 16-byte store where the row allows it.
-__global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, int64_t M, int64_t N) {
+__global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, int64_t M, int64_t N,
+                                                      int64_t* zero) {
+  if (zero != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *zero = 0;
   const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (j >= N) return;
   for (int64_t row = blockIdx.y; row < M; row += gridDim.y) {
@@ -421,22 +455,23 @@ __global__ __launch_bounds__(256) void clear_c_kernel(uint32_t* c, int64_t ldc, 
   }
 }
 
-void launch_clear_c(uint32_t* c, int64_t ldc, int64_t M, int64_t N, hipStream_t s) {
+void launch_clear_c(uint32_t* c, int64_t ldc, int64_t M, int64_t N, hipStream_t s, int64_t* zero = nullptr) {
   if (M <= 0 || N <= 0) return;
   const dim3 grid((unsigned)((N + 1023) / 1024), (unsigned)(M < 65535 ? M : 65535));
-  hipLaunchKernelGGL(clear_c_kernel, grid, dim3(256), 0, s, c, ldc, M, N);
+  hipLaunchKernelGGL(clear_c_kernel, grid, dim3(256), 0, s, c, ldc, M, N, zero);
 }
 
 // Store and accumulate: the (tile, stage) units cut into one range per
 // compute unit (at least 2 units each); a plain store clears C first.
-template <int MT, int WM>
+template <int MT, int WM, bool BW = false>
 hipError_t launch_shared_a(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
   const int64_t tiles = (g.N + SA_BN - 1) / SA_BN;
   const int64_t units = tiles * (g.Kp / 64);
   const int64_t cus = compute_units();
   const int64_t grid = cus < (units + 1) / 2 ? cus : (units + 1) / 2;
   if (epi == EPI_STORE) launch_clear_c(g.c, g.ldc, g.M, g.N, s);
-  hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, WM>), dim3((unsigned)grid), dim3(64 * WM * SA_WN), 0, s, g, units);
+  hipLaunchKernelGGL((ring_gemm_skinny_kernel<MT, WM, BW>), dim3((unsigned)grid), dim3(64 * WM * SA_WN), 0, s, g,
+                     units);
   return hipGetLastError();
 }
 
@@ -483,6 +518,27 @@ hipError_t launch_unmask(const GemmLaunch& g, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_ring_gemm_words_b(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.Kp == 0) {
+    if (epi == EPI_STORE) launch_clear_c(g.c, g.ldc, g.M, g.N, s);
+    return hipGetLastError();
+  }
+  const int mt = (int)((g.M + 15) / 16);
+  if (mt <= 1) return launch_shared_a<1, 1, true>(g, epi, s);
+  if (mt == 2) return launch_shared_a<2, 2, true>(g, epi, s);
+  return launch_shared_a<4, 2, true>(g, epi, s);
+}
+
+hipError_t launch_clear_check(uint32_t* d, int64_t ldd, int64_t rows, int64_t cols, int64_t* count, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) {
+    hipLaunchKernelGGL(clear_c_kernel, dim3(1), dim3(1), 0, s, d, ldd, int64_t(0), int64_t(0), count);
+    return hipGetLastError();
+  }
+  launch_clear_c(d, ldd, rows, cols, s, count);
+  return hipGetLastError();
+}
 
 hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;

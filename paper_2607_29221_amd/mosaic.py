@@ -192,6 +192,34 @@ def mosaic_masked_matmul(a: Digits, b: Digits, M: int, N: int, K: int, c: torch.
                                             c.stride(0), _stream()), "mosaic_masked_matmul")
 
 
+def mosaic_masked_matmul_words(a: Digits, b: torch.Tensor, M: int, N: int, K: int, c: torch.Tensor,
+                               accumulate: bool = False) -> None:
+    """c[:M, :N] (+)= A B^T over Z_{2^32} with B (N x K) given as ring words
+    (an int32 tensor); A has at most 64 rows."""
+    _need_dig(a, M, K, "a", optional=False)
+    _need(b, N, K, "b", _INT, optional=False)
+    _need(c, M, N, "c", _INT, optional=False)
+    _check(_lib.load().mosaic_masked_matmul_words(a.ptr, a.pitch, b.data_ptr(), b.stride(0), M, N, K, c.data_ptr(),
+                                                  c.stride(0), 1 if accumulate else 0, _stream()),
+           "mosaic_masked_matmul_words")
+
+
+def mosaic_integrity_check(ct: Digits, a: Digits, v: Digits, yq: torch.Tensor, t: int, M: int, K: int, NR: int,
+                           d: torch.Tensor, count: torch.Tensor) -> None:
+    """d = c^T A'^T - V [Y' | Q]^T (t x M) and count[0] = its nonzero entries,
+    with [Y' | Q] given as the ring words of yq's first NR columns."""
+    _need_dig(ct, t, K, "ct", optional=False)
+    _need_dig(a, M, K, "a", optional=False)
+    _need_dig(v, t, NR, "v", optional=False)
+    _need(yq, M, NR, "yq", _INT, optional=False)
+    _need(d, t, M, "d", _INT, optional=False)
+    if count.dtype != torch.int64 or count.numel() < 1 or not count.is_cuda:
+        raise ValueError("count must be an int64 device tensor")
+    _check(_lib.load().mosaic_integrity_check(ct.ptr, ct.pitch, a.ptr, a.pitch, v.ptr, v.pitch, yq.data_ptr(),
+                                              yq.stride(0), t, M, K, NR, d.data_ptr(), d.stride(0),
+                                              count.data_ptr(), _stream()), "mosaic_integrity_check")
+
+
 def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digits], l: Optional[Digits],
                   M: int, N: int, R: int, y: Optional[torch.Tensor] = None,
                   s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,

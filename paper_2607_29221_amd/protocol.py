@@ -194,13 +194,22 @@ class MaskedWeight:
         self.t = int(check_vectors)
         if self.t > 0:
             t = self.t
-            self.aW = Digits.empty(t, N, dev)
+            if N % 64 == 0:
+                # [a_W | a_Q] in one buffer whose columns line up with [Y' | Q]
+                cat = Digits.concat(t, [N] + self.slot_ranks, dev)
+                self.aW, self.aQ = cat[0], cat[1:]
+                self.aWQ: Optional[Digits] = Digits(cat[0].buf, N + self.R, 0)
+                self.aQ_all = Digits(cat[0].buf, self.R, N)
+            else:
+                self.aW = Digits.empty(t, N, dev)
+                self.aQ = Digits.concat(t, self.slot_ranks, dev)
+                self.aWQ = None
+                self.aQ_all = self.aQ[0].whole(self.R)
             m.mosaic_sample(m.rng(s, STREAM_CHECK_W, weight_id, U), t, N, out_dig=self.aW)
-            self.aQ = Digits.concat(t, self.slot_ranks, dev)
             for slot, lv in enumerate(self.slot_levels):
                 m.mosaic_sample(m.rng(s, STREAM_CHECK_Q + lv, weight_id, U), t, r[lv - 1], out_dig=self.aQ[slot])
             key_q = _ring_empty(t, K, dev)          # sum_i a_i Mc_i = aQcat McTcat^T
-            m.mosaic_masked_matmul(self.aQ[0].whole(self.R), McTcat[0].whole(self.R), t, K, self.R, key_q)
+            m.mosaic_masked_matmul(self.aQ_all, McTcat[0].whole(self.R), t, K, self.R, key_q)
 
         # U_w = Lcat McTcat^T (= L Mc_d + sum S_{i+1} Mc_i); W' = W + U_w + E_w
         U_w = _ring_empty(N, K, dev)
@@ -265,7 +274,8 @@ class CallBuffers:
     YQ: torch.Tensor           # [Y' | Q], M x (N + R)
     Qdig: List[Digits]         # Q slots in digit layout, M x R
     Y: torch.Tensor            # unmasked output, M x N int32
-    check: Optional[tuple] = None   # (lhs, rhs) of the last integrity check
+    check: Optional[tuple] = None   # (lhs, rhs) of the last integrity check formed side by side
+    check_diff: Optional[torch.Tensor] = None   # lhs - rhs of the last check in one call
 
 
 def alloc_call(w: MaskedWeight, M: int, device="cuda") -> CallBuffers:
@@ -335,28 +345,51 @@ def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tens
         m.mosaic_unmask(buf.Y, None, None, None, M, w.N, 0, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
 
 
-def verify(w: MaskedWeight, M: int, buf: CallBuffers) -> torch.Tensor:
-    """Online step 4 (Freivalds' test) on the server's [Y' | Q]: forms
-    lhs = c^T A'^T and rhs = a_W Y'^T^T + a_Q Q^T^T (both t x M, on the masked
+def verify(w: MaskedWeight, M: int, buf: CallBuffers, sides: bool = False) -> torch.Tensor:
+    """Online step 4 (Freivalds' test) on the server's [Y' | Q]: compares
+    lhs = c^T A'^T with rhs = a_W Y'^T + a_Q Q^T (both t x M, on the masked
     activations A' the server multiplied) and returns a one-element int64
     device tensor with the number of entries where they differ: 0 accepts
-    the call. Work O((K + N + R) M t), against M K (N + R) for the product."""
+    the call. Work O((K + N + R) M t), against M K (N + R) for the product.
+
+    When N is a multiple of 64 (a_W and a_Q then sit side by side like Y'
+    and Q) and t <= 64, one library call forms d = lhs - rhs, reading
+    [Y' | Q] as ring words, and counts its nonzero entries (d is kept in
+    buf.check_diff). Otherwise, or with ``sides``, both sides are formed
+    and kept in buf.check: rhs from the ring words in two products when N is
+    a multiple of 4, else through digit copies of Y' and Q."""
     if w.t <= 0:
         raise ValueError("the weight was prepared without check vectors")
     dev = buf.YQ.device
     t = w.t
+    if w.aWQ is not None and t <= 64 and not sides:
+        d = _ring_empty(t, M, dev)
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+        m.mosaic_integrity_check(w.cT, buf.A_masked, w.aWQ, buf.YQ, t, M, w.K, w.N + w.R, d, count)
+        buf.check_diff = d
+        return count
+    lhs = _ring_empty(t, M, dev)
+    m.mosaic_masked_matmul(w.cT, buf.A_masked, t, M, w.K, lhs)
+    if w.N % 4 == 0 and t <= 64:
+        # straight from the server's ring words (one read of [Y' | Q]; Q's
+        # padding columns are zero, as are a_Q's digits there)
+        rhs = _ring_empty(t, M, dev)
+        m.mosaic_masked_matmul_words(w.aW, buf.YQ[:, : w.N], t, M, w.N, rhs)
+        m.mosaic_masked_matmul_words(w.aQ_all, buf.YQ[:, w.N: w.N + w.R], t, M, w.R, rhs, accumulate=True)
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+        m.mosaic_count_mismatches(lhs, rhs, count)
+        buf.check = (lhs, rhs)
+        return count
     Ydig = Digits.empty(M, w.N, dev)
     m.mosaic_mask(None, buf.YQ[:, : w.N], None, M, w.N, out_dig=Ydig)
     r = list(w.params.ranks)
     for slot, lv in enumerate(w.slot_levels):
         c0 = w.q_cols[slot]
         m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
-    lhs = _ring_empty(t, M, dev)
-    m.mosaic_masked_matmul(w.cT, buf.A_masked, t, M, w.K, lhs)
     ry = _ring_empty(t, M, dev)
     m.mosaic_masked_matmul(w.aW, Ydig, t, M, w.N, ry)
     rq = _ring_empty(t, M, dev)
-    m.mosaic_masked_matmul(w.aQ[0].whole(w.R), buf.Qdig[0].whole(w.R), t, M, w.R, rq)
+    m.mosaic_masked_matmul(w.aQ_all, buf.Qdig[0].whole(w.R), t, M, w.R, rq)
     rhs = _ring_empty(t, M, dev)
     m.mosaic_mask(ry, rq, None, t, M, out=rhs)
     count = torch.empty(1, dtype=torch.int64, device=dev)

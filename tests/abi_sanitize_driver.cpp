@@ -73,6 +73,26 @@ int main() {
   EXPECT(mosaic_masked_matmul(Fd, int64_t(1) << 24, Fd, 256, 4, 4, 64, Fu, 4, nullptr), UNS);
   EXPECT(mosaic_masked_matmul(Fd, 256, Fd, 256, -1, 4, 64, Fu, 4, nullptr), INV);
   EXPECT(mosaic_masked_matmul(Fd, 256, Fd, 256, 0, 4, 64, Fu, 4, nullptr), OK);
+  EXPECT(mosaic_masked_matmul_words(Fd, 256, Fu, 64, 65, 4, 64, Fu, 4, 0, nullptr), UNS);     // M > 64
+  EXPECT(mosaic_masked_matmul_words(Fd, 256, Fu, 63, 4, 4, 64, Fu, 4, 0, nullptr), INV);      // ldb < K
+  EXPECT(mosaic_masked_matmul_words(Fd, 256, Fu, 66, 4, 4, 64, Fu, 4, 0, nullptr), UNS);      // ldb % 4
+  EXPECT(mosaic_masked_matmul_words(Fd, 256, Fu + 1, 64, 4, 4, 64, Fu, 4, 0, nullptr), UNS);  // alignment
+  EXPECT(mosaic_masked_matmul_words(Fd, 256, nullptr, 64, 4, 4, 64, Fu, 4, 0, nullptr), INV);
+  EXPECT(mosaic_masked_matmul_words(Fd, 256, Fu, 64, 4, 4, 64, nullptr, 4, 0, nullptr), INV);
+  int64_t* Fc = (int64_t*)F;
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu, 64, 4, 4, 64, 64, Fu, 4, nullptr, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu, 64, 65, 4, 64, 64, Fu, 4, Fc, nullptr), UNS);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu, 64, 4, -1, 64, 64, Fu, 4, Fc, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu, 64, 4, 4, 64, 64, nullptr, 4, Fc, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu, 64, 4, 4, 64, 64, Fu, 3, Fc, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd + 1, 256, Fd, 256, Fd, 256, Fu, 64, 4, 4, 64, 64, Fu, 4, Fc, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 192, Fd, 256, Fu, 64, 4, 4, 64, 64, Fu, 4, Fc, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, nullptr, 64, 4, 4, 64, 64, Fu, 4, Fc, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu, 60, 4, 4, 64, 64, Fu, 4, Fc, nullptr), INV);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu + 1, 64, 4, 4, 64, 64, Fu, 4, Fc, nullptr), UNS);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, 256, Fd, 256, Fu, 66, 4, 4, 64, 64, Fu, 4, Fc, nullptr), UNS);
+  EXPECT(mosaic_integrity_check(Fd, 256, Fd, int64_t(1) << 24, Fd, 256, Fu, 64, 4, 4, 64, 64, Fu, 4, Fc, nullptr),
+         UNS);
   EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 32768, (int32_t*)F, 4, nullptr, nullptr,
                        nullptr, 0, nullptr), UNS);
   EXPECT(mosaic_unmask(nullptr, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr,

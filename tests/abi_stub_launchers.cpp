@@ -26,9 +26,11 @@ hipError_t launch_weighted_csr_fill(const RngArgs&, int64_t, int64_t, const int6
                                     hipStream_t) STUB
 hipError_t launch_mfma_probe(int, int64_t, int32_t*, int64_t*, hipStream_t) STUB
 hipError_t launch_count_mismatches(const uint32_t*, int64_t, const uint32_t*, int64_t, int64_t, int64_t, int64_t*,
-                                   hipStream_t) STUB
+                                   hipStream_t, bool) STUB
+hipError_t launch_clear_check(uint32_t*, int64_t, int64_t, int64_t, int64_t*, hipStream_t) STUB
 hipError_t launch_ring_gemm(const GemmLaunch&, EpilogueKind, hipStream_t) STUB
 hipError_t launch_ring_gemm_skinny(const GemmLaunch&, EpilogueKind, hipStream_t) STUB
+hipError_t launch_ring_gemm_words_b(const GemmLaunch&, EpilogueKind, hipStream_t) STUB
 hipError_t launch_unmask_elementwise(const GemmLaunch&, hipStream_t) STUB
 hipError_t launch_hadamard(const float*, int64_t, float*, int64_t, int64_t, int64_t, int, const int8_t*, int,
                            hipStream_t) STUB

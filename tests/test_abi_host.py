@@ -164,6 +164,25 @@ def test_count_mismatches_validation(lib):
 
 
 @cpu_only
+def test_integrity_check_validation(lib):
+    def call(ct=FAKE, a=FAKE, a_pitch=256, v=FAKE, yq=FAKE, ldyq=64, t=4, M=4, K=64, NR=64, d=FAKE, ldd=4,
+             count=FAKE):
+        return lib.mosaic_integrity_check(ct, 256, a, a_pitch, v, 256, yq, ldyq, t, M, K, NR, d, ldd, count, None)
+    assert call(count=None) == INVALID
+    assert call(t=65) == UNSUPPORTED
+    assert call(M=-1) == INVALID
+    assert call(d=None) == INVALID
+    assert call(ldd=3) == INVALID
+    assert call(ct=FAKE + 1) == INVALID
+    assert call(a_pitch=192) == INVALID
+    assert call(yq=None) == INVALID
+    assert call(ldyq=60) == INVALID
+    assert call(yq=FAKE + 4) == UNSUPPORTED
+    assert call(ldyq=66) == UNSUPPORTED
+    assert call(a_pitch=1 << 24) == UNSUPPORTED
+
+
+@cpu_only
 def test_hadamard_validation(lib):
     def call(x=FAKE, ldx=64, y=FAKE + (1 << 24), ldy=64, rows=2, n=64, block=64, signs=None, inv=0):
         return lib.mosaic_hadamard_rotate(x, ldx, y, ldy, rows, n, block, signs, inv, None)

@@ -10,7 +10,7 @@ from oracle import integrity as integ
 from oracle import protocol as oproto
 from paper_2607_29221_amd import protocol as gproto
 from synthetic_inputs import (PARAMS_D1_SMALL_R128, PARAMS_D2_SPARSE, PARAMS_D3_SPARSE_SMALL, PARAMS_PAPER_D1,
-                              PREFILL_SEED, int8_operands)
+                              PREFILL_KN, PREFILL_SEED, int8_operands)
 from tests.gpu_util import to_np_u32
 
 pytestmark = pytest.mark.gpu
@@ -25,23 +25,68 @@ def _add_host(t: torch.Tensor, i: int, j: int, delta: int) -> None:
 
 
 @pytest.mark.parametrize("name", ["d1", "d2", "d3"])
-def test_check_sides_match_oracle(name):
+@pytest.mark.parametrize("N", [512, 516, 510], ids=["one-call", "words", "digit-copies"])
+def test_check_sides_match_oracle(name, N):
+    """Both sides of the check against the oracle, with rhs formed from
+    [Y' | Q] as ring words (N a multiple of 4) or through digit copies
+    (N = 510); at N = 512 the one-call check (d = lhs - rhs) is also run and
+    must return an all-zero d."""
     p = PARAMS[name]
-    A, W = int8_operands(64, 512, 512, 0)
+    A, W = int8_operands(64, 512, N, 0)
     seed, t = 4321, 8
     w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), p, seed, weight_id=2, check_vectors=t)
     buf = gproto.run_call(w, torch.from_numpy(A).cuda(), call_id=9)
-    count = gproto.verify(w, 64, buf)
+    count = gproto.verify(w, 64, buf, sides=True)
     torch.cuda.synchronize()
     assert int(count.item()) == 0
     res = oproto.run(A, W, p, seed, weight_id=2, call_id=9)
-    aW, aQ = integ.check_vectors(t, 512, list(p.ranks), seed, 2)
+    aW, aQ = integ.check_vectors(t, N, list(p.ranks), seed, 2)
     cT = integ.key(aW, aQ, res.ws.W_masked, {i + 1: mc for i, mc in enumerate(res.ws.Mc)})
     lhs, rhs = integ.sides(cT, aW, aQ, res.X_masked.T, res.Y_masked.T.copy(),
                            {i + 1: q.T.copy() for i, q in enumerate(res.Q)})
     assert np.array_equal(to_np_u32(buf.check[0]), lhs)
     assert np.array_equal(to_np_u32(buf.check[1]), rhs)
     assert np.array_equal(lhs, rhs)
+    if N % 64 == 0:
+        assert int(gproto.verify(w, 64, buf).item()) == 0
+        assert not np.any(to_np_u32(buf.check_diff))
+
+
+def _check_column_vectors(w, aW, aQ, col):
+    """The check vectors' column that multiplies column col of [Y' | Q]."""
+    if col < w.N:
+        return aW[:, col]
+    for slot, lv in enumerate(w.slot_levels):
+        c0 = w.q_cols[slot]
+        if c0 <= col < c0 + aQ[lv].shape[1]:
+            return aQ[lv][:, col - c0]
+    return np.zeros(aW.shape[0], dtype=np.uint32)           # a padding column of Q
+
+
+@pytest.mark.parametrize("name", ["d1", "d2", "d3"])
+def test_check_difference_matches_oracle(name):
+    """The one-call check after several outputs were changed: d equals, for
+    every (vector, token), minus the sum over that token's changed columns of
+    the vector's entry times the change, computed from the oracle's check
+    vectors; count is the number of nonzero entries of d."""
+    p = PARAMS[name]
+    A, W = int8_operands(64, 512, 512, 1)
+    seed, t = 555, 12
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), p, seed, weight_id=3, check_vectors=t)
+    buf = gproto.run_call(w, torch.from_numpy(A).cuda(), call_id=4)
+    torch.cuda.synchronize()
+    aW, aQ = integ.check_vectors(t, 512, list(p.ranks), seed, 3)
+    last = w.q_cols[-1]
+    changes = [(5, 17, 1), (5, 512 + 3, 0x12345), (40, 511, 1 << 31), (63, last, 7), (63, 0, 2 ** 32 - 7)]
+    expect = np.zeros((t, 64), dtype=np.uint64)
+    for i, col, delta in changes:
+        _add_host(buf.YQ, i, col, delta)
+        a = _check_column_vectors(w, aW, aQ, col).astype(np.uint64)
+        expect[:, i] = (expect[:, i] + (2 ** 32 - (a * delta) % 2 ** 32)) % 2 ** 32
+    got = int(gproto.verify(w, 64, buf).item())
+    d = to_np_u32(buf.check_diff)
+    assert np.array_equal(d, expect.astype(np.uint32))
+    assert got == int(np.count_nonzero(expect)) > 0
 
 
 @pytest.mark.parametrize("delta", [1, 0x10000, 1 << 31])
@@ -76,17 +121,73 @@ def test_corrupted_outputs_detected(delta):
     assert got == expect
 
 
-def test_full_size_prefill_check():
-    """M = 2048, K = N = 8192, rank 1536, 32 check vectors: honest outputs
-    pass, an odd error in one Y' entry is caught by every vector."""
-    K, N, M, t = 8192, 8192, 2048, 32
+@pytest.mark.parametrize("shape_id", range(len(PREFILL_KN)), ids=[f"{k}x{n}" for k, n in PREFILL_KN])
+def test_full_size_prefill_check(shape_id):
+    """M = 2048 at the three prefill shapes, rank 1536, 32 check vectors:
+    honest outputs pass; an odd error in one Y' entry, then in one Q entry,
+    is caught by every vector."""
+    K, N = PREFILL_KN[shape_id]
+    M, t = 2048, 32
     A, W = int8_operands(M, K, N, PREFILL_SEED)
     seed = 0x6D6F736169630000 | PREFILL_SEED
-    print("integrity check at 2048 x 8192 x 8192", flush=True)
-    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), PARAMS_PAPER_D1, seed, weight_id=0, check_vectors=t)
+    print(f"integrity check at 2048 x {K} x {N}", flush=True)
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), PARAMS_PAPER_D1, seed, weight_id=shape_id, check_vectors=t)
     buf = gproto.run_call(w, torch.from_numpy(A).cuda(), call_id=1)
     assert int(gproto.verify(w, M, buf).item()) == 0
-    aW, _ = integ.check_vectors(t, N, [1536], seed, 0)
-    _add_host(buf.YQ, 1000, 4321, 3)
+    aW, aQ = integ.check_vectors(t, N, [1536], seed, shape_id)
+    _add_host(buf.YQ, 1000, N - 7, 3)
     got = int(gproto.verify(w, M, buf).item())
-    assert got == sum(1 for j in range(t) if (int(aW[j, 4321]) * 3) % 2 ** 32 != 0) == t
+    assert got == sum(1 for j in range(t) if (int(aW[j, N - 7]) * 3) % 2 ** 32 != 0) == t
+    _add_host(buf.YQ, 1000, N - 7, 2 ** 32 - 3)                     # undo
+    assert int(gproto.verify(w, M, buf).item()) == 0
+    _add_host(buf.YQ, 2047, w.q_cols[0] + 1535, 5)
+    got = int(gproto.verify(w, M, buf).item())
+    assert got == sum(1 for j in range(t) if (int(aQ[1][j, 1535]) * 5) % 2 ** 32 != 0) == t
+
+
+def test_check_graph_replay():
+    """The check captured in a HIP graph and replayed with the server's
+    outputs changed on the host between replays: each replay's count equals
+    the eager check's on the same outputs."""
+    p = PARAMS_D1_SMALL_R128
+    A, W = int8_operands(64, 512, 512, 5)
+    t = 16
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), p, 99, weight_id=4, check_vectors=t)
+    buf = gproto.run_call(w, torch.from_numpy(A).cuda(), call_id=2)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        count = gproto.verify(w, 64, buf)
+    for rep, (i, j, delta) in enumerate([(0, 0, 0), (7, 300, 1), (7, 300, 2 ** 32 - 1), (63, 512 + 9, 1 << 31)]):
+        if delta:
+            _add_host(buf.YQ, i, j, delta)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = int(count.item())
+        eager = int(gproto.verify(w, 64, buf).item())
+        assert got == eager, rep
+    assert got > 0
+
+
+@pytest.mark.parametrize("rows,cols,ld", [(1, 1, 1), (3, 5, 8), (32, 2048, 2048), (64, 2049, 2051),
+                                          (4096, 4100, 4101)])
+def test_count_mismatches(rows, cols, ld):
+    """Differing entries counted over every element, in one workgroup up to
+    grids that stride (4096 x 4100: more 4-column groups than 1024
+    workgroups of 256 threads cover at once); entries past cols differ in
+    every row and must not be counted. The count starts non-zero."""
+    from paper_2607_29221_amd import mosaic as m
+    rng = np.random.default_rng(rows * 31 + cols)
+    a = rng.integers(0, 2 ** 32, (rows, ld), dtype=np.uint64).astype(np.uint32)
+    b = a.copy()
+    b[:, cols:] ^= 1
+    flip = rng.random((rows, cols)) < 0.01
+    flip[rows - 1, cols - 1] = True
+    b[:, :cols][flip] += np.uint32(1 << 31)
+    da = torch.from_numpy(a.view(np.int32)).cuda()[:, :cols]
+    db = torch.from_numpy(b.view(np.int32)).cuda()[:, :cols]
+    count = torch.full((1,), 12345, dtype=torch.int64, device="cuda")
+    m.mosaic_count_mismatches(da, db, count)
+    torch.cuda.synchronize()
+    assert int(count.item()) == int(flip.sum())

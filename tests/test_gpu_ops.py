@@ -253,6 +253,52 @@ def test_masked_matmul_ldc_and_offsets(M, K):
     assert np.all(got[:, :5] == 12345) and np.all(got[:, 5 + N:] == 12345)
 
 
+def _gemm_words(a_np, b_np, ldb, c0=None, accumulate=False, ldc_extra=0):
+    """C (+)= A B^T with A as digits and B as ring words in the first K
+    columns of an N x ldb buffer whose other columns hold random words."""
+    M, K = a_np.shape
+    N = b_np.shape[0]
+    A = Digits.empty(M, K)
+    m.mosaic_mask(to_dev_ring(a_np), None, None, M, K, out_dig=A)
+    wide = _rng_np(ldb + N).integers(0, 2 ** 32, (N, ldb), dtype=np.uint64).astype(np.uint32)
+    wide[:, :K] = b_np
+    Bw = to_dev_ring(wide)[:, :K]
+    C = to_dev_ring(c0 if c0 is not None else np.full((M, N + ldc_extra), 777, dtype=np.uint32))
+    m.mosaic_masked_matmul_words(A, Bw, M, N, K, C[:, :N], accumulate=accumulate)
+    torch.cuda.synchronize()
+    return to_np_u32(C)
+
+
+@pytest.mark.parametrize("M", [1, 16, 17, 33, 64])
+@pytest.mark.parametrize("N,K,ldb", [(33, 64, 64), (100, 576, 580), (300, 1001, 1008), (2049, 1024, 1024),
+                                     (37, 1, 4), (130, 4161, 4164)])
+def test_masked_matmul_words(M, N, K, ldb):
+    """B read as ring words (the integrity check's operand layout): row
+    counts of one, two and four 16-row tiles, ragged N and K, a leading
+    dimension above K whose extra words are random (A's zero digits past K
+    cancel them), and B's last row ending at its K-th word (ldb = K)."""
+    rng = _rng_np(M * 3 + N * 5 + K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    got = _gemm_words(a, b, ldb, ldc_extra=3)
+    assert np.array_equal(got[:, :N], ring_matmul(a, b.T))
+    assert np.all(got[:, N:] == 777)
+
+
+@pytest.mark.parametrize("M,N,K", [(3, 37, 33000), (64, 20, 65600)])
+def test_masked_matmul_words_long_k_accumulate(M, N, K):
+    """K above one launch's range runs as chunks added into C; with
+    accumulate set, C's prior values are kept and the product added."""
+    rng = _rng_np(M + N + K)
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    c0 = _random_ring(rng, (M, N))
+    got = _gemm_words(a, b, K + (-K) % 4 + 4, c0=c0, accumulate=True)
+    assert np.array_equal(got, (c0.astype(np.uint64) + ring_matmul(a, b.T)).astype(np.uint32))
+    got = _gemm_words(a, b, K + (-K) % 4, c0=c0, accumulate=False)
+    assert np.array_equal(got, ring_matmul(a, b.T))
+
+
 @pytest.mark.parametrize("M,N,R", [(64, 512, 128), (33, 70, 0), (200, 130, 192), (1, 300, 2560), (8, 33, 64),
                                    (200, 132, 192), (130, 256, 64), (257, 4, 128), (1, 4096, 1536),
                                    (1, 4200, 1536), (16, 4111, 320)])
