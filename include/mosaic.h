@@ -193,9 +193,12 @@ mosaic_status mosaic_masked_matmul_words(const int8_t* a_dig, int64_t a_pitch,
  * ym: M x N (ldy); kc: M x N (ldk, NULL means 0); q: M x R digits (q_pitch),
  * l: N x R digits (l_pitch) -- the factors concatenated along R; R may be 0
  * (then q and l are ignored). y: M x N int32 (ldo), the centred lift.
- * Optional dequantisation (Pi_Sec-Linear, online step 3): if y_f32 is not
- * NULL it receives (float)y(i, j) * s_rows[i] * s_cols[j] (ldf); y may then
- * be NULL. An output may coincide with ym or kc element for element (in
+ * Optional dequantisation (Pi_Sec-Linear, online step 3, Section 5 box):
+ * if y_f32 is not NULL it receives (float)y(i, j) * s_rows[i] * s_cols[j]
+ * (ldf; products in that order, each rounded to fp32), plus bias[j] when
+ * bias (N floats) is not NULL, added after the products in one more fp32
+ * rounding; y may then be NULL. bias without y_f32 is
+ * MOSAIC_ERR_INVALID_ARG. An output may coincide with ym or kc element for element (in
  * place, same leading dimension); otherwise outputs and inputs must not
  * overlap. Output memory may hold intermediate values while the call runs
  * (with at most 64 rows, an output that shares no memory with the inputs
@@ -206,7 +209,7 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy,
                             const int8_t* l_dig, int64_t l_pitch,
                             int64_t M, int64_t N, int64_t R,
                             int32_t* y, int64_t ldo,
-                            const float* s_rows, const float* s_cols,
+                            const float* s_rows, const float* s_cols, const float* bias,
                             float* y_f32, int64_t ldf, void* stream);
 
 /* Fused client input pass of Pi_Sec-Linear (Section 5 protocol box, online

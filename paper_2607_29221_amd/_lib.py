@@ -50,7 +50,7 @@ _SIGNATURES = {
     "mosaic_integrity_check": ([c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64,
                                 c_i64, c_ptr, c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_unmask": ([c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64,
-                       c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
+                       c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
     "mosaic_sample_signs": ([ctypes.POINTER(MosaicRng), c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_rotate_quantize_mask": ([c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr, c_i64,
                                      ctypes.POINTER(MosaicRng), c_ptr, c_i64, c_ptr, c_ptr], c_i32),

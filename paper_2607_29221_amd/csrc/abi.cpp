@@ -502,8 +502,8 @@ mosaic_status mosaic_count_mismatches(const uint32_t* a, int64_t lda, const uint
 
 mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy, const uint32_t* kc, int64_t ldk, const int8_t* q_dig,
                             int64_t q_pitch, const int8_t* l_dig, int64_t l_pitch, int64_t M, int64_t N, int64_t R,
-                            int32_t* y, int64_t ldo, const float* s_rows, const float* s_cols, float* y_f32,
-                            int64_t ldf, void* stream) {
+                            int32_t* y, int64_t ldo, const float* s_rows, const float* s_cols, const float* bias,
+                            float* y_f32, int64_t ldf, void* stream) {
   if (M < 0 || N < 0 || R < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
   if (R >= 32768) return fail(MOSAIC_ERR_UNSUPPORTED, "R must be < 32768");
   if (M == 0 || N == 0) return MOSAIC_OK;
@@ -514,6 +514,7 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy, const uint32_t* kc,
   if (y != nullptr && ldo < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldo < N");
   if (y_f32 != nullptr && (ldf < N || s_rows == nullptr || s_cols == nullptr))
     return fail(MOSAIC_ERR_INVALID_ARG, "y_f32 needs ldf >= N and both scale vectors");
+  if (bias != nullptr && y_f32 == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "bias needs y_f32");
   GemmLaunch g{};
   g.M = M;
   g.N = N;
@@ -525,6 +526,7 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy, const uint32_t* kc,
   g.ldo = ldo;
   g.s_rows = s_rows;
   g.s_cols = s_cols;
+  g.bias = bias;
   g.y_f32 = y_f32;
   g.ldf = ldf;
   if (R == 0) {

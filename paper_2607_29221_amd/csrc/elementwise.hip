@@ -258,8 +258,10 @@ __global__ __launch_bounds__(256) void unmask_elementwise_kernel(GemmLaunch g) {
   if (g.kc != nullptr) v -= g.kc[i * g.ldk + j];
   if (g.c != nullptr) v -= g.c[i * g.ldc + j];
   if (g.y != nullptr) g.y[i * g.ldo + j] = (int32_t)v;
-  if (g.y_f32 != nullptr)
-    g.y_f32[i * g.ldf + j] = (float)(int32_t)v * g.s_rows[i] * g.s_cols[j];
+  if (g.y_f32 != nullptr) {
+    const float f = (float)(int32_t)v * g.s_rows[i] * g.s_cols[j];
+    g.y_f32[i * g.ldf + j] = g.bias != nullptr ? __fadd_rn(f, g.bias[j]) : f;
+  }
 }
 
 }  // namespace

@@ -92,6 +92,7 @@ struct GemmLaunch {
   int64_t ldo;
   const float* s_rows;
   const float* s_cols;
+  const float* bias;      // optional, N entries, added to y_f32
   float* y_f32;
   int64_t ldf;
 };
@@ -126,7 +127,8 @@ hipError_t launch_clear_check(uint32_t* d, int64_t ldd, int64_t rows, int64_t co
 
 // Writes one recombined ring value of C = A B^T at (m, n) through the
 // epilogue: EPI_STORE stores it; EPI_UNMASK forms y = ym - val - kc and
-// stores it as int32 and/or dequantised fp32.
+// stores it as int32 and/or dequantised fp32 (plus the bias, added after the
+// two scale products with no fused multiply-add).
 template <int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmLaunch& g, int64_t m, int64_t n, uint32_t val) {
   if (EPI == EPI_STORE) {
@@ -137,7 +139,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmLaunch& g, int64_t m, in
     uint32_t y = g.ym[m * g.ldy + n] - val;
     if (g.kc != nullptr) y -= g.kc[m * g.ldk + n];
     if (g.y != nullptr) g.y[m * g.ldo + n] = (int32_t)y;
-    if (g.y_f32 != nullptr) g.y_f32[m * g.ldf + n] = (float)(int32_t)y * g.s_rows[m] * g.s_cols[n];
+    if (g.y_f32 != nullptr) {
+      const float v = (float)(int32_t)y * g.s_rows[m] * g.s_cols[n];
+      g.y_f32[m * g.ldf + n] = g.bias != nullptr ? __fadd_rn(v, g.bias[n]) : v;
+    }
   }
 }
 
@@ -149,7 +154,7 @@ inline bool gemm_epilogue_vectorizable(const GemmLaunch& g, EpilogueKind epi) {
   if (g.N % 4 != 0) return false;
   if (epi == EPI_STORE || epi == EPI_ACCUM) return ok(g.c, g.ldc);
   return ok(g.ym, g.ldy) && ok(g.kc, g.ldk) && ok(g.y, g.ldo) && ok(g.y_f32, g.ldf) &&
-         (g.y_f32 == nullptr || (((uintptr_t)g.s_cols) & 15) == 0);
+         (g.y_f32 == nullptr || ((((uintptr_t)g.s_cols) & 15) == 0 && (((uintptr_t)g.bias) & 15) == 0));
 }
 
 // Epilogue of a TM x TN output tile held in LDS (row pitch TROW words) by a
@@ -211,7 +216,7 @@ __device__ __forceinline__ void gemm_tile_epilogue(const GemmLaunch& g, const ui
   }
   const bool dq = g.y_f32 != nullptr;
   uint4 ymv[PER], kcv[PER];
-  float4 scv[PER];
+  float4 scv[PER], bv[PER];
   float srv[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -223,6 +228,7 @@ __device__ __forceinline__ void gemm_tile_epilogue(const GemmLaunch& g, const ui
     if (dq) {
       scv[k] = *(const float4*)(g.s_cols + n);
       srv[k] = g.s_rows[m];
+      bv[k] = g.bias != nullptr ? *(const float4*)(g.bias + n) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
 #pragma unroll
@@ -236,10 +242,14 @@ __device__ __forceinline__ void gemm_tile_epilogue(const GemmLaunch& g, const ui
     const uint32_t o0 = ymv[k].x - kcv[k].x - a.x, o1 = ymv[k].y - kcv[k].y - a.y;
     const uint32_t o2 = ymv[k].z - kcv[k].z - a.z, o3 = ymv[k].w - kcv[k].w - a.w;
     if (g.y != nullptr) *(int4*)(g.y + m * g.ldo + n) = make_int4((int)o0, (int)o1, (int)o2, (int)o3);
-    if (dq)
-      *(float4*)(g.y_f32 + m * g.ldf + n) =
-          make_float4((float)(int32_t)o0 * srv[k] * scv[k].x, (float)(int32_t)o1 * srv[k] * scv[k].y,
-                      (float)(int32_t)o2 * srv[k] * scv[k].z, (float)(int32_t)o3 * srv[k] * scv[k].w);
+    if (dq) {
+      float4 f = make_float4((float)(int32_t)o0 * srv[k] * scv[k].x, (float)(int32_t)o1 * srv[k] * scv[k].y,
+                             (float)(int32_t)o2 * srv[k] * scv[k].z, (float)(int32_t)o3 * srv[k] * scv[k].w);
+      if (g.bias != nullptr)
+        f = make_float4(__fadd_rn(f.x, bv[k].x), __fadd_rn(f.y, bv[k].y), __fadd_rn(f.z, bv[k].z),
+                        __fadd_rn(f.w, bv[k].w));
+      *(float4*)(g.y_f32 + m * g.ldf + n) = f;
+    }
   }
 }
 

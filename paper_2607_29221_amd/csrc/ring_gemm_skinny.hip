@@ -495,11 +495,12 @@ Span span(const void* p, int64_t rows, int64_t cols, int64_t ld, int64_t elem) {
 bool overlap(Span a, Span b) { return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi; }
 
 // An output of the unmask call that shares no byte with any input (ym, kc,
-// the digit factors, the scale vectors) nor with the other output, or null.
+// the digit factors, the scale and bias vectors) nor with the other output, or null.
 uint32_t* unmask_scratch(const GemmLaunch& g, int64_t* ld) {
   const Span in[] = {span(g.ym, g.M, g.N, g.ldy, 4), span(g.kc, g.M, g.N, g.ldk, 4),
                      span(g.a, g.M, 4 * g.Kp, g.a_pitch, 1), span(g.b, g.N, 4 * g.Kp, g.b_pitch, 1),
-                     span(g.s_rows, 1, g.M, g.M, 4), span(g.s_cols, 1, g.N, g.N, 4)};
+                     span(g.s_rows, 1, g.M, g.M, 4), span(g.s_cols, 1, g.N, g.N, 4),
+                     span(g.bias, 1, g.N, g.N, 4)};
   const Span sy = span(g.y, g.M, g.N, g.ldo, 4), sf = span(g.y_f32, g.M, g.N, g.ldf, 4);
   auto free_of_inputs = [&](Span o) {
     for (const Span& i : in)

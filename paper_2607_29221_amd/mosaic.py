@@ -223,7 +223,7 @@ def mosaic_integrity_check(ct: Digits, a: Digits, v: Digits, yq: torch.Tensor, t
 def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digits], l: Optional[Digits],
                   M: int, N: int, R: int, y: Optional[torch.Tensor] = None,
                   s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,
-                  y_f32: Optional[torch.Tensor] = None) -> None:
+                  y_f32: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None) -> None:
     _need(ym, M, N, "ym", _INT, optional=False)
     _need(kc, M, N, "kc", _INT)
     if R > 0:
@@ -234,11 +234,12 @@ def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digi
     if y_f32 is not None:
         _need(s_rows, 1, M, "s_rows", (torch.float32,), optional=False)
         _need(s_cols, 1, N, "s_cols", (torch.float32,), optional=False)
+    _need(bias, 1, N, "bias", (torch.float32,))
     _check(_lib.load().mosaic_unmask(ym.data_ptr(), ym.stride(0), _ptr(kc), kc.stride(0) if kc is not None else 0,
                                      q.ptr if q else None, q.pitch if q else 0,
                                      l.ptr if l else None, l.pitch if l else 0, M, N, R,
                                      _ptr(y), y.stride(0) if y is not None else 0,
-                                     _ptr(s_rows), _ptr(s_cols), _ptr(y_f32),
+                                     _ptr(s_rows), _ptr(s_cols), _ptr(bias), _ptr(y_f32),
                                      y_f32.stride(0) if y_f32 is not None else 0, _stream()), "mosaic_unmask")
 
 

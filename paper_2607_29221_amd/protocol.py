@@ -321,7 +321,8 @@ def server(w: MaskedWeight, M: int, buf: CallBuffers) -> None:
 
 
 def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tensor] = None,
-           s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None) -> None:
+           s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,
+           bias: Optional[torch.Tensor] = None) -> None:
     """Online step 5: Y = Y' - K_c - Q Lcat^T (digits of Q first). In sparse
     mode the product covers the level-d slot (L Q_d) and each S_{i+1} Q_i is
     subtracted by gathering from Q_i's ring words."""
@@ -333,7 +334,7 @@ def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tens
         m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
     if not sparse:
         m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
-                        M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
+                        M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32, bias=bias)
         return
     m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.Rd), w.Lcat[0].whole(w.Rd),
                     M, w.N, w.Rd, y=buf.Y)
@@ -342,7 +343,7 @@ def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tens
             c0 = w.q_cols[slot]
             m.mosaic_sparse_gather_cols(w.S[lv], buf.YQ[:, c0: c0 + r[lv - 1]], M, buf.Y, subtract=True)
     if y_f32 is not None:                    # dequantise the finished result (no product term)
-        m.mosaic_unmask(buf.Y, None, None, None, M, w.N, 0, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32)
+        m.mosaic_unmask(buf.Y, None, None, None, M, w.N, 0, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32, bias=bias)
 
 
 def verify(w: MaskedWeight, M: int, buf: CallBuffers, sides: bool = False) -> torch.Tensor:

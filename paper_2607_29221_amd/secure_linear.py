@@ -13,7 +13,8 @@ Online (activations A, M x K fp32, one row per token):
   1. rotate every token, A~ = A R^T (the protocol box's R X in the row-major layout), and
      quantise each token to q_x with scale s_x;
   2. Init X, mask, server product and unmask of Pi_Sec-Approx-MatMul;
-  3. dequantise in the unmask epilogue: Y = s_x[m] s_w[n] Y^[m, n].
+  3. dequantise in the unmask epilogue: Y = s_x[m] s_w[n] Y^[m, n], plus
+     the optional bias b[n].
 
 The activation window q_x is the largest value for which no inner product of
 the noisy codes can leave the signed ring range: with |E| <= bound,
@@ -51,12 +52,17 @@ def activation_window(K: int, q_w: int, bound: int) -> int:
 
 
 class SecureLinear:
-    """One linear layer y = x W^T through Pi_Sec-Linear (no bias)."""
+    """One linear layer y = x W^T + b through Pi_Sec-Linear (b optional, N
+    floats, added in the unmask epilogue)."""
 
     def __init__(self, W: torch.Tensor, params, seed: int, weight_id: int, q_w: int = 127,
-                 keep_weight_codes: bool = False):
+                 keep_weight_codes: bool = False, bias: Optional[torch.Tensor] = None):
         if W.dtype != torch.float32 or W.dim() != 2:
             raise ValueError("W must be a 2-D float32 tensor (N x K)")
+        if bias is not None and (bias.dtype != torch.float32 or bias.shape != (W.shape[0],)
+                                 or not bias.is_contiguous()):
+            raise ValueError("bias must be a contiguous float32 vector of N entries")
+        self.bias = bias
         dev = W.device
         self.N, self.K = W.shape
         self.block = rotation_block(self.K)
@@ -131,7 +137,7 @@ class SecureLinear:
         gp.server(self.w, M, buf)
         self._mark("server")
         y = torch.empty((M, self.N), dtype=torch.float32, device=x.device)
-        gp.unmask(self.w, M, buf, y_f32=y, s_rows=s_x, s_cols=self.s_w)
+        gp.unmask(self.w, M, buf, y_f32=y, s_rows=s_x, s_cols=self.s_w, bias=self.bias)
         self._mark("unmask")
         if keep_codes:
             self.last_codes, self.last_scales, self.last_buf = codes, s_x, buf

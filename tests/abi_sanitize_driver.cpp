@@ -94,15 +94,17 @@ int main() {
   EXPECT(mosaic_integrity_check(Fd, 256, Fd, int64_t(1) << 24, Fd, 256, Fu, 64, 4, 4, 64, 64, Fu, 4, Fc, nullptr),
          UNS);
   EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 32768, (int32_t*)F, 4, nullptr, nullptr,
-                       nullptr, 0, nullptr), UNS);
+                       nullptr, nullptr, 0, nullptr), UNS);
   EXPECT(mosaic_unmask(nullptr, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr,
+                       nullptr, nullptr, 0, nullptr), INV);
+  EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, nullptr, 4, nullptr, nullptr, nullptr,
                        nullptr, 0, nullptr), INV);
-  EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, nullptr, 4, nullptr, nullptr, nullptr, 0,
-                       nullptr), INV);
-  EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, nullptr, 4, nullptr, nullptr, Ff, 4,
-                       nullptr), INV);
-  EXPECT(mosaic_unmask(Fu, 4, Fu, 3, Fd, 256, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr, nullptr, 0,
-                       nullptr), INV);
+  EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, nullptr, 4, nullptr, nullptr, nullptr, Ff,
+                       4, nullptr), INV);
+  EXPECT(mosaic_unmask(Fu, 4, Fu, 3, Fd, 256, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr, nullptr,
+                       nullptr, 0, nullptr), INV);
+  EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr, Ff,
+                       nullptr, 0, nullptr), INV);     // bias without y_f32
 
   // rotation and quantisation
   EXPECT(mosaic_hadamard_rotate(Ff, 64, Ff, 64, 4, 64, 48, nullptr, 0, nullptr), UNS);

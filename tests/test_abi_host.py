@@ -121,12 +121,13 @@ def test_matmul_validation(lib):
 @cpu_only
 def test_unmask_validation(lib):
     args = dict(ym=FAKE, ldy=8, kc=None, ldk=0, q=FAKE, qp=256, l=FAKE, lp=256, M=2, N=8, R=64,
-                y=FAKE, ldo=8, sr=None, sc=None, yf=None, ldf=0)
+                y=FAKE, ldo=8, sr=None, sc=None, bias=None, yf=None, ldf=0)
 
     def call(**kw):
         a = dict(args, **kw)
         return lib.mosaic_unmask(a["ym"], a["ldy"], a["kc"], a["ldk"], a["q"], a["qp"], a["l"], a["lp"], a["M"],
-                                 a["N"], a["R"], a["y"], a["ldo"], a["sr"], a["sc"], a["yf"], a["ldf"], None)
+                                 a["N"], a["R"], a["y"], a["ldo"], a["sr"], a["sc"], a["bias"], a["yf"], a["ldf"],
+                                 None)
     assert call(ym=None) == INVALID
     assert call(y=None) == INVALID
     assert call(ldy=7) == INVALID
@@ -134,6 +135,7 @@ def test_unmask_validation(lib):
     assert call(qp=128) == INVALID
     assert call(l=None) == INVALID
     assert call(yf=FAKE, ldf=8) == INVALID          # fp32 output without scales
+    assert call(bias=FAKE) == INVALID               # bias without the fp32 output
     assert call(R=40000, qp=4 * 40000 + 64, lp=4 * 40000 + 64) == UNSUPPORTED
 
 
@@ -220,7 +222,8 @@ def test_zero_sized_calls_are_noops(lib):
     assert lib.mosaic_sample(ctypes.byref(r), 0, 0, None, 0, None, 0, None) == 0
     assert lib.mosaic_masked_matmul(None, 0, None, 0, 0, 7, 64, None, 7, None) == 0
     assert lib.mosaic_masked_matmul(None, 0, None, 0, 7, 0, 64, None, 0, None) == 0
-    assert lib.mosaic_unmask(None, 0, None, 0, None, 0, None, 0, 0, 4, 64, None, 0, None, None, None, 0, None) == 0
+    assert lib.mosaic_unmask(None, 0, None, 0, None, 0, None, 0, 0, 4, 64, None, 0, None, None, None, None, 0,
+                             None) == 0
     assert lib.mosaic_sample_signs(ctypes.byref(r), 0, None, None) == 0
     assert lib.mosaic_hadamard_rotate(None, 64, None, 64, 0, 64, 64, None, 0, None) == 0
     assert lib.mosaic_quantize_rows(None, 8, 0, 8, 127, None, 0, None, 0, None, None) == 0

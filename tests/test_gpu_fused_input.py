@@ -78,6 +78,29 @@ def test_secure_linear_fused_equals_separate():
     assert np.array_equal(y_fused.cpu().numpy(), y_sep.cpu().numpy())
 
 
+@pytest.mark.parametrize("sparse", [False, True], ids=["dense-mask", "sparse-lpn"])
+def test_secure_linear_bias(sparse):
+    """Pi_Sec-Linear with a bias (Section 5 box, online step 3): with the same
+    weight, seed and call, y with bias equals y without it plus b, added in
+    fp32 after the dequantisation (one rounding), for the dense mask and for
+    the depth-2 sparse mask whose dequantisation runs after the gathers."""
+    from synthetic_inputs import PARAMS_D2_SPARSE
+    dev = torch.device("cuda", 0)
+    gen = torch.Generator(device=dev).manual_seed(11)
+    N, K, M = 640, 2048, 8 if sparse else 96
+    W = torch.randn((N, K), generator=gen, device=dev)
+    b = torch.randn(N, generator=gen, device=dev)
+    x = torch.randn((M, K), generator=gen, device=dev)
+    p = PARAMS_D2_SPARSE if sparse else PARAMS_PAPER_D1
+    y0 = SecureLinear(W, p, 0xB1A5, weight_id=1)(x, call_id=2)
+    yb = SecureLinear(W, p, 0xB1A5, weight_id=1, bias=b)(x, call_id=2)
+    torch.cuda.synchronize()
+    want = (y0.cpu().numpy() + b.cpu().numpy()[None, :]).astype(np.float32)
+    assert np.array_equal(yb.cpu().numpy(), want)
+    with pytest.raises(ValueError):
+        SecureLinear(W, p, 0xB1A5, weight_id=1, bias=b[:-1])
+
+
 @pytest.mark.parametrize("rows,n,block,qmax", [(64, 8192, 8192, 1997), (48, 28672, 4096, 567),
                                                (16, 16384, 16384, 1000), (32, 8192, 1024, 1997)],
                          ids=["one-launch-8192", "two-launch-28672", "one-launch-16384", "blocks-1024"])

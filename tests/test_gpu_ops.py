@@ -358,14 +358,17 @@ def test_unmask_short_a_outputs(M, case):
         yf = torch.empty((M, N), dtype=torch.float32, device="cuda")
     elif case == "f32_over_ym":
         yf = ymd.view(torch.float32)
+    bd, bn = _bias(N, "aligned" if case in ("f32", "f32_over_ym") else None, M + 11)
     m.mosaic_unmask(ymd, kcd, Q, L, M, N, R, y=y, s_rows=sr if want_f32 else None,
-                    s_cols=sc if want_f32 else None, y_f32=yf)
+                    s_cols=sc if want_f32 else None, y_f32=yf, bias=bd)
     torch.cuda.synchronize()
     yi = ring_sub(ring_sub(ym, kc), ring_matmul(q, l.T)).view(np.int32)
     if y is not None:
         assert np.array_equal(y.cpu().numpy(), yi)
     if want_f32:
         ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+        if bd is not None:
+            ref = (ref + bn).astype(np.float32)
         assert np.array_equal(yf.cpu().numpy(), ref)
 
 
@@ -387,13 +390,15 @@ def test_unmask_one_row_large_factor(with_f32):
     sr = torch.rand(M, device="cuda") * 1e-3
     sc = torch.rand(N, device="cuda") * 1e-3
     yf = torch.empty((M, N), dtype=torch.float32, device="cuda") if with_f32 else None
+    bd, bn = _bias(N, "offset" if with_f32 else None, 99)
     m.mosaic_unmask(to_dev_ring(ym), to_dev_ring(kc), Q, L, M, N, R, y=y, s_rows=sr if with_f32 else None,
-                    s_cols=sc if with_f32 else None, y_f32=yf)
+                    s_cols=sc if with_f32 else None, y_f32=yf, bias=bd)
     torch.cuda.synchronize()
     yi = ring_sub(ring_sub(ym, kc), ring_matmul(q, l.T)).view(np.int32)
     assert np.array_equal(y.cpu().numpy(), yi)
     if with_f32:
         ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+        ref = (ref + bn).astype(np.float32)
         assert np.array_equal(yf.cpu().numpy(), ref)
 
 
@@ -419,8 +424,21 @@ def test_unmask_in_place_tiled(M, target):
     assert np.array_equal(y.cpu().numpy(), ref)
 
 
+def _bias(N, kind, seed):
+    """None, a 16-byte aligned bias, or one at a 4-byte offset (the tiled
+    kernel's epilogue then takes its one-word path)."""
+    if kind is None:
+        return None, 0.0
+    b = torch.from_numpy(_rng_np(seed).standard_normal(N + 1).astype(np.float32)).cuda()
+    b = b[:N] if kind == "aligned" else b[1:]
+    return b, b.cpu().numpy()[None, :]
+
+
 @pytest.mark.parametrize("M,N", [(40, 90), (150, 90), (150, 92), (300, 260)])
-def test_unmask_dequantised(M, N):
+@pytest.mark.parametrize("bias", [None, "aligned", "offset"])
+def test_unmask_dequantised(M, N, bias):
+    """y_f32 = (y s_rows) s_cols (+ bias), each step rounded to fp32, equal
+    bit for bit to the same steps in numpy."""
     rng = _rng_np(5 + M + N)
     R = 64
     ym = _random_ring(rng, (M, N))
@@ -432,10 +450,13 @@ def test_unmask_dequantised(M, N):
     sr = torch.rand(M, device="cuda") * 1e-3
     sc = torch.rand(N, device="cuda") * 1e-3
     yf = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    m.mosaic_unmask(to_dev_ring(ym), None, Q, L, M, N, R, s_rows=sr, s_cols=sc, y_f32=yf)
+    bd, bn = _bias(N, bias, M * N)
+    m.mosaic_unmask(to_dev_ring(ym), None, Q, L, M, N, R, s_rows=sr, s_cols=sc, y_f32=yf, bias=bd)
     torch.cuda.synchronize()
     yi = ring_sub(ym, ring_matmul(q, l.T)).view(np.int32)
     ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+    if bd is not None:
+        ref = (ref + bn).astype(np.float32)
     assert np.array_equal(yf.cpu().numpy(), ref)
 
 
