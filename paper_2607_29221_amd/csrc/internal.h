@@ -79,6 +79,10 @@ struct GemmLaunch {
   int64_t b_last;
   // decode kernel, EPI_ACCUM: subtract the product from c instead of adding
   bool negate;
+  // tiled kernel (set by its launcher): the last split_tiles tiles run as
+  // split_k pieces of the inner dimension, added into c atomically
+  int64_t split_tiles;
+  int32_t split_k;
   // EPI_STORE
   uint32_t* c;
   int64_t ldc;

@@ -75,16 +75,19 @@ struct Tile {
 // the column tiles together. The blocks an XCD runs at once thus cover a
 // compact patch of the output, whose operand slices are shared in that XCD's
 // L2; XCDs that own the same columns for different row groups sweep them at
-// the same pace, so B is shared in the last-level cache as well. The remap is
-// a bijection of [0, tiles); correctness does not depend on dispatch order.
-__device__ __forceinline__ Tile tile_of(int64_t pid, int64_t tiles_m, int64_t tiles_n) {
+// the same pace, so B is shared in the last-level cache as well. Both maps
+// are bijections of [0, tiles); correctness does not depend on dispatch
+// order.
+__device__ __forceinline__ int64_t xcd_order(int64_t pid, int64_t tiles) {
   constexpr int64_t NXCD = 8;
-  constexpr int64_t GROUP_M = 8;
-  const int64_t tiles = tiles_m * tiles_n;
   const int64_t xcd = pid % NXCD;
   const int64_t local = pid / NXCD;
   const int64_t q = tiles / NXCD, r = tiles % NXCD;
-  const int64_t lin = xcd * q + (xcd < r ? xcd : r) + local;
+  return xcd * q + (xcd < r ? xcd : r) + local;
+}
+
+__device__ __forceinline__ Tile tile_at(int64_t lin, int64_t tiles_m, int64_t tiles_n) {
+  constexpr int64_t GROUP_M = 8;
   const int64_t per_group = GROUP_M * tiles_n;
   const int64_t group = lin / per_group;
   const int64_t first_m = group * GROUP_M;
@@ -125,19 +128,67 @@ __device__ __forceinline__ void wait_loads(int n) {
 
 __device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
 
+// Adds a TM x TN tile held in LDS (row pitch TROW words) into C with 32-bit
+// atomics (wrap-around adds: exact over the ring), chunks of 4 columns as in
+// gemm_tile_epilogue.
+template <int TM, int TN, int NT, int TROW>
+__device__ __forceinline__ void gemm_tile_atomic_add(const GemmLaunch& g, const uint32_t* tile, int64_t m0,
+                                                     int64_t n0, int tid) {
+  constexpr int CPR = TN / 4;
+  constexpr int PER = TM * CPR / NT;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + NT * k;
+    const int r = c / CPR;
+    const int64_t m = m0 + r;
+    const int64_t n = n0 + 4 * (c % CPR);
+    if (m >= g.M || n >= g.N) continue;
+    const uint4 a = *(const uint4*)(tile + r * TROW + 4 * (c % CPR));
+    uint32_t* cr = g.c + m * g.ldc + n;
+    atomicAdd(cr, a.x);
+    if (n + 1 < g.N) atomicAdd(cr + 1, a.y);
+    if (n + 2 < g.N) atomicAdd(cr + 2, a.z);
+    if (n + 3 < g.N) atomicAdd(cr + 3, a.w);
+  }
+}
+
+// Workgroup b < tiles - split_tiles computes a whole tile, in the XCD-aware
+// order over those tiles. The last split_tiles tiles of the logical order
+// run as split_k pieces each (workgroup full + p: piece p / split_tiles of
+// tile full + p % split_tiles), each piece a contiguous range of stage
+// pairs, added into C atomically; C is cleared for those tiles first when the
+// result is stored (launch_ring_gemm).
 template <int EPI, int VEC>
 __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   __shared__ __attribute__((aligned(1024))) char lds[NSTAGE * STAGE];
 
   const int64_t tiles_m = (g.M + BM - 1) / BM;
   const int64_t tiles_n = (g.N + BN - 1) / BN;
-  const Tile tile = tile_of(blockIdx.x, tiles_m, tiles_n);
+  const int64_t full = tiles_m * tiles_n - g.split_tiles;
+  int64_t lin;
+  int s0 = 0;
+  int stages = (int)(g.Kp / BK);   // even: Kp is a multiple of 64
+  bool piece = false;
+  if ((int64_t)blockIdx.x < full) {
+    lin = xcd_order(blockIdx.x, full);
+  } else {
+    const int64_t p = (int64_t)blockIdx.x - full;
+    const int64_t q = p / g.split_tiles;
+    lin = full + (p - q * g.split_tiles);
+    const int64_t pairs = stages / 2;
+    s0 = 2 * (int)(pairs * q / g.split_k);
+    stages = 2 * (int)(pairs * (q + 1) / g.split_k) - s0;
+    piece = true;
+  }
+  const Tile tile = tile_at(lin, tiles_m, tiles_n);
   const int64_t m0 = tile.tm * BM;
   const int64_t n0 = tile.tn * BN;
   const int64_t rows_a = (g.M - m0) < BM ? (g.M - m0) : BM;
   const int64_t rows_b = (g.N - n0) < BN ? (g.N - n0) : BN;
-  const v4i rsa = make_rsrc(g.a + m0 * g.a_pitch, rows_a * g.a_pitch);
-  const v4i rsb = make_rsrc(g.b + n0 * g.b_pitch, rows_b * g.b_pitch);
+  // a piece's operands start at its first stage; the ranges end where the
+  // tile's rows end
+  const v4i rsa = make_rsrc(g.a + m0 * g.a_pitch + s0 * ROWB, rows_a * g.a_pitch - s0 * ROWB);
+  const v4i rsb = make_rsrc(g.b + n0 * g.b_pitch + s0 * ROWB, rows_b * g.b_pitch - s0 * ROWB);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -177,7 +228,6 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][s][v] = 0;
 
-  const int stages = (int)(g.Kp / BK);   // even: Kp is a multiple of 64
   v4i fa[2][2][4], fb[2][4];             // [register set][tile][digit], [register set][digit]
 
 #define MOSAIC_DMA(S, k)                                                                   \
@@ -301,7 +351,52 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
     }
   }
   __syncthreads();
-  gemm_tile_epilogue<EPI, VEC, BM, BN, NTHREADS, TROW>(g, ctile, m0, n0, tid);
+  if (EPI != EPI_UNMASK && piece) gemm_tile_atomic_add<BM, BN, NTHREADS, TROW>(g, ctile, m0, n0, tid);
+  else gemm_tile_epilogue<EPI, VEC, BM, BN, NTHREADS, TROW>(g, ctile, m0, n0, tid);
+}
+
+// C = 0 over the last split_tiles tiles of the logical order (one workgroup
+// per tile).
+__global__ __launch_bounds__(256) void clear_split_tiles_kernel(GemmLaunch g) {
+  const int64_t tiles_m = (g.M + BM - 1) / BM;
+  const int64_t tiles_n = (g.N + BN - 1) / BN;
+  const Tile tile = tile_at(tiles_m * tiles_n - g.split_tiles + blockIdx.x, tiles_m, tiles_n);
+  const int64_t m0 = tile.tm * BM, n0 = tile.tn * BN;
+  for (int e = threadIdx.x; e < BM * BN; e += 256) {
+    const int64_t m = m0 + e / BN, n = n0 + e % BN;
+    if (m < g.M && n < g.N) g.c[m * g.ldc + n] = 0u;
+  }
+}
+
+// Tiles to split and pieces per tile for a launch of `tiles` whole tiles
+// over `cus` compute units. Only the last, partial round of tiles is split,
+// and only when it would leave at least half of the compute units idle: the
+// chip is power-limited on uniform digits, so a last round on three quarters
+// of the units runs at higher clocks, and splitting it measured no faster
+// (2048 x 9728 x 8192: 1.22 ms whole, 1.24-1.26 ms with the last 192 tiles in
+// four pieces). With a round costing one tile's stages plus a fixed cost per
+// workgroup (its prologue and epilogue, taken as 6 stages) and the clear
+// before a store (5 stages), split_k pieces of the tail's tiles take
+// ceil(tail split_k / cus) rounds of stages / split_k + 6; pieces keep at
+// least two stage pairs.
+void choose_split(int64_t tiles, int64_t stages, int64_t cus, bool store, int64_t* split_tiles, int* split_k) {
+  *split_tiles = 0;
+  *split_k = 1;
+  if (cus <= 0) return;
+  const int64_t tail = tiles % cus;
+  if (tail == 0 || 2 * tail >= cus) return;
+  constexpr int64_t kFixed = 6, kClear = 5;
+  int64_t best = stages + kFixed;
+  for (int k : {2, 3, 4, 6, 8}) {
+    if (stages / 2 < 2 * (int64_t)k) break;
+    const int64_t rounds = (tail * k + cus - 1) / cus;
+    const int64_t cost = rounds * (stages / k + kFixed) + (store ? kClear : 0);
+    if (cost < best) {
+      best = cost;
+      *split_k = k;
+    }
+  }
+  if (*split_k > 1) *split_tiles = tail;
 }
 
 }  // namespace
@@ -310,17 +405,24 @@ hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s
   if (g.M <= SKINNY_MAX_M) return launch_ring_gemm_skinny(g, epi, s);
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles == 0) return hipSuccess;
-  const dim3 grid((unsigned)tiles);
+  GemmLaunch gs = g;
+  gs.split_tiles = 0;
+  gs.split_k = 1;
+  if (epi != EPI_UNMASK)   // the unmask epilogue needs the whole product of a tile
+    choose_split(tiles, g.Kp / BK, compute_units(), epi == EPI_STORE, &gs.split_tiles, &gs.split_k);
+  if (gs.split_tiles > 0 && epi == EPI_STORE)
+    hipLaunchKernelGGL(clear_split_tiles_kernel, dim3((unsigned)gs.split_tiles), dim3(256), 0, s, gs);
+  const dim3 grid((unsigned)(tiles + gs.split_tiles * (gs.split_k - 1)));
   const bool vec = gemm_epilogue_vectorizable(g, epi);
   if (epi == EPI_STORE) {
-    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 1>), grid, dim3(NTHREADS), 0, s, g);
-    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 0>), grid, dim3(NTHREADS), 0, s, g);
+    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 1>), grid, dim3(NTHREADS), 0, s, gs);
+    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 0>), grid, dim3(NTHREADS), 0, s, gs);
   } else if (epi == EPI_ACCUM) {
-    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 1>), grid, dim3(NTHREADS), 0, s, g);
-    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 0>), grid, dim3(NTHREADS), 0, s, g);
+    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 1>), grid, dim3(NTHREADS), 0, s, gs);
+    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 0>), grid, dim3(NTHREADS), 0, s, gs);
   } else {
-    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 1>), grid, dim3(NTHREADS), 0, s, g);
-    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 0>), grid, dim3(NTHREADS), 0, s, g);
+    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 1>), grid, dim3(NTHREADS), 0, s, gs);
+    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 0>), grid, dim3(NTHREADS), 0, s, gs);
   }
   return hipGetLastError();
 }
