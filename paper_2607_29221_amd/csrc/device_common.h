@@ -159,14 +159,25 @@ __device__ __forceinline__ uint32_t digit_word(uint32_t x) {
 }
 
 // Transpose four digit words (elements k..k+3) into four words holding digit
-// t of those four elements (byte b = element k+b).
+// t of those four elements (byte b = element k+b): two rounds of byte
+// permutes (__builtin_amdgcn_perm(hi, lo, sel): selector bytes 0-3 pick lo's
+// bytes, 4-7 hi's), eight instructions for the 16 bytes.
 __device__ __forceinline__ void digit_transpose4(const uint32_t w[4], uint32_t out[4]) {
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int s = 8 * t;
-    out[t] = ((w[0] >> s) & 0xFFu) | (((w[1] >> s) & 0xFFu) << 8) |
-             (((w[2] >> s) & 0xFFu) << 16) | (((w[3] >> s) & 0xFFu) << 24);
-  }
+  const uint32_t e01 = __builtin_amdgcn_perm(w[1], w[0], 0x06020400u);   // w0.0 w1.0 w0.2 w1.2
+  const uint32_t o01 = __builtin_amdgcn_perm(w[1], w[0], 0x07030501u);   // w0.1 w1.1 w0.3 w1.3
+  const uint32_t e23 = __builtin_amdgcn_perm(w[3], w[2], 0x06020400u);
+  const uint32_t o23 = __builtin_amdgcn_perm(w[3], w[2], 0x07030501u);
+  out[0] = __builtin_amdgcn_perm(e23, e01, 0x05040100u);
+  out[1] = __builtin_amdgcn_perm(o23, o01, 0x05040100u);
+  out[2] = __builtin_amdgcn_perm(e23, e01, 0x07060302u);
+  out[3] = __builtin_amdgcn_perm(o23, o01, 0x07060302u);
+}
+
+// Digit planes of four consecutive ring elements: out[t] holds digit t of
+// v[0..3] (byte b = element b).
+__device__ __forceinline__ void digit_planes4(const uint32_t v[4], uint32_t out[4]) {
+  const uint32_t w[4] = {digit_word(v[0]), digit_word(v[1]), digit_word(v[2]), digit_word(v[3])};
+  digit_transpose4(w, out);
 }
 
 // Digit planes of one 16-column group held by four consecutive lanes: lane

@@ -227,19 +227,12 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
         uint32_t pl[4][4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const uint32_t w0 = digit_word((uint32_t)fb[j][c][0]), w1 = digit_word((uint32_t)fb[j][c][1]);
-          const uint32_t w2 = digit_word((uint32_t)fb[j][c][2]), w3 = digit_word((uint32_t)fb[j][c][3]);
-          // 4 x 4 byte transpose in two rounds of byte permutes
-          // (__builtin_amdgcn_perm(hi, lo, sel): selector bytes 0-3 pick lo's bytes,
-          // 4-7 hi's)
-          const uint32_t e01 = __builtin_amdgcn_perm(w1, w0, 0x06020400u);   // w0.0 w1.0 w0.2 w1.2
-          const uint32_t o01 = __builtin_amdgcn_perm(w1, w0, 0x07030501u);   // w0.1 w1.1 w0.3 w1.3
-          const uint32_t e23 = __builtin_amdgcn_perm(w3, w2, 0x06020400u);
-          const uint32_t o23 = __builtin_amdgcn_perm(w3, w2, 0x07030501u);
-          pl[0][c] = __builtin_amdgcn_perm(e23, e01, 0x05040100u);           // digit 0 of w0..w3
-          pl[1][c] = __builtin_amdgcn_perm(o23, o01, 0x05040100u);
-          pl[2][c] = __builtin_amdgcn_perm(e23, e01, 0x07060302u);
-          pl[3][c] = __builtin_amdgcn_perm(o23, o01, 0x07060302u);
+          const uint32_t v4[4] = {(uint32_t)fb[j][c][0], (uint32_t)fb[j][c][1], (uint32_t)fb[j][c][2],
+                                  (uint32_t)fb[j][c][3]};
+          uint32_t p4[4];
+          digit_planes4(v4, p4);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) pl[t][c] = p4[t];
         }
 #pragma unroll
         for (int t = 0; t < 4; ++t) fb[j][t] = v4i{(int)pl[t][0], (int)pl[t][1], (int)pl[t][2], (int)pl[t][3]};
