@@ -267,7 +267,14 @@ mosaic_status mosaic_sparse_csr_fill(const mosaic_rng* rng, int64_t rows, int64_
  * mosaic_sparse_gather_cols: c(m, n) +-= sum_j d(m, j) P(n, j) for
  *   0 <= m < M, 0 <= n < N: P is N x r, d is a dense M x r uint32 matrix
  *   (ldd), c is M x N (ldc). Used for the S_{i+1} Q_i terms of unmasking.
- * c must not overlap d or the sparse arrays. */
+ *   When y_f32 is not NULL the finished c is also dequantised as in
+ *   mosaic_unmask (Pi_Sec-Linear, online step 3): y_f32(m, n) =
+ *   (float)c(m, n) * s_rows[m] * s_cols[n] (+ bias[n]), leading dimension
+ *   ldf >= N; the last gather of a sparse unmasking then writes the
+ *   floating-point output with no further pass. s_rows, s_cols, bias and
+ *   ldf are ignored when y_f32 is NULL (bias without y_f32 is
+ *   MOSAIC_ERR_INVALID_ARG).
+ * c must not overlap d or the sparse arrays, y_f32 none of them. */
 mosaic_status mosaic_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const int32_t* col_idx,
                                         const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
                                         uint32_t* c, int64_t ldc, int32_t subtract, void* stream);
@@ -281,7 +288,8 @@ mosaic_status mosaic_sparse_stream_gather_rows(const mosaic_rng* rng, int64_t ro
                                                int32_t subtract, void* stream);
 mosaic_status mosaic_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
                                         const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
-                                        int64_t ldc, int32_t subtract, void* stream);
+                                        int64_t ldc, int32_t subtract, const float* s_rows, const float* s_cols,
+                                        const float* bias, float* y_f32, int64_t ldf, void* stream);
 
 /* Integrity check (Freivalds' test; Appendix "Computational integrity" and
  * online step 4 of the Section 4.2 protocol box): the client compares two

@@ -61,8 +61,8 @@ _SIGNATURES = {
                                   c_i32),
     "mosaic_sparse_stream_gather_rows": ([ctypes.POINTER(MosaicRng), c_i64, c_i64, c_ptr, c_i64, c_i64, c_ptr, c_i64,
                                           c_i32, c_ptr], c_i32),
-    "mosaic_sparse_gather_cols": ([c_i64, c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr, c_i64, c_i32, c_ptr],
-                                  c_i32),
+    "mosaic_sparse_gather_cols": ([c_i64, c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr, c_i64, c_i32,
+                                   c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
     "mosaic_hadamard_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
     "mosaic_hadamard28_rotate": ([c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr], c_i32),
     "mosaic_probe_mfma_i8": ([c_i32, c_i64, c_ptr, ctypes.POINTER(c_i64), c_ptr], c_i32),

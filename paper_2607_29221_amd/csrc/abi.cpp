@@ -477,14 +477,19 @@ mosaic_status mosaic_sparse_stream_gather_rows(const mosaic_rng* rng, int64_t ro
 
 mosaic_status mosaic_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
                                         const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
-                                        int64_t ldc, int32_t subtract, void* stream) {
+                                        int64_t ldc, int32_t subtract, const float* s_rows, const float* s_cols,
+                                        const float* bias, float* y_f32, int64_t ldf, void* stream) {
   if (M < 0 || N < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
   if (M == 0 || N == 0) return MOSAIC_OK;
   if (row_ptr == nullptr || col_idx == nullptr || values == nullptr || d == nullptr || c == nullptr)
     return fail(MOSAIC_ERR_INVALID_ARG, "NULL operand");
   if (ldc < N || ldd < 0) return fail(MOSAIC_ERR_INVALID_ARG, "ldc < N");
+  if (y_f32 != nullptr && (ldf < N || s_rows == nullptr || s_cols == nullptr))
+    return fail(MOSAIC_ERR_INVALID_ARG, "y_f32 needs ldf >= N and both scale vectors");
+  if (bias != nullptr && y_f32 == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "bias needs y_f32");
   if (M > 0x7FFFFFFF || (N + 31) / 32 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
-  return hip_status(launch_sparse_gather_cols(M, N, row_ptr, col_idx, values, d, ldd, c, ldc, subtract != 0,
+  const Dequant dq{s_rows, s_cols, bias, y_f32, ldf};
+  return hip_status(launch_sparse_gather_cols(M, N, row_ptr, col_idx, values, d, ldd, c, ldc, subtract != 0, dq,
                                               (hipStream_t)stream), "sparse gather launch");
 }
 

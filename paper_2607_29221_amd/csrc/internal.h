@@ -37,9 +37,18 @@ hipError_t launch_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const
 hipError_t launch_sparse_stream_gather_rows(const RngArgs& r, int64_t rows, int64_t rcols, const uint32_t* d,
                                             int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc, int subtract,
                                             hipStream_t s);
+// Dequantised copy of a finished ring result: y[m, n] = (float)(int32)c *
+// s_rows[m] * s_cols[n] (+ bias[n]); y null for none.
+struct Dequant {
+  const float* s_rows;
+  const float* s_cols;
+  const float* bias;
+  float* y;
+  int64_t ld;
+};
 hipError_t launch_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
                                      const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
-                                     int64_t ldc, int subtract, hipStream_t s);
+                                     int64_t ldc, int subtract, const Dequant& dq, hipStream_t s);
 
 // Fixed-row-weight (WEIGHT) streams: at most WEIGHT_MAX_COLS columns (the
 // row's permutation lives in LDS) and, where a row is staged whole in LDS,

@@ -264,7 +264,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rco
 // eight partial sums are combined with lane shuffles.
 __global__ __launch_bounds__(256) void gather_cols_kernel(int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
                                                           const uint32_t* values, const uint32_t* d, int64_t ldd,
-                                                          uint32_t* c, int64_t ldc, int subtract) {
+                                                          uint32_t* c, int64_t ldc, int subtract, Dequant dq) {
   const int64_t m = blockIdx.x;
   const int sub = threadIdx.x & 7;
   const int64_t n = (int64_t)blockIdx.y * 32 + (threadIdx.x >> 3);
@@ -279,7 +279,13 @@ __global__ __launch_bounds__(256) void gather_cols_kernel(int64_t N, const int64
   acc += __shfl_xor(acc, 1, 8);
   if (n < N && sub == 0) {
     uint32_t* out = c + m * ldc + n;
-    *out = subtract ? *out - acc : *out + acc;
+    const uint32_t v = subtract ? *out - acc : *out + acc;
+    *out = v;
+    if (dq.y != nullptr) {
+      // the same steps and roundings as the unmask epilogue's dequantisation
+      const float f = (float)(int32_t)v * dq.s_rows[m] * dq.s_cols[n];
+      dq.y[m * dq.ld + n] = dq.bias != nullptr ? __fadd_rn(f, dq.bias[n]) : f;
+    }
   }
 }
 
@@ -353,10 +359,10 @@ hipError_t launch_weighted_csr_fill(const RngArgs& r, int64_t rows, int64_t cols
 
 hipError_t launch_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
                                      const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
-                                     int64_t ldc, int subtract, hipStream_t s) {
+                                     int64_t ldc, int subtract, const Dequant& dq, hipStream_t s) {
   if (M == 0 || N == 0) return hipSuccess;
   hipLaunchKernelGGL(gather_cols_kernel, dim3((unsigned)M, (unsigned)((N + 31) / 32)), dim3(256), 0, s, N,
-                     row_ptr, col_idx, values, d, ldd, c, ldc, subtract);
+                     row_ptr, col_idx, values, d, ldd, c, ldc, subtract, dq);
   return hipGetLastError();
 }
 

@@ -314,13 +314,24 @@ def mosaic_sparse_stream_gather_rows(r: _lib.MosaicRng, rows: int, rcols: int, d
 
 
 def mosaic_sparse_gather_cols(p: SparseRows, d: torch.Tensor, M: int, c: torch.Tensor,
-                              subtract: bool = False) -> None:
-    """c[m, n] +-= sum_j d[m, j] P[n, j] for m < M, n < P.rows."""
+                              subtract: bool = False, y_f32: Optional[torch.Tensor] = None,
+                              s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,
+                              bias: Optional[torch.Tensor] = None) -> None:
+    """c[m, n] +-= sum_j d[m, j] P[n, j] for m < M, n < P.rows; with y_f32,
+    also y_f32 = c s_rows[m] s_cols[n] (+ bias[n]) of the finished c."""
+    N = p.rows
     _need(d, M, p.cols, "d", _INT, optional=False)
-    _need(c, M, p.rows, "c", _INT, optional=False)
-    _check(_lib.load().mosaic_sparse_gather_cols(M, p.rows, p.row_ptr.data_ptr(), p.col_idx.data_ptr(),
+    _need(c, M, N, "c", _INT, optional=False)
+    _need(y_f32, M, N, "y_f32", (torch.float32,))
+    if y_f32 is not None:
+        _need(s_rows, 1, M, "s_rows", (torch.float32,), optional=False)
+        _need(s_cols, 1, N, "s_cols", (torch.float32,), optional=False)
+    _need(bias, 1, N, "bias", (torch.float32,))
+    _check(_lib.load().mosaic_sparse_gather_cols(M, N, p.row_ptr.data_ptr(), p.col_idx.data_ptr(),
                                                  p.values.data_ptr(), d.data_ptr(), d.stride(0), c.data_ptr(),
-                                                 c.stride(0), 1 if subtract else 0, _stream()),
+                                                 c.stride(0), 1 if subtract else 0, _ptr(s_rows), _ptr(s_cols),
+                                                 _ptr(bias), _ptr(y_f32), y_f32.stride(0) if y_f32 is not None else 0,
+                                                 _stream()),
            "mosaic_sparse_gather_cols")
 
 

@@ -338,11 +338,14 @@ def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tens
         return
     m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.Rd), w.Lcat[0].whole(w.Rd),
                     M, w.N, w.Rd, y=buf.Y)
-    for slot, lv in enumerate(w.slot_levels):
-        if lv in w.S:
-            c0 = w.q_cols[slot]
-            m.mosaic_sparse_gather_cols(w.S[lv], buf.YQ[:, c0: c0 + r[lv - 1]], M, buf.Y, subtract=True)
-    if y_f32 is not None:                    # dequantise the finished result (no product term)
+    gathers = [(slot, lv) for slot, lv in enumerate(w.slot_levels) if lv in w.S]
+    for k, (slot, lv) in enumerate(gathers):
+        c0 = w.q_cols[slot]
+        last = k == len(gathers) - 1         # the last gather also writes the dequantised output
+        m.mosaic_sparse_gather_cols(w.S[lv], buf.YQ[:, c0: c0 + r[lv - 1]], M, buf.Y, subtract=True,
+                                    y_f32=y_f32 if last else None, s_rows=s_rows if last else None,
+                                    s_cols=s_cols if last else None, bias=bias if last else None)
+    if y_f32 is not None and not gathers:    # dequantise the finished result (no product term)
         m.mosaic_unmask(buf.Y, None, None, None, M, w.N, 0, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32, bias=bias)
 
 

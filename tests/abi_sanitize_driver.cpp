@@ -127,7 +127,14 @@ int main() {
   EXPECT(mosaic_sparse_csr_fill(&sp, 4, 4, Fl, nullptr, Fu, nullptr), INV);
   EXPECT(mosaic_sparse_gather_rows(4, Fl, (int32_t*)F, Fu, Fu, 3, 4, Fu, 4, 0, nullptr), INV);
   EXPECT(mosaic_sparse_stream_gather_rows(&u, 4, 8, Fu, 4, 4, Fu, 4, 0, nullptr), INV);
-  EXPECT(mosaic_sparse_gather_cols(4, 4, Fl, (int32_t*)F, Fu, Fu, 4, Fu, 3, 0, nullptr), INV);
+  EXPECT(mosaic_sparse_gather_cols(4, 4, Fl, (int32_t*)F, Fu, Fu, 4, Fu, 3, 0, nullptr, nullptr, nullptr, nullptr, 0,
+                                   nullptr), INV);
+  EXPECT(mosaic_sparse_gather_cols(4, 4, Fl, (int32_t*)F, Fu, Fu, 4, Fu, 4, 0, nullptr, Ff, nullptr, Ff, 4,
+                                   nullptr), INV);     // y_f32 without s_rows
+  EXPECT(mosaic_sparse_gather_cols(4, 4, Fl, (int32_t*)F, Fu, Fu, 4, Fu, 4, 0, Ff, Ff, nullptr, Ff, 3,
+                                   nullptr), INV);     // ldf < N
+  EXPECT(mosaic_sparse_gather_cols(4, 4, Fl, (int32_t*)F, Fu, Fu, 4, Fu, 4, 0, nullptr, nullptr, Ff, nullptr, 0,
+                                   nullptr), INV);     // bias without y_f32
   EXPECT(mosaic_count_mismatches(Fu, 4, Fu, 4, 4, 4, nullptr, nullptr), INV);
   EXPECT(mosaic_count_mismatches(Fu, 3, Fu, 4, 4, 4, Fl, nullptr), INV);
   int64_t ops = 0;

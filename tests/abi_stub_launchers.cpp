@@ -18,7 +18,8 @@ hipError_t launch_sparse_gather_rows(int64_t, const int64_t*, const int32_t*, co
 hipError_t launch_sparse_stream_gather_rows(const RngArgs&, int64_t, int64_t, const uint32_t*, int64_t, int64_t,
                                             uint32_t*, int64_t, int, hipStream_t) STUB
 hipError_t launch_sparse_gather_cols(int64_t, int64_t, const int64_t*, const int32_t*, const uint32_t*,
-                                     const uint32_t*, int64_t, uint32_t*, int64_t, int, hipStream_t) STUB
+                                     const uint32_t*, int64_t, uint32_t*, int64_t, int, const Dequant&,
+                                     hipStream_t) STUB
 hipError_t launch_weighted_sample(const RngArgs&, int64_t, int64_t, uint32_t*, int64_t, int8_t*, int64_t,
                                   hipStream_t) STUB
 hipError_t launch_weighted_csr_count(int64_t, int64_t, int64_t*, hipStream_t) STUB

@@ -72,6 +72,25 @@ def test_gather_rows_and_cols(subtract):
     torch.cuda.synchronize()
     assert np.array_equal(to_np_u32(c1), want)
 
+    # the same gather writing the dequantised result too (with and without a
+    # bias): y = (c s_rows) s_cols (+ bias), each step rounded to fp32
+    for with_bias in (False, True):
+        c2 = to_dev_ring(C1)
+        sr = torch.rand(M, device="cuda") * 1e-3
+        sc = torch.rand(rows, device="cuda") * 1e-3
+        bias = torch.randn(rows, device="cuda") if with_bias else None
+        yf = torch.full((M, rows + 2), 7.0, device="cuda")
+        m.mosaic_sparse_gather_cols(p, dm[:, :r], M, c2, subtract=subtract, y_f32=yf[:, :rows], s_rows=sr,
+                                    s_cols=sc, bias=bias)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_np_u32(c2), want)
+        ref = (want.view(np.int32).astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+        if with_bias:
+            ref = (ref + bias.cpu().numpy()[None, :]).astype(np.float32)
+        got = yf.cpu().numpy()
+        assert np.array_equal(got[:, :rows], ref)
+        assert np.all(got[:, rows:] == 7.0)
+
 
 @pytest.mark.parametrize("rows,r,ncols,s", [(9, 300, 517, 3), (3, 5000, 70, 0), (4, 5000, 300, 6), (1, 1, 1, 0),
                                             (2, 64, 4096, 31)])
