@@ -901,9 +901,9 @@ def _cpu_model() -> str:
 
 
 def run_cpu_baseline():
-    """The oracle on the GPU machine's host cores (its plain C leg, OpenMP over
-    output rows; ``cores`` is the thread count OpenMP uses), on bounded
-    samples:
+    """The oracle on the host cores of the machine that runs the benchmark
+    (its plain C leg, OpenMP over output rows; ``cores`` is the thread count
+    OpenMP uses), on bounded samples:
 
     * the whole prefill call at the first shape, M = 2048, (K, N) = (8192,
       8192), rank 1536: Init X, mask, server product with Q, unmasking (Init
@@ -1011,6 +1011,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--extras-file", default=None,
+                    help="also write every extra measurement (the JSON line keeps a compact summary) to this file")
     ap.add_argument("--product-only", action="store_true",
                     help="only time the server ring product on uniform digits (for counter runs)")
     ap.add_argument("--passes-only", action="store_true",
@@ -1082,14 +1084,15 @@ def main():
     }
     if "extras" in gpu:
         line.update(_compact(gpu["extras"]))
-        path = os.path.join(ROOT, "gpurun_out", "bench_extras.json")
-        try:
-            os.makedirs(os.path.dirname(path), exist_ok=True)
-            with open(path, "w") as f:
-                json.dump(gpu["extras"], f, indent=1)
-            line["extras_file"] = os.path.relpath(path, ROOT)
-        except OSError:
-            pass
+        if args.extras_file:
+            path = os.path.abspath(args.extras_file)
+            try:
+                os.makedirs(os.path.dirname(path), exist_ok=True)
+                with open(path, "w") as f:
+                    json.dump(gpu["extras"], f, indent=1)
+                line["extras_file"] = args.extras_file
+            except OSError as err:
+                print(f"extras not written to {path}: {err}", file=sys.stderr)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = run_cpu_baseline()
     print(json.dumps(line), flush=True)
