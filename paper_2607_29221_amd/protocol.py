@@ -328,10 +328,11 @@ def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tens
     subtracted by gathering from Q_i's ring words."""
     r = list(w.params.ranks)
     sparse = w.sparse_call(M)
-    slots = w.slot_levels[:1] if sparse else w.slot_levels
-    for slot, lv in enumerate(slots):
-        c0 = w.q_cols[slot]
-        m.mosaic_mask(None, buf.YQ[:, c0: c0 + r[lv - 1]], None, M, r[lv - 1], out_dig=buf.Qdig[slot])
+    # digits of Q: the slots sit side by side in [Y' | Q] with the padded
+    # widths of Qdig, and the padding columns of Q are zero (Bext's padding
+    # rows are), so one pass converts every slot; sparse mode needs slot 0
+    qw = w.Rd if sparse else w.R
+    m.mosaic_mask(None, buf.YQ[:, w.q_cols[0]: w.q_cols[0] + qw], None, M, qw, out_dig=buf.Qdig[0].whole(qw))
     if not sparse:
         m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
                         M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32, bias=bias)
