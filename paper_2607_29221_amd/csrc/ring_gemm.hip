@@ -158,28 +158,22 @@ __device__ __forceinline__ void gemm_tile_atomic_add(const GemmLaunch& g, const 
 // tile full + p % split_tiles), each piece a contiguous range of stage
 // pairs, added into C atomically; C is cleared for those tiles first when the
 // result is stored (launch_ring_gemm).
-template <int EPI, int VEC>
+// SPLIT: compiled in only for launches with split tiles, so that the
+// whole-tile kernel keeps a compile-time stage origin of 0.
+template <int EPI, int VEC, bool SPLIT>
 __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   __shared__ __attribute__((aligned(1024))) char lds[NSTAGE * STAGE];
 
   const int64_t tiles_m = (g.M + BM - 1) / BM;
   const int64_t tiles_n = (g.N + BN - 1) / BN;
-  const int64_t full = tiles_m * tiles_n - g.split_tiles;
-  int64_t lin;
-  int s0 = 0;
-  int stages = (int)(g.Kp / BK);   // even: Kp is a multiple of 64
-  bool piece = false;
-  if ((int64_t)blockIdx.x < full) {
-    lin = xcd_order(blockIdx.x, full);
-  } else {
-    const int64_t p = (int64_t)blockIdx.x - full;
-    const int64_t q = p / g.split_tiles;
-    lin = full + (p - q * g.split_tiles);
-    const int64_t pairs = stages / 2;
-    s0 = 2 * (int)(pairs * q / g.split_k);
-    stages = 2 * (int)(pairs * (q + 1) / g.split_k) - s0;
-    piece = true;
-  }
+  const int64_t full = SPLIT ? tiles_m * tiles_n - g.split_tiles : tiles_m * tiles_n;
+  const int total = (int)(g.Kp / BK);   // even: Kp is a multiple of 64
+  const bool piece = SPLIT && (int64_t)blockIdx.x >= full;
+  const int64_t p = (int64_t)blockIdx.x - full;
+  const int64_t q = piece ? p / g.split_tiles : 0;
+  const int64_t lin = piece ? full + (p - q * g.split_tiles) : xcd_order(blockIdx.x, full);
+  const int s0 = piece ? 2 * (int)((int64_t)(total / 2) * q / g.split_k) : 0;
+  const int stages = piece ? 2 * (int)((int64_t)(total / 2) * (q + 1) / g.split_k) - s0 : total;
   const Tile tile = tile_at(lin, tiles_m, tiles_n);
   const int64_t m0 = tile.tm * BM;
   const int64_t n0 = tile.tn * BN;
@@ -414,15 +408,26 @@ hipError_t launch_ring_gemm(const GemmLaunch& g, EpilogueKind epi, hipStream_t s
     hipLaunchKernelGGL(clear_split_tiles_kernel, dim3((unsigned)gs.split_tiles), dim3(256), 0, s, gs);
   const dim3 grid((unsigned)(tiles + gs.split_tiles * (gs.split_k - 1)));
   const bool vec = gemm_epilogue_vectorizable(g, epi);
+  const bool split = gs.split_tiles > 0;
   if (epi == EPI_STORE) {
-    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 1>), grid, dim3(NTHREADS), 0, s, gs);
-    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 0>), grid, dim3(NTHREADS), 0, s, gs);
+    if (split) {
+      if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 1, true>), grid, dim3(NTHREADS), 0, s, gs);
+      else hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 0, true>), grid, dim3(NTHREADS), 0, s, gs);
+    } else {
+      if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 1, false>), grid, dim3(NTHREADS), 0, s, gs);
+      else hipLaunchKernelGGL((ring_gemm_kernel<EPI_STORE, 0, false>), grid, dim3(NTHREADS), 0, s, gs);
+    }
   } else if (epi == EPI_ACCUM) {
-    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 1>), grid, dim3(NTHREADS), 0, s, gs);
-    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 0>), grid, dim3(NTHREADS), 0, s, gs);
+    if (split) {
+      if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 1, true>), grid, dim3(NTHREADS), 0, s, gs);
+      else hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 0, true>), grid, dim3(NTHREADS), 0, s, gs);
+    } else {
+      if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 1, false>), grid, dim3(NTHREADS), 0, s, gs);
+      else hipLaunchKernelGGL((ring_gemm_kernel<EPI_ACCUM, 0, false>), grid, dim3(NTHREADS), 0, s, gs);
+    }
   } else {
-    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 1>), grid, dim3(NTHREADS), 0, s, gs);
-    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 0>), grid, dim3(NTHREADS), 0, s, gs);
+    if (vec) hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 1, false>), grid, dim3(NTHREADS), 0, s, gs);
+    else hipLaunchKernelGGL((ring_gemm_kernel<EPI_UNMASK, 0, false>), grid, dim3(NTHREADS), 0, s, gs);
   }
   return hipGetLastError();
 }
