@@ -191,3 +191,29 @@ def test_count_mismatches(rows, cols, ld):
     m.mosaic_count_mismatches(da, db, count)
     torch.cuda.synchronize()
     assert int(count.item()) == int(flip.sum())
+
+
+@pytest.mark.parametrize("M,K,N,t", [(16, 33000, 512, 1), (5, 64, 32768, 64), (1, 4096, 4096, 32)],
+                         ids=["key-chunks-t1", "check-chunks-t64", "one-token"])
+def test_check_chunks_and_vector_counts(M, K, N, t):
+    """The one-call check where an inner dimension exceeds one launch's range
+    (K = 33000: the key product in two chunks; N + R = 32896: the check
+    product in two chunks), with 1 and 64 check vectors and for one token:
+    honest outputs give an all-zero d; one changed output is caught by the
+    vectors whose entry times the change is non-zero, and d holds exactly
+    that column's entries."""
+    p = PARAMS_D1_SMALL_R128
+    A, W = int8_operands(M, K, N, 9)
+    seed = 31337
+    w = gproto.MaskedWeight(torch.from_numpy(W).cuda(), p, seed, weight_id=5, check_vectors=t)
+    buf = gproto.run_call(w, torch.from_numpy(A).cuda(), call_id=3)
+    assert int(gproto.verify(w, M, buf).item()) == 0
+    assert not np.any(to_np_u32(buf.check_diff))
+    aW, _ = integ.check_vectors(t, N, list(p.ranks), seed, 5)
+    col, delta = N - 1, 0x01000001
+    _add_host(buf.YQ, M - 1, col, delta)
+    got = int(gproto.verify(w, M, buf).item())
+    expect = np.zeros((t, M), dtype=np.uint64)
+    expect[:, M - 1] = (2 ** 32 - (aW[:, col].astype(np.uint64) * delta) % 2 ** 32) % 2 ** 32
+    assert np.array_equal(to_np_u32(buf.check_diff), expect.astype(np.uint32))
+    assert got == int(np.count_nonzero(expect[:, M - 1]))
