@@ -35,7 +35,7 @@
 // output buffer of the call (y, else y_f32) shares no memory with any input,
 // the product is computed into that buffer by the shared-A kernel and an
 // elementwise pass then forms y = ym - kc - product in place. Otherwise
-// ring_gemm_skinny_unmask_kernel runs: one workgroup per column tile of 32
+// ring_gemm_skinny_ksplit_kernel runs: one workgroup per column tile of 32
 // (A of at most 16 rows) or 64 rows of B computes the whole K range, its 4
 // waves splitting the stages, streaming their part of B straight into
 // registers and summing their partial products in LDS before the epilogue.
@@ -329,8 +329,8 @@ __device__ __forceinline__ void transpose4(v4i (&q)[4]) {
 // one set only. Prefetches past the wave's last stage are clamped to that
 // stage: the duplicate request hits in cache and the loop needs no branches
 // around loads. K must be non-zero.
-template <int MT, int NT, int S, int W>
-__global__ __launch_bounds__(64 * W) void ring_gemm_skinny_unmask_kernel(GemmLaunch g) {
+template <int EPI, int MT, int NT, int S, int W>
+__global__ __launch_bounds__(64 * W) void ring_gemm_skinny_ksplit_kernel(GemmLaunch g) {
   constexpr int NOUT = MT * NT * 4;   // output registers per lane
   __shared__ uint32_t red[W][NOUT][64];
   const int lane = threadIdx.x & 63;
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(64 * W) void ring_gemm_skinny_unmask_kernel(GemmLau
     const int i = q / (NT * 4), j = (q / 4) % NT, v = q % 4;
     const int64_t m = i * 16 + 4 * (l >> 4) + v;
     const int64_t n = n0 + j * 16 + (l & 15);
-    if (m < g.M && n < g.N) gemm_epilogue<EPI_UNMASK>(g, m, n, val);
+    if (m < g.M && n < g.N) gemm_epilogue<EPI>(g, m, n, val);
   }
 }
 
@@ -511,10 +511,11 @@ uint32_t* unmask_scratch(const GemmLaunch& g, int64_t* ld) {
   return nullptr;
 }
 
-template <int MT, int NT, int S, int W>
-hipError_t launch_unmask(const GemmLaunch& g, hipStream_t s) {
+template <int EPI, int MT, int NT, int S, int W>
+hipError_t launch_ksplit(const GemmLaunch& g, hipStream_t s) {
   const int64_t tiles = (g.N + 16 * NT - 1) / (16 * NT);
-  hipLaunchKernelGGL((ring_gemm_skinny_unmask_kernel<MT, NT, S, W>), dim3((unsigned)tiles), dim3(64 * W), 0, s, g);
+  hipLaunchKernelGGL((ring_gemm_skinny_ksplit_kernel<EPI, MT, NT, S, W>), dim3((unsigned)tiles), dim3(64 * W), 0, s,
+                     g);
   return hipGetLastError();
 }
 
@@ -575,10 +576,10 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
     // compute unit idle (one row, 2048 x 1536 factor: 7.6 against 10.9 us).
     // For one row, 8 or 16 waves and 3 to 6 stages in flight were slower at
     // every size tried (factors of 12-96 MiB: by 4-50%).
-    if (mt <= 1 && g.N <= 16 * compute_units()) return launch_unmask<1, 1, 2, 4>(g, s);
-    if (mt <= 1) return launch_unmask<1, 2, 2, 4>(g, s);
-    if (mt == 2) return launch_unmask<2, 4, 1, 4>(g, s);
-    return launch_unmask<4, 4, 1, 4>(g, s);
+    if (mt <= 1 && g.N <= 16 * compute_units()) return launch_ksplit<EPI_UNMASK, 1, 1, 2, 4>(g, s);
+    if (mt <= 1) return launch_ksplit<EPI_UNMASK, 1, 2, 2, 4>(g, s);
+    if (mt == 2) return launch_ksplit<EPI_UNMASK, 2, 4, 1, 4>(g, s);
+    return launch_ksplit<EPI_UNMASK, 4, 4, 1, 4>(g, s);
   }
   // MT: 16-row tiles of A (33-64 rows padded to 64: faster than 48 rows on
   // one row of waves); WM: rows of 4 waves
