@@ -371,7 +371,7 @@ def verify(w: MaskedWeight, M: int, buf: CallBuffers, sides: bool = False) -> to
         d = _ring_empty(t, M, dev)
         count = torch.empty(1, dtype=torch.int64, device=dev)
         m.mosaic_integrity_check(w.cT, buf.A_masked, w.aWQ, buf.YQ, t, M, w.K, w.N + w.R, d, count)
-        buf.check_diff = d
+        buf.check_diff, buf.check = d, None
         return count
     lhs = _ring_empty(t, M, dev)
     m.mosaic_masked_matmul(w.cT, buf.A_masked, t, M, w.K, lhs)
@@ -383,7 +383,7 @@ def verify(w: MaskedWeight, M: int, buf: CallBuffers, sides: bool = False) -> to
         m.mosaic_masked_matmul_words(w.aQ_all, buf.YQ[:, w.N: w.N + w.R], t, M, w.R, rhs, accumulate=True)
         count = torch.empty(1, dtype=torch.int64, device=dev)
         m.mosaic_count_mismatches(lhs, rhs, count)
-        buf.check = (lhs, rhs)
+        buf.check, buf.check_diff = (lhs, rhs), None
         return count
     Ydig = Digits.empty(M, w.N, dev)
     m.mosaic_mask(None, buf.YQ[:, : w.N], None, M, w.N, out_dig=Ydig)
@@ -399,7 +399,7 @@ def verify(w: MaskedWeight, M: int, buf: CallBuffers, sides: bool = False) -> to
     m.mosaic_mask(ry, rq, None, t, M, out=rhs)
     count = torch.empty(1, dtype=torch.int64, device=dev)
     m.mosaic_count_mismatches(lhs, rhs, count)
-    buf.check = (lhs, rhs)
+    buf.check, buf.check_diff = (lhs, rhs), None
     return count
 
 
