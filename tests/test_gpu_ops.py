@@ -125,14 +125,38 @@ def test_masked_matmul(M, N, K):
     assert np.array_equal(got, ring_matmul(a, b.T))
 
 
-@pytest.mark.parametrize("M,N,K", [(200, 1000, 4096), (130, 3000, 2048)])
+@pytest.mark.parametrize("M,N,K", [(200, 1000, 4096), (130, 3000, 2048), (200, 1001, 4096), (65, 130, 512),
+                                   (300, 4099, 640)])
 def test_masked_matmul_mid_size(M, N, K):
     """Tiled-kernel products with fewer tiles than compute units and a long
-    K range, checked in full."""
+    K range, checked in full: the tiles run as split-K pieces added
+    atomically after a clear of their outputs (2-8 pieces; N = 1001 and 4099
+    take the one-word epilogue paths, 65 x 130 x 512 the smallest pieces)."""
     rng = _rng_np(M + N + K)
     a = _random_ring(rng, (M, K), edge=True)
     b = _random_ring(rng, (N, K), edge=True)
     assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
+
+
+def test_masked_matmul_split_output_window():
+    """Split-K pieces writing into a window of a wider C (ldc > N, a column
+    offset): the clear before a store and the atomic adds touch only the
+    window; K past one launch's range makes the second chunk accumulate, in
+    two pieces per tile."""
+    M, N, K = 150, 203, 33000
+    rng = _rng_np(5)
+    a = _random_ring(rng, (M, K))
+    b = _random_ring(rng, (N, K))
+    A, B = Digits.empty(M, K), Digits.empty(N, K)
+    m.mosaic_mask(to_dev_ring(a), None, None, M, K, out_dig=A)
+    m.mosaic_mask(to_dev_ring(b), None, None, N, K, out_dig=B)
+    C0 = _random_ring(rng, (M, N + 9))
+    C = to_dev_ring(C0)
+    m.mosaic_masked_matmul(A, B, M, N, K, C[:, 3:3 + N])
+    torch.cuda.synchronize()
+    got = to_np_u32(C)
+    assert np.array_equal(got[:, 3:3 + N], ring_matmul(a, b.T))
+    assert np.array_equal(got[:, :3], C0[:, :3]) and np.array_equal(got[:, 3 + N:], C0[:, 3 + N:])
 
 
 @pytest.mark.parametrize("M", [1, 8, 15, 16, 17, 33, 48, 63, 64, 65])
