@@ -455,7 +455,7 @@ mosaic_status mosaic_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, co
   if (row_ptr == nullptr || col_idx == nullptr || values == nullptr || d == nullptr || c == nullptr)
     return fail(MOSAIC_ERR_INVALID_ARG, "NULL operand");
   if (ldd < ncols || ldc < ncols) return fail(MOSAIC_ERR_INVALID_ARG, "leading dimension < ncols");
-  if (rows > 0x7FFFFFFF || (ncols + 255) / 256 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
+  if (rows > 0x7FFFFFFF || (ncols + 63) / 64 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
   return hip_status(launch_sparse_gather_rows(rows, row_ptr, col_idx, values, d, ldd, ncols, c, ldc, subtract != 0,
                                               (hipStream_t)stream), "sparse gather launch");
 }
@@ -470,7 +470,7 @@ mosaic_status mosaic_sparse_stream_gather_rows(const mosaic_rng* rng, int64_t ro
   RngArgs a{};
   mosaic_status st = check_lpn_rng(rng, rcols, &a);
   if (st != MOSAIC_OK) return st;
-  if (rows > 0x7FFFFFFF || (ncols + 255) / 256 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
+  if (rows > 0x7FFFFFFF || (ncols + 63) / 64 > 65535) return fail(MOSAIC_ERR_UNSUPPORTED, "too large for one launch");
   return hip_status(launch_sparse_stream_gather_rows(a, rows, rcols, d, ldd, ncols, c, ldc, subtract != 0,
                                                      (hipStream_t)stream), "sparse gather launch");
 }

@@ -180,15 +180,18 @@ __global__ __launch_bounds__(256) void sparse_fill_kernel(RngArgs r, int64_t row
   }
 }
 
-// c[i][k] +-= sum_j P(i, j) d[j][k] for k < ncols. A workgroup owns 256
+// c[i][k] +-= sum_j P(i, j) d[j][k] for k < ncols. A workgroup owns 64
 // consecutive k of one row i. The row's nonzeros are staged in LDS in chunks
 // of CH entries -- copied from compressed rows (STREAM = 0), drawn from the
 // SPARSE stream of rng over the row's rcols columns (STREAM = 1: each wave
 // appends its nonzeros through an LDS counter; the ring sum does not depend
 // on their order) or drawn as the t entries of a WEIGHT row (STREAM = 2, one
-// chunk: t <= CH; the shuffle's scratch is dynamic LDS) -- and every thread
-// then runs over the staged entries, which are LDS broadcasts, with several
-// independent loads of d in flight.
+// chunk: t <= CH; the shuffle's scratch is dynamic LDS). Wave w then takes
+// staged entries w, w + 4, ... (LDS broadcasts), each of its lanes one k, so
+// a load instruction reads 256 consecutive bytes of a row of d and the four
+// waves' loads are in flight together; the waves' partial sums meet in LDS.
+// (With 256 k per workgroup and every thread running over all entries, one
+// token against an 8192-column d had 32 workgroups and took 8.4 us.)
 template <int STREAM>
 __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rcols, const int64_t* row_ptr,
                                                           const int32_t* col_idx, const uint32_t* values,
@@ -197,10 +200,12 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rco
   constexpr int CH = 2048;
   __shared__ int32_t scol[CH];
   __shared__ uint32_t sval[CH];
+  __shared__ uint32_t part[4][64];
   __shared__ int scount;
   const int tid = threadIdx.x;
+  const int wave = tid >> 6;
   const int64_t i = blockIdx.x;
-  const int64_t k = (int64_t)blockIdx.y * 256 + tid;
+  const int64_t k = (int64_t)blockIdx.y * 64 + (tid & 63);
   const bool active = k < ncols;
   const uint32_t* dk = d + (active ? k : 0);
   const int64_t lo = STREAM ? 0 : row_ptr[i];
@@ -242,19 +247,22 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rco
       n = (int)(end - base);
     }
     if (active) {
-      int q = 0;
-      for (; q + 4 <= n; q += 4) {
-        const uint32_t a0 = dk[(int64_t)scol[q] * ldd], a1 = dk[(int64_t)scol[q + 1] * ldd];
-        const uint32_t a2 = dk[(int64_t)scol[q + 2] * ldd], a3 = dk[(int64_t)scol[q + 3] * ldd];
-        acc += sval[q] * a0 + sval[q + 1] * a1 + sval[q + 2] * a2 + sval[q + 3] * a3;
+      int q = wave;
+      for (; q + 12 < n; q += 16) {
+        const uint32_t a0 = dk[(int64_t)scol[q] * ldd], a1 = dk[(int64_t)scol[q + 4] * ldd];
+        const uint32_t a2 = dk[(int64_t)scol[q + 8] * ldd], a3 = dk[(int64_t)scol[q + 12] * ldd];
+        acc += sval[q] * a0 + sval[q + 4] * a1 + sval[q + 8] * a2 + sval[q + 12] * a3;
       }
-      for (; q < n; ++q) acc += sval[q] * dk[(int64_t)scol[q] * ldd];
+      for (; q < n; q += 4) acc += sval[q] * dk[(int64_t)scol[q] * ldd];
     }
     __syncthreads();                                   // before the next chunk overwrites the staging
   }
-  if (active) {
+  part[wave][tid & 63] = acc;
+  __syncthreads();
+  if (wave == 0 && active) {
+    const uint32_t sum = part[0][tid] + part[1][tid] + part[2][tid] + part[3][tid];
     uint32_t* out = c + i * ldc + k;
-    *out = subtract ? *out - acc : *out + acc;
+    *out = subtract ? *out - sum : *out + sum;
   }
 }
 
@@ -312,7 +320,7 @@ hipError_t launch_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const
                                      const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
                                      uint32_t* c, int64_t ldc, int subtract, hipStream_t s) {
   if (rows == 0 || ncols == 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_rows_kernel<0>, dim3((unsigned)rows, (unsigned)((ncols + 255) / 256)), dim3(256), 0, s,
+  hipLaunchKernelGGL(gather_rows_kernel<0>, dim3((unsigned)rows, (unsigned)((ncols + 63) / 64)), dim3(256), 0, s,
                      RngArgs{}, (int64_t)0, row_ptr, col_idx, values, d, ldd, ncols, c, ldc, subtract);
   return hipGetLastError();
 }
@@ -321,7 +329,7 @@ hipError_t launch_sparse_stream_gather_rows(const RngArgs& r, int64_t rows, int6
                                             int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc, int subtract,
                                             hipStream_t s) {
   if (rows == 0 || ncols == 0 || rcols == 0) return hipSuccess;
-  const dim3 grid((unsigned)rows, (unsigned)((ncols + 255) / 256));
+  const dim3 grid((unsigned)rows, (unsigned)((ncols + 63) / 64));
   if (r.dist == 4) {
     if (r.row_weight == 0) return hipSuccess;
     // perm (rcols uint16, rounded up to words), then u (t words)
