@@ -180,19 +180,21 @@ __global__ __launch_bounds__(256) void sparse_fill_kernel(RngArgs r, int64_t row
   }
 }
 
-// c[i][k] +-= sum_j P(i, j) d[j][k] for k < ncols. A workgroup owns 64
-// consecutive k of one row i. The row's nonzeros are staged in LDS in chunks
+// c[i][k] +-= sum_j P(i, j) d[j][k] for k < ncols. A workgroup owns
+// 256 / NSPLIT consecutive k of one row i. The row's nonzeros are staged in LDS in chunks
 // of CH entries -- copied from compressed rows (STREAM = 0), drawn from the
 // SPARSE stream of rng over the row's rcols columns (STREAM = 1: each wave
 // appends its nonzeros through an LDS counter; the ring sum does not depend
 // on their order) or drawn as the t entries of a WEIGHT row (STREAM = 2, one
-// chunk: t <= CH; the shuffle's scratch is dynamic LDS). Wave w then takes
-// staged entries w, w + 4, ... (LDS broadcasts), each of its lanes one k, so
-// a load instruction reads 256 consecutive bytes of a row of d and the four
-// waves' loads are in flight together; the waves' partial sums meet in LDS.
-// (With 256 k per workgroup and every thread running over all entries, one
-// token against an 8192-column d had 32 workgroups and took 8.4 us.)
-template <int STREAM>
+// chunk: t <= CH; the shuffle's scratch is dynamic LDS). Each lane takes one
+// k, so a load instruction reads 256 consecutive bytes of a row of d; the
+// NSPLIT waves that share 64 k split the staged entries (wave w takes
+// entries w % NSPLIT, + NSPLIT, ..., LDS broadcasts) and their partial sums
+// meet in LDS. NSPLIT = 4 gives rows with few workgroups four times as many
+// (one token against an 8192-column d: 128 instead of 32 workgroups, 8.4 us
+// before); with many rows NSPLIT = 1 keeps the per-workgroup staging (for a
+// WEIGHT row, a serial shuffle) from being repeated four times as often.
+template <int STREAM, int NSPLIT>
 __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rcols, const int64_t* row_ptr,
                                                           const int32_t* col_idx, const uint32_t* values,
                                                           const uint32_t* d, int64_t ldd, int64_t ncols,
@@ -202,10 +204,11 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rco
   __shared__ uint32_t sval[CH];
   __shared__ uint32_t part[4][64];
   __shared__ int scount;
+  static_assert(NSPLIT == 1 || NSPLIT == 2 || NSPLIT == 4, "waves per column group");
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int64_t i = blockIdx.x;
-  const int64_t k = (int64_t)blockIdx.y * 64 + (tid & 63);
+  const int64_t k = (int64_t)blockIdx.y * (256 / NSPLIT) + (wave / NSPLIT) * 64 + (tid & 63);
   const bool active = k < ncols;
   const uint32_t* dk = d + (active ? k : 0);
   const int64_t lo = STREAM ? 0 : row_ptr[i];
@@ -247,52 +250,80 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rco
       n = (int)(end - base);
     }
     if (active) {
-      int q = wave;
-      for (; q + 12 < n; q += 16) {
-        const uint32_t a0 = dk[(int64_t)scol[q] * ldd], a1 = dk[(int64_t)scol[q + 4] * ldd];
-        const uint32_t a2 = dk[(int64_t)scol[q + 8] * ldd], a3 = dk[(int64_t)scol[q + 12] * ldd];
-        acc += sval[q] * a0 + sval[q + 4] * a1 + sval[q + 8] * a2 + sval[q + 12] * a3;
+      constexpr int ST = NSPLIT;
+      int q = wave % NSPLIT;
+      for (; q + 3 * ST < n; q += 4 * ST) {
+        const uint32_t a0 = dk[(int64_t)scol[q] * ldd], a1 = dk[(int64_t)scol[q + ST] * ldd];
+        const uint32_t a2 = dk[(int64_t)scol[q + 2 * ST] * ldd], a3 = dk[(int64_t)scol[q + 3 * ST] * ldd];
+        acc += sval[q] * a0 + sval[q + ST] * a1 + sval[q + 2 * ST] * a2 + sval[q + 3 * ST] * a3;
       }
-      for (; q < n; q += 4) acc += sval[q] * dk[(int64_t)scol[q] * ldd];
+      for (; q < n; q += ST) acc += sval[q] * dk[(int64_t)scol[q] * ldd];
     }
     __syncthreads();                                   // before the next chunk overwrites the staging
   }
-  part[wave][tid & 63] = acc;
-  __syncthreads();
-  if (wave == 0 && active) {
-    const uint32_t sum = part[0][tid] + part[1][tid] + part[2][tid] + part[3][tid];
+  if (NSPLIT > 1) {
+    part[wave][tid & 63] = acc;
+    __syncthreads();
+    if (wave % NSPLIT != 0) return;
+#pragma unroll
+    for (int w = 1; w < NSPLIT; ++w) acc += part[wave + w][tid & 63];
+  }
+  if (active) {
     uint32_t* out = c + i * ldc + k;
-    *out = subtract ? *out - sum : *out + sum;
+    *out = subtract ? *out - acc : *out + acc;
   }
 }
 
+// Waves per 64 columns of the row gathers: split a row's entries between
+// four waves while that keeps the workgroup count under four per compute
+// unit, else one wave per 64 columns.
+int gather_split(int64_t rows, int64_t ncols) {
+  return rows * ((ncols + 63) / 64) <= 4 * (int64_t)compute_units() ? 4 : 1;
+}
+
 // c[m][n] +-= sum_{p in row n} values[p] * d[m][col_idx[p]]. A workgroup owns
-// 32 consecutive n of one row m; eight lanes share each n and split its
-// nonzeros, so a row's entries are read in a few coalesced rounds, then the
-// eight partial sums are combined with lane shuffles.
-__global__ __launch_bounds__(256) void gather_cols_kernel(int64_t N, const int64_t* row_ptr, const int32_t* col_idx,
-                                                          const uint32_t* values, const uint32_t* d, int64_t ldd,
-                                                          uint32_t* c, int64_t ldc, int subtract, Dequant dq) {
-  const int64_t m = blockIdx.x;
+// 32 consecutive n and MB consecutive m; eight lanes share each n and split
+// its nonzeros, so a row's entries are read once, in a few coalesced rounds,
+// for MB rows of d (with one m per workgroup, 8 tokens against a 14336-row P
+// with 80 entries per row re-read the entries 8 times: 23-25 us), then the
+// eight partial sums of each m are combined with lane shuffles.
+template <int MB>
+__global__ __launch_bounds__(256) void gather_cols_kernel(int64_t M, int64_t N, const int64_t* row_ptr,
+                                                          const int32_t* col_idx, const uint32_t* values,
+                                                          const uint32_t* d, int64_t ldd, uint32_t* c, int64_t ldc,
+                                                          int subtract, Dequant dq) {
+  const int64_t m0 = (int64_t)blockIdx.x * MB;
   const int sub = threadIdx.x & 7;
   const int64_t n = (int64_t)blockIdx.y * 32 + (threadIdx.x >> 3);
-  uint32_t acc = 0;
+  uint32_t acc[MB];
+#pragma unroll
+  for (int mm = 0; mm < MB; ++mm) acc[mm] = 0;
   if (n < N) {
     const int64_t p0 = row_ptr[n], p1 = row_ptr[n + 1];
-    const uint32_t* dr = d + m * ldd;
-    for (int64_t p = p0 + sub; p < p1; p += 8) acc += values[p] * dr[col_idx[p]];
+    for (int64_t p = p0 + sub; p < p1; p += 8) {
+      const uint32_t v = values[p];
+      const int64_t col = col_idx[p];
+#pragma unroll
+      for (int mm = 0; mm < MB; ++mm)
+        if (m0 + mm < M) acc[mm] += v * d[(m0 + mm) * ldd + col];
+    }
   }
-  acc += __shfl_xor(acc, 4, 8);
-  acc += __shfl_xor(acc, 2, 8);
-  acc += __shfl_xor(acc, 1, 8);
-  if (n < N && sub == 0) {
-    uint32_t* out = c + m * ldc + n;
-    const uint32_t v = subtract ? *out - acc : *out + acc;
-    *out = v;
-    if (dq.y != nullptr) {
-      // the same steps and roundings as the unmask epilogue's dequantisation
-      const float f = (float)(int32_t)v * dq.s_rows[m] * dq.s_cols[n];
-      dq.y[m * dq.ld + n] = dq.bias != nullptr ? __fadd_rn(f, dq.bias[n]) : f;
+#pragma unroll
+  for (int mm = 0; mm < MB; ++mm) {
+    uint32_t a = acc[mm];
+    a += __shfl_xor(a, 4, 8);
+    a += __shfl_xor(a, 2, 8);
+    a += __shfl_xor(a, 1, 8);
+    const int64_t m = m0 + mm;
+    if (n < N && sub == 0 && m < M) {
+      uint32_t* out = c + m * ldc + n;
+      const uint32_t val = subtract ? *out - a : *out + a;
+      *out = val;
+      if (dq.y != nullptr) {
+        // the same steps and roundings as the unmask epilogue's dequantisation
+        const float f = (float)(int32_t)val * dq.s_rows[m] * dq.s_cols[n];
+        dq.y[m * dq.ld + n] = dq.bias != nullptr ? __fadd_rn(f, dq.bias[n]) : f;
+      }
     }
   }
 }
@@ -320,8 +351,12 @@ hipError_t launch_sparse_gather_rows(int64_t rows, const int64_t* row_ptr, const
                                      const uint32_t* values, const uint32_t* d, int64_t ldd, int64_t ncols,
                                      uint32_t* c, int64_t ldc, int subtract, hipStream_t s) {
   if (rows == 0 || ncols == 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_rows_kernel<0>, dim3((unsigned)rows, (unsigned)((ncols + 63) / 64)), dim3(256), 0, s,
-                     RngArgs{}, (int64_t)0, row_ptr, col_idx, values, d, ldd, ncols, c, ldc, subtract);
+  if (gather_split(rows, ncols) == 4)
+    hipLaunchKernelGGL((gather_rows_kernel<0, 4>), dim3((unsigned)rows, (unsigned)((ncols + 63) / 64)), dim3(256), 0,
+                       s, RngArgs{}, (int64_t)0, row_ptr, col_idx, values, d, ldd, ncols, c, ldc, subtract);
+  else
+    hipLaunchKernelGGL((gather_rows_kernel<0, 1>), dim3((unsigned)rows, (unsigned)((ncols + 255) / 256)), dim3(256),
+                       0, s, RngArgs{}, (int64_t)0, row_ptr, col_idx, values, d, ldd, ncols, c, ldc, subtract);
   return hipGetLastError();
 }
 
@@ -329,16 +364,28 @@ hipError_t launch_sparse_stream_gather_rows(const RngArgs& r, int64_t rows, int6
                                             int64_t ldd, int64_t ncols, uint32_t* c, int64_t ldc, int subtract,
                                             hipStream_t s) {
   if (rows == 0 || ncols == 0 || rcols == 0) return hipSuccess;
-  const dim3 grid((unsigned)rows, (unsigned)((ncols + 63) / 64));
+  const bool split = gather_split(rows, ncols) == 4;
+  const dim3 grid((unsigned)rows, (unsigned)(split ? (ncols + 63) / 64 : (ncols + 255) / 256));
+  const int64_t* np = nullptr;
+  const int32_t* ni = nullptr;
+  const uint32_t* nv = nullptr;
   if (r.dist == 4) {
     if (r.row_weight == 0) return hipSuccess;
     // perm (rcols uint16, rounded up to words), then u (t words)
     const size_t lds = (size_t)(4 * ((rcols + 1) / 2) + 4 * r.row_weight);
-    hipLaunchKernelGGL(gather_rows_kernel<2>, grid, dim3(256), lds, s, r, rcols, (const int64_t*)nullptr,
-                       (const int32_t*)nullptr, (const uint32_t*)nullptr, d, ldd, ncols, c, ldc, subtract);
+    if (split)
+      hipLaunchKernelGGL((gather_rows_kernel<2, 4>), grid, dim3(256), lds, s, r, rcols, np, ni, nv, d, ldd, ncols, c,
+                         ldc, subtract);
+    else
+      hipLaunchKernelGGL((gather_rows_kernel<2, 1>), grid, dim3(256), lds, s, r, rcols, np, ni, nv, d, ldd, ncols, c,
+                         ldc, subtract);
   } else {
-    hipLaunchKernelGGL(gather_rows_kernel<1>, grid, dim3(256), 0, s, r, rcols, (const int64_t*)nullptr,
-                       (const int32_t*)nullptr, (const uint32_t*)nullptr, d, ldd, ncols, c, ldc, subtract);
+    if (split)
+      hipLaunchKernelGGL((gather_rows_kernel<1, 4>), grid, dim3(256), 0, s, r, rcols, np, ni, nv, d, ldd, ncols, c,
+                         ldc, subtract);
+    else
+      hipLaunchKernelGGL((gather_rows_kernel<1, 1>), grid, dim3(256), 0, s, r, rcols, np, ni, nv, d, ldd, ncols, c,
+                         ldc, subtract);
   }
   return hipGetLastError();
 }
@@ -369,8 +416,25 @@ hipError_t launch_sparse_gather_cols(int64_t M, int64_t N, const int64_t* row_pt
                                      const uint32_t* values, const uint32_t* d, int64_t ldd, uint32_t* c,
                                      int64_t ldc, int subtract, const Dequant& dq, hipStream_t s) {
   if (M == 0 || N == 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_cols_kernel, dim3((unsigned)M, (unsigned)((N + 31) / 32)), dim3(256), 0, s, N,
-                     row_ptr, col_idx, values, d, ldd, c, ldc, subtract, dq);
+  const unsigned nb = (unsigned)((N + 31) / 32);
+  // rows of d per workgroup: as many as keep four workgroups per compute
+  // unit (up to 16), so that a row's entries are read fewer times without
+  // losing the parallelism the short rows need
+  int mb = 1;
+  while (mb < 16 && mb < M && ((M + 2 * mb - 1) / (2 * mb)) * (int64_t)nb >= 4 * (int64_t)compute_units()) mb *= 2;
+  const dim3 grid((unsigned)((M + mb - 1) / mb), nb);
+  switch (mb) {
+    case 1: hipLaunchKernelGGL((gather_cols_kernel<1>), grid, dim3(256), 0, s, M, N, row_ptr, col_idx, values, d,
+                               ldd, c, ldc, subtract, dq); break;
+    case 2: hipLaunchKernelGGL((gather_cols_kernel<2>), grid, dim3(256), 0, s, M, N, row_ptr, col_idx, values, d,
+                               ldd, c, ldc, subtract, dq); break;
+    case 4: hipLaunchKernelGGL((gather_cols_kernel<4>), grid, dim3(256), 0, s, M, N, row_ptr, col_idx, values, d,
+                               ldd, c, ldc, subtract, dq); break;
+    case 8: hipLaunchKernelGGL((gather_cols_kernel<8>), grid, dim3(256), 0, s, M, N, row_ptr, col_idx, values, d,
+                               ldd, c, ldc, subtract, dq); break;
+    default: hipLaunchKernelGGL((gather_cols_kernel<16>), grid, dim3(256), 0, s, M, N, row_ptr, col_idx, values, d,
+                                ldd, c, ldc, subtract, dq); break;
+  }
   return hipGetLastError();
 }
 

@@ -93,11 +93,13 @@ def test_gather_rows_and_cols(subtract):
 
 
 @pytest.mark.parametrize("rows,r,ncols,s", [(9, 300, 517, 3), (3, 5000, 70, 0), (4, 5000, 300, 6), (1, 1, 1, 0),
-                                            (2, 64, 4096, 31)])
+                                            (2, 64, 4096, 31), (40, 700, 2000, 2), (6, 2100, 13000, 0)])
 @pytest.mark.parametrize("subtract", [False, True])
 def test_stream_gather_rows_and_long_rows(rows, r, ncols, s, subtract):
     """Rows drawn inside the gather, and compressed rows longer than one LDS
-    staging chunk (density 1 over 5000 columns)."""
+    staging chunk (density 1 over 5000 columns); few rows split their entries
+    between four waves per 64 columns, 40 x 2000 and 6 x 13000 (more than
+    four workgroups per compute unit) take one wave per 64 columns."""
     rng = np.random.default_rng(rows * r + ncols)
     seed, stream, inst = 12, 0x43, 5
     P = smp.sample_matrix("sparse", rows, r, seed, stream, inst, log2_inv_density=s)
@@ -113,6 +115,29 @@ def test_stream_gather_rows_and_long_rows(rows, r, ncols, s, subtract):
     torch.cuda.synchronize()
     assert np.array_equal(to_np_u32(c), want)
     assert np.array_equal(to_np_u32(c2), want)
+
+
+@pytest.mark.parametrize("M", [1, 3, 4, 5, 16, 17])
+@pytest.mark.parametrize("kind", ["sparse", "weight"])
+def test_gather_cols_token_blocks(M, kind):
+    """The column gather for 1 to 17 rows of d (one workgroup covers all rows
+    up to 16), against the oracle's product, with a WEIGHT matrix of 80
+    entries per row and a Bernoulli one."""
+    rows, r = 1000, 1024
+    rng = np.random.default_rng(M * 7 + len(kind))
+    if kind == "weight":
+        rr = m.rng(44, 0x45, 2, m.DIST_WEIGHT, row_weight=80)
+        P = smp.sample_matrix("weight", rows, r, 44, 0x45, 2, row_weight=80)
+    else:
+        rr = m.rng(44, 0x45, 2, m.DIST_SPARSE, log2_inv_density=4)
+        P = smp.sample_matrix("sparse", rows, r, 44, 0x45, 2, log2_inv_density=4)
+    p = m.mosaic_sparse_csr(rr, rows, r)
+    D = rng.integers(0, 2 ** 32, (M, r + 3), dtype=np.uint32)
+    C0 = rng.integers(0, 2 ** 32, (M, rows), dtype=np.uint32)
+    c = to_dev_ring(C0)
+    m.mosaic_sparse_gather_cols(p, to_dev_ring(D)[:, :r], M, c, subtract=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_u32(c), ring_sub(C0, ring_matmul(D[:, :r], P.T)))
 
 
 @pytest.mark.parametrize("params", [PARAMS_D2_SPARSE, PARAMS_D3_SPARSE_SMALL,
