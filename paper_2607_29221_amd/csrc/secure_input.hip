@@ -8,9 +8,12 @@
 //   4. write A' as digits, and s.
 // It performs exactly the arithmetic of mosaic_hadamard_rotate,
 // mosaic_quantize_rows and mosaic_mask in sequence (same butterfly order,
-// same fp32 scale and division, same noise element indices), so the digits
-// are bit-identical to that sequence, with 16 bytes of HBM traffic per
-// element instead of 28 for the three passes.
+// same fp32 scale, the same correctly rounded quotient before rounding to an
+// integer, same noise element indices), so the digits are bit-identical to
+// that sequence, with 16 bytes of HBM traffic per element instead of 28 for
+// the three passes. The pass is bound by vector-ALU issue, so the quotient
+// of each code is replaced by a product with the reciprocal of the scale
+// wherever that provably rounds to the same integer (quant_codes4).
 //
 // Rows that fit in registers with room to spare (n = 8192 with b = 8192,
 // 4096 or 1024, and 16384 with b = 16384) run in one launch
@@ -90,18 +93,20 @@ __global__ __launch_bounds__((FS<LOGB>::T), (FS<LOGB>::WAVES)) void rqm_mask_ker
   const float* xr = x + row * ldx;
   const float amax = scale[row];    // written by rqm_max_kernel
   const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
+  const float rs = 1.0f / s, thr = quant_threshold(s, qmax);
   for (int64_t blk = 0; blk < n / B; ++blk) {
     float v[E];
     fwht_load<LOGB, SG, true, fwht_tmax(LOGB)>(xr + blk * B, SG ? signs + blk * B : nullptr, v);
     const float sb = scale_b * fwht_transform<LOGB, fwht_tmax(LOGB)>(sm, v);   // the lane sign folded into the scale
+    const float kb = sb * rs;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       // columns 4 c .. 4 c + 3 of the row; lanes t .. t + 3 hold one 16-column group
       const int64_t c = blk * (B / 4) + t + T * k;
       const u32x4 uu = HU ? __builtin_nontemporal_load((const u32x4*)(u + row * ldu + 4 * c)) : u32x4{0, 0, 0, 0};
       uint32_t w[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)(int32_t)rintf((v[4 * k + q] * sb) / s) + uu[q];
+      quant_codes4(&v[4 * k], sb, kb, s, thr, w);
+      w[0] += uu[0]; w[1] += uu[1]; w[2] += uu[2]; w[3] += uu[3];
       if (HN) {
         uint32_t e[4];
         sample4_aligned(noise, (uint64_t)row * (uint64_t)n + (uint64_t)(4 * c), e);
@@ -155,6 +160,7 @@ __global__ __launch_bounds__((FS<LOGB>::T)) void rqm_row_kernel(
   const float amax = block_max<LOGB>(m, red);
   const float s = (amax > 0.0f) ? amax / (float)qmax : 1.0f;
   const float sb = scale_b * c;
+  const float kb = sb * (1.0f / s), thr = quant_threshold(s, qmax);
 #pragma unroll
   for (int k = 0; k < NB; ++k) {
 #pragma unroll
@@ -163,8 +169,8 @@ __global__ __launch_bounds__((FS<LOGB>::T)) void rqm_row_kernel(
       const int64_t cc = k * (B / 4) + t + T * kk;
       const u32x4 uu = __builtin_nontemporal_load((const u32x4*)(u + row * ldu + 4 * cc));
       uint32_t w[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)(int32_t)rintf((v[k][4 * kk + q] * sb) / s) + uu[q];
+      quant_codes4(&v[k][4 * kk], sb, kb, s, thr, w);
+      w[0] += uu[0]; w[1] += uu[1]; w[2] += uu[2]; w[3] += uu[3];
       if (HN) {
         uint32_t e[4];
         sample4_aligned(noise, (uint64_t)row * (uint64_t)n + (uint64_t)(4 * cc), e);

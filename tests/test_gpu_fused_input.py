@@ -32,7 +32,11 @@ def _separate(x, block, signs, qmax, u, noise):
 @pytest.mark.parametrize("rows,n,block,qmax", [(5, 8192, 8192, 1997), (3, 28672, 4096, 567), (4, 1024, 1024, 300),
                                                (2, 16384, 16384, 1000), (3, 3072, 1024, 127), (2, 32768, 4096, 511),
                                                (2, 36864, 4096, 400), (3, 6144, 2048, 255), (3, 8192, 4096, 777),
-                                               (3, 8192, 1024, 1997), (2, 16384, 8192, 1500)])
+                                               (3, 8192, 1024, 1997), (2, 16384, 8192, 1500),
+                                               # large code ranges: the product with 1 / s is within the
+                                               # rounding margin for some codes, none at qmax >= 2^20
+                                               (3, 8192, 1024, 700001), (3, 28672, 4096, 300001),
+                                               (2, 8192, 8192, 500001), (2, 28672, 4096, 3000000)])
 @pytest.mark.parametrize("with_u,with_noise", [(True, True), (False, False), (True, False)])
 def test_fused_matches_separate_passes(rows, n, block, qmax, with_u, with_noise):
     x = torch.from_numpy(outlier_activations(rows, n, rows + n)).cuda()
@@ -129,3 +133,51 @@ def test_fused_against_oracle(rows, n, block, qmax):
     keep = np.array([i for i in range(rows) if i != 3])
     amb = code_validity(codes[keep], s[keep], x[keep].astype(np.float64), signs_np, block, qmax)
     assert amb < 0.1
+
+
+def _tie_rows(rows, n, qmax, a_sum):
+    """Rows whose rotation (block 1024, signs +1) lands on or next to
+    half-integer multiples of the row scale: every block
+    holds x = (A + B) / 2 at its first entry and (A - B) / 2 at its second,
+    so the rotated block is (A + B) / 32 at even and (A - B) / 32 at odd
+    entries; A = a_sum sets max |y| = A / 32, and B = (k + 1/2) A / qmax for
+    k = 0, 1, 2, ... (sign alternating by block) puts y / s at k + 1/2."""
+    x = np.zeros((rows, n), dtype=np.float32)
+    for r in range(rows):
+        for blk in range(n // 1024):
+            k = (blk + 3 * r) % qmax
+            B = (k + 0.5) * a_sum / qmax * (-1.0 if (blk + r) % 2 else 1.0)
+            x[r, 1024 * blk] = np.float32((a_sum + B) / 2)
+            x[r, 1024 * blk + 1] = np.float32((a_sum - B) / 2)
+    return x
+
+
+@pytest.mark.parametrize("n", [8192, 28672], ids=["one-launch", "two-launch"])
+@pytest.mark.parametrize("qmax,a_sum", [(8, 4.0), (10, 4.0), (127, 3.0), (1000, 8.0)])
+def test_fused_rounding_ties(n, qmax, a_sum):
+    """Codes at and next to rounding ties: y / s exactly k + 1/2 where the
+    scale is a power of two (qmax 8, A 4: ties to even) and within a few
+    ulp of it otherwise, all taking the division branch of the code rounding.
+    The fused pass (no u, no noise: the digits hold the codes) against the
+    oracle's quantisation of the exact float32 rotation, and against the
+    separate passes."""
+    from oracle import hadamard as ohad
+    from oracle import quant as oquant
+    from oracle.ring import lift
+    rows = 4
+    x = _tie_rows(rows, n, qmax, a_sum)
+    # every rotated entry is (a +- b) / 32 with one rounding in float32: the
+    # butterflies add a and b once and zeros otherwise, and 1 / 32 is exact
+    y = ohad.rotate(x.astype(np.float64), np.ones(n), block=1024).astype(np.float32)
+    q_ref, s_ref = oquant.quantize_rows(y, qmax)
+    xd = torch.from_numpy(x).cuda()
+    d = Digits.empty(rows, n)
+    sc = torch.empty(rows, dtype=torch.float32, device="cuda")
+    m.mosaic_rotate_quantize_mask(xd, qmax, d, block=1024, scale=sc)
+    torch.cuda.synchronize()
+    assert np.array_equal(sc.cpu().numpy(), s_ref)
+    assert np.array_equal(lift(unpack_digits(d)), q_ref.astype(np.int64))
+    if qmax == 8:
+        assert np.any(q_ref % 2 == 0) and np.all(np.abs(q_ref) <= qmax)
+    d_sep, s_sep = _separate(xd, 1024, None, qmax, None, None)
+    assert np.array_equal(digits_np(d), digits_np(d_sep))
