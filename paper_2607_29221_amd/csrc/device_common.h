@@ -203,41 +203,39 @@ __device__ __forceinline__ void quad_digit_planes(const uint32_t v[4], int q, ui
 // entry and a row scale s with |y| <= qmax s up to the rounding of s, so
 // |y / s| < L = qmax + 1. With r = fl(1 / s) and k = fl(c r), t = fl(v k)
 // equals y / s up to four roundings of relative size u = 2^-24 (r, k, t and
-// y), and fl(y / s) equals it up to one more: |t - fl(y / s)| <= 5 u L (to
-// first order) < 2^-21 L. rint of t and of fl(y / s) can therefore differ
-// only where a half-integer lies within 2^-21 L of t, i.e. where
-// |t - rint(t)| > 1/2 - 2^-21 L; those entries (about one in 2^20 / L) are
-// computed by the division itself, and so are non-finite t.
+// y): |t - y / s| <= (4 u + 8 u^2) |y / s|; fl(y / s) is within u |y / s|
+// of it, so |t - fl(y / s)| < 6 u L. rint of t and of fl(y / s) can
+// therefore differ only where a half-integer lies within 6 u L of t, i.e.
+// where |t - rint(t)| > 1/2 - 6 u L; those entries (a fraction 12 u L of
+// them) are computed by the division itself, and so are non-finite t.
 // quant_threshold gives that bound, or -1 (every entry divides) where the
 // argument needs more care: qmax >= 2^20, or s outside [2^-100, 2^100], which
 // keeps r and k normal and the rounding of subnormal y far below the margin.
 __device__ __forceinline__ float quant_threshold(float s, int32_t qmax) {
   const bool ok = s >= 0x1p-100f && s <= 0x1p100f && qmax < (1 << 20);
-  return ok ? 0.5f - (float)(qmax + 1) * 0x1p-21f : -1.0f;
+  return ok ? 0.5f - (float)(qmax + 1) * 0x1.8p-22f : -1.0f;   // 6 u L, exact in fp32
 }
 
 // Codes of four entries v[0..3] with a common factor c: k = fl(c fl(1 / s)),
 // thr = quant_threshold(s, qmax). The codes equal rint(fl(fl(v c) / s)).
+// One branch per entry: a wave runs a division only for an entry that one
+// of its lanes needs. (One branch for all four entries, with a margin of
+// 8 u L, sent 13-39% of the wave-groups of four entries through four
+// divisions at qmax = 567-1997; the fused input pass was 1-10% slower.)
 __device__ __forceinline__ void quant_codes4(const float v[4], float c, float k, float s, float thr,
                                              uint32_t q[4]) {
-  float f[4];
-  bool slow = false;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const float t = __fmul_rn(v[i], k);
-    f[i] = rintf(t);
-    slow |= !(fabsf(t - f[i]) <= thr);
+    float f = rintf(t);
+    if (!(fabsf(t - f) <= thr)) {
+      // the divisor passes through an empty volatile statement, so that the
+      // division stays inside this rarely taken branch
+      float sd = s;
+      asm volatile("" : "+v"(sd));
+      f = rintf((v[i] * c) / sd);
+    }
+    q[i] = (uint32_t)(int32_t)f;
   }
-  if (slow) {
-    // the divisor passes through an empty volatile statement, so that the
-    // divisions stay inside this rarely taken branch
-    float sd = s;
-    asm volatile("" : "+v"(sd));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) f[i] = rintf((v[i] * c) / sd);
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) q[i] = (uint32_t)(int32_t)f[i];
 }
-
 }  // namespace mosaic
