@@ -991,7 +991,9 @@ def _compact(ex):
                                                       "hbm_frac": round(si["fused_gbs"] / HBM_PEAK_GBS, 3)}
     out["passes"] = p
     if "decode" in ex:
-        out["decode"] = [{"K": d["K"], "N": d["N"], "M": d["M"], "server_hbm_frac": d["server_hbm_frac"],
+        # device time of the server loop replayed as a graph (clear and
+        # product; the eager loop's figure also holds the host's launch gaps)
+        out["decode"] = [{"K": d["K"], "N": d["N"], "M": d["M"], "server_hbm_frac_graph": d["server_hbm_frac_graph"],
                           "call_us_graph": d["call_us_auto_lpn_graph"]} for d in ex["decode"]]
     if "lpn_client_cost" in ex:
         out["lpn_client_cost"] = ex["lpn_client_cost"]["summary"]
