@@ -801,6 +801,32 @@ def _shape(name):
     return decoder_linear_shape(name)
 
 
+def _mfma_probe_tops(mode):
+    """int8 TOP/s of the register-only MFMA probe (mosaic_probe_mfma_i8;
+    mode 0 zero, 1 constant, 2 uniformly random operands): 0.5 s of the same
+    load, then about 0.3 s timed."""
+    import torch
+
+    from paper_2607_29221_amd import mosaic as m
+
+    out = torch.zeros(1, dtype=torch.int32, device=torch.device("cuda", 0))
+    iters = 8192
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 0.5:
+        m.mosaic_probe_mfma_i8(mode, iters, out)
+        torch.cuda.synchronize()
+    e0, e1 = _events(2)
+    e0.record()
+    ops, n = 0, 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 0.3 or n < 3:
+        ops += m.mosaic_probe_mfma_i8(mode, iters, out)
+        n += 1
+    e1.record()
+    torch.cuda.synchronize()
+    return round(ops / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+
+
 def run_mfma_ceiling():
     """The ceiling the server product runs under: the register-only MFMA
     probe (v_mfma_i32_32x32x32_i8, operands in registers, no memory traffic)
@@ -814,24 +840,9 @@ def run_mfma_ceiling():
     from paper_2607_29221_amd.mosaic import Digits
 
     dev = torch.device("cuda", 0)
-    out = torch.zeros(1, dtype=torch.int32, device=dev)
     res = {}
-    iters = 8192
     for mode, name in ((0, "zero"), (1, "constant"), (2, "random")):
-        t0 = time.perf_counter()
-        while time.perf_counter() - t0 < 0.5:
-            m.mosaic_probe_mfma_i8(mode, iters, out)
-            torch.cuda.synchronize()
-        e0, e1 = _events(2)
-        e0.record()
-        ops, n = 0, 0
-        t0 = time.perf_counter()
-        while time.perf_counter() - t0 < 0.3 or n < 3:
-            ops += m.mosaic_probe_mfma_i8(mode, iters, out)
-            n += 1
-        e1.record()
-        torch.cuda.synchronize()
-        res[f"register_{name}_tops"] = round(ops / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+        res[f"register_{name}_tops"] = _mfma_probe_tops(mode)
     M, K, Np = 2048, 8192, 30208
     A, B = Digits.empty(M, K, dev), Digits.empty(Np, K, dev)
     C = torch.empty((M, Np), dtype=torch.int32, device=dev)
@@ -1085,6 +1096,12 @@ def main():
         "per_shape": gpu["per_shape"],
     }
     if "extras" in gpu:
+        # the matrix cores' own limit on operands like the masked ones
+        # (uniformly random, changing every instruction): the roofline's
+        # kernel against it, next to its fraction of the datasheet peak
+        ceil = _mfma_probe_tops(2)
+        line["mfma_random_operand_ceiling"] = {"tops": ceil, "unit": "TOP/s",
+                                               "kernel_frac_of_it": round(gpu["roofline"]["achieved"] / ceil, 3)}
         line.update(_compact(gpu["extras"]))
         if args.extras_file:
             path = os.path.abspath(args.extras_file)
