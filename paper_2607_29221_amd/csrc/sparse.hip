@@ -18,18 +18,123 @@ namespace {
 
 // Entries of row ``row`` of a WEIGHT stream matrix, computed by one wave
 // (the calling workgroup's first 64 threads; every thread of the workgroup
-// must call it, the others only wait). perm: LDS scratch of ``cols``
-// uint16, u: LDS scratch of t words; pos / val (LDS, t entries) receive the
-// chosen column and the value of each step. The permutation is stored as
-// perm[k] ^ k so that zero-filled memory is the identity. Ends with a
-// workgroup barrier, after which pos and val are visible to all threads.
-__device__ void weighted_row(const RngArgs& r, int64_t row, int cols, uint16_t* perm, uint32_t* u, int32_t* pos,
-                             uint32_t* val) {
+// must call it, the others only wait). scratch: weighted_scratch_bytes(cols,
+// t) of LDS; pos / val (LDS, t entries) receive the chosen column and the
+// value of each step. Ends with a workgroup barrier, after which pos and val
+// are visible to all threads.
+//
+// Step j of the partial shuffle draws k_j = j + floor(u_j (cols - j) / 2^32)
+// and swaps entries j and k_j of a running permutation (the identity at
+// first); its column is the entry that lands at j, i.e. entry k_j just
+// before the step. Up to WEIGHT_PAR_T steps that entry is found without
+// running the swaps one after the other: position p >= j has been touched
+// before step j only by the steps i < j with k_i = p (the steps' own
+// positions i are all below j), and the latest of them left there the entry
+// that position i held just before step i. Position i in turn held i unless
+// an earlier step i' < i had k_{i'} = i, in which case it held what position
+// i' held before step i', and so on. So the column of step j is k_j if no
+// earlier step chose k_j, else E(i) for the latest such i, with E(i) = i if
+// no step before i chose position i and E(i) = E(i') for the latest such i'.
+// A table over the positions counts each position's choosers (and keeps
+// the first one): a step whose position has one chooser takes it; the few
+// steps on positions chosen more than once (a handful per row at t = 80 of
+// r = 1024) go to a short list, which answers "latest earlier chooser" for
+// them and, with the table, the chains of E. Longer rows take the steps one
+// by one on a permutation kept in LDS as perm[k] ^ k, so that zero-filled
+// memory is the identity.
+constexpr int WEIGHT_PAR_T = 256;
+
+inline size_t weighted_scratch_bytes(int64_t cols, int64_t t) {
+  return t <= WEIGHT_PAR_T ? (size_t)(4 * cols + 8 * t + 16) : (size_t)(2 * cols + 4 * t + 16);
+}
+
+__device__ void weighted_row(const RngArgs& r, int64_t row, int cols, void* scratch, int32_t* pos, uint32_t* val) {
   const int t = r.row_weight;
   const int tid = threadIdx.x;
+  const uint64_t w0 = 2 * (uint64_t)t * (uint64_t)row;   // even: each (u, value) pair is one half block
+  if (t <= WEIGHT_PAR_T) {
+    uint32_t* tab = (uint32_t*)scratch;        // per position: (choosers << 16) | first chooser
+    uint32_t* kk = tab + cols;                 // per step: its position
+    int32_t* shared_steps = (int32_t*)(kk + t); // steps on positions with several choosers
+    int* nshared = (int*)(shared_steps + t);
+    const int lane = tid;
+    uint32_t k[4];
+    if (tid < 64) {
+      for (int p = lane; p < cols; p += 64) tab[p] = 0;
+      if (lane == 0) *nshared = 0;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int j = lane + 64 * s;
+        k[s] = 0;
+        if (j < t) {
+          const uint64_t w = w0 + 2 * (uint64_t)j;
+          const uint4 blk = philox_block(r, w >> 2);
+          const bool hi = ((w >> 1) & 1) != 0;
+          const uint32_t uj = hi ? blk.z : blk.x;
+          val[j] = hi ? blk.w : blk.y;
+          k[s] = (uint32_t)j + (uint32_t)(((uint64_t)uj * (uint64_t)(uint32_t)(cols - j)) >> 32);
+          kk[j] = k[s];
+        }
+      }
+    }
+    __syncthreads();
+    if (tid < 64) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int j = lane + 64 * s;
+        if (j < t) {
+          // the first chooser's step number goes to the low half; the others
+          // only add to the count, so the two updates commute
+          const uint32_t old = atomicAdd(&tab[k[s]], 0x10000u);
+          if ((old >> 16) == 0) atomicOr(&tab[k[s]], (uint32_t)j);
+        }
+      }
+    }
+    __syncthreads();
+    if (tid < 64) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int j = lane + 64 * s;
+        if (j < t && (tab[k[s]] >> 16) >= 2) shared_steps[atomicAdd(nshared, 1)] = j;
+      }
+    }
+    __syncthreads();
+    if (tid < 64) {
+      const int n = *nshared;
+      // latest step before `before` whose position is p, or -1
+      auto latest = [&](uint32_t p, int before) -> int {
+        const uint32_t e = tab[p];
+        const uint32_t choosers = e >> 16;
+        if (choosers == 0) return -1;
+        if (choosers == 1) return ((int)(e & 0xFFFFu) < before) ? (int)(e & 0xFFFFu) : -1;
+        int best = -1;
+        for (int q = 0; q < n; ++q) {
+          const int i = shared_steps[q];
+          if (i < before && i > best && kk[i] == p) best = i;
+        }
+        return best;
+      };
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int j = lane + 64 * s;
+        if (j < t) {
+          int x = latest(k[s], j);
+          uint32_t col = k[s];
+          if (x >= 0) {
+            for (int y = latest((uint32_t)x, x); y >= 0; y = latest((uint32_t)x, x)) x = y;
+            col = (uint32_t)x;
+          }
+          pos[j] = (int32_t)col;
+        }
+      }
+    }
+    __syncthreads();
+    return;
+  }
+  uint16_t* perm = (uint16_t*)scratch;
+  uint32_t* u = (uint32_t*)scratch + ((cols + 1) >> 1);
   if (tid < 64) {
     for (int k = tid; k < cols; k += 64) perm[k] = 0;
-    const uint64_t w0 = 2 * (uint64_t)t * (uint64_t)row;   // even: each (u, value) pair is one half block
     for (int j = tid; j < t; j += 64) {
       const uint64_t w = w0 + 2 * (uint64_t)j;
       const uint4 blk = philox_block(r, w >> 2);
@@ -52,9 +157,9 @@ __device__ void weighted_row(const RngArgs& r, int64_t row, int cols, uint16_t* 
   __syncthreads();
 }
 
-// Dynamic LDS of the WEIGHT kernels: u (t words), pos (t), val (t), then
-// perm (cols uint16).
-inline size_t weighted_lds_bytes(int64_t cols, int64_t t) { return (size_t)(12 * t + 2 * cols + 16); }
+// Dynamic LDS of the WEIGHT kernels: pos (t), val (t), then the row's
+// scratch.
+inline size_t weighted_lds_bytes(int64_t cols, int64_t t) { return (size_t)(8 * t) + weighted_scratch_bytes(cols, t); }
 
 // One 64-thread workgroup per row: the row of a WEIGHT matrix as ring words
 // and/or digits (zeros, then the t entries).
@@ -62,10 +167,8 @@ __global__ __launch_bounds__(64) void weighted_sample_kernel(RngArgs r, int64_t 
                                                              int8_t* dig, int64_t pitch) {
   extern __shared__ uint32_t wlds[];
   const int t = r.row_weight;
-  uint32_t* u = wlds;
-  int32_t* pos = (int32_t*)(wlds + t);
-  uint32_t* val = wlds + 2 * t;
-  uint16_t* perm = (uint16_t*)(wlds + 3 * t);
+  int32_t* pos = (int32_t*)wlds;
+  uint32_t* val = wlds + t;
   const int64_t row = blockIdx.x;
   const int tid = threadIdx.x;
   if (out != nullptr)
@@ -74,7 +177,7 @@ __global__ __launch_bounds__(64) void weighted_sample_kernel(RngArgs r, int64_t 
     const int64_t bytes = 4 * (64 * ((cols + 63) / 64));   // the padded row, zero digits
     for (int64_t k = 16 * tid; k < bytes; k += 16 * 64) *(uint4*)(dig + row * pitch + k) = make_uint4(0, 0, 0, 0);
   }
-  weighted_row(r, row, (int)cols, perm, u, pos, val);   // its barriers also order the zero stores first
+  weighted_row(r, row, (int)cols, wlds + 2 * t, pos, val);   // its barriers also order the zero stores first
   for (int j = tid; j < t; j += 64) {
     const int64_t c = pos[j];
     const uint32_t v = val[j];
@@ -101,11 +204,11 @@ __global__ __launch_bounds__(64) void weighted_fill_kernel(RngArgs r, int64_t co
   extern __shared__ uint32_t wlds[];
   const int t = r.row_weight;
   const int64_t row = blockIdx.x;
-  weighted_row(r, row, (int)cols, (uint16_t*)(wlds + 3 * t), wlds, (int32_t*)(wlds + t), wlds + 2 * t);
+  weighted_row(r, row, (int)cols, wlds + 2 * t, (int32_t*)wlds, wlds + t);
   const int64_t base = row_ptr[row];
   for (int j = threadIdx.x; j < t; j += 64) {
-    col_idx[base + j] = (int32_t)wlds[t + j];
-    values[base + j] = wlds[2 * t + j];
+    col_idx[base + j] = (int32_t)wlds[j];
+    values[base + j] = wlds[t + j];
   }
 }
 
@@ -219,7 +322,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RngArgs r, int64_t rco
     int n;
     if (STREAM == 2) {
       extern __shared__ uint32_t wlds[];
-      weighted_row(r, i, (int)rcols, (uint16_t*)wlds + 0, wlds + ((rcols + 1) >> 1), scol, sval);
+      weighted_row(r, i, (int)rcols, wlds, scol, sval);
       n = r.row_weight;
     } else if (STREAM == 1) {
       if (tid == 0) scount = 0;
@@ -371,8 +474,8 @@ hipError_t launch_sparse_stream_gather_rows(const RngArgs& r, int64_t rows, int6
   const uint32_t* nv = nullptr;
   if (r.dist == 4) {
     if (r.row_weight == 0) return hipSuccess;
-    // perm (rcols uint16, rounded up to words), then u (t words)
-    const size_t lds = (size_t)(4 * ((rcols + 1) / 2) + 4 * r.row_weight);
+    // the drawn row's scratch; its entries go to the static staging arrays
+    const size_t lds = weighted_scratch_bytes(rcols, r.row_weight);
     if (split)
       hipLaunchKernelGGL((gather_rows_kernel<2, 4>), grid, dim3(256), lds, s, r, rcols, np, ni, nv, d, ldd, ncols, c,
                          ldc, subtract);

@@ -222,7 +222,11 @@ def test_sparse_mode_dequantised_output():
 # --- fixed row weight (Example 4.1: t nonzeros per row) ---
 
 @pytest.mark.parametrize("rows,cols,t", [(5, 1536, 80), (64, 1024, 80), (33, 70, 70), (4, 8192, 2048),
-                                         (3, 5, 0), (1, 1, 1), (130, 652, 80)])
+                                         (3, 5, 0), (1, 1, 1), (130, 652, 80),
+                                         # rows of up to 256 entries are resolved in parallel: full
+                                         # permutations and dense rows (many repeated positions)
+                                         (5, 256, 256), (4, 300, 256), (6, 64, 64), (6, 65, 65),
+                                         (3, 300, 257)])
 def test_weighted_sample_matches_oracle(rows, cols, t):
     """mosaic_sample with a WEIGHT stream: ring words and digits equal the
     oracle's partial-shuffle matrix (zeros elsewhere, padding digits zero)."""
@@ -241,7 +245,8 @@ def test_weighted_sample_matches_oracle(rows, cols, t):
     assert pad_is_zero(dig)
 
 
-@pytest.mark.parametrize("rows,cols,t", [(300, 1536, 80), (17, 1024, 80), (9, 40, 40), (2, 8192, 2048)])
+@pytest.mark.parametrize("rows,cols,t", [(300, 1536, 80), (17, 1024, 80), (9, 40, 40), (2, 8192, 2048),
+                                         (7, 256, 256), (5, 8192, 256)])
 def test_weighted_csr_matches_oracle(rows, cols, t):
     """Compressed rows of a WEIGHT stream: row_ptr = i t, and each row lists
     the oracle's columns and values in the order of the shuffle's steps."""
@@ -255,7 +260,8 @@ def test_weighted_csr_matches_oracle(rows, cols, t):
 
 
 @pytest.mark.parametrize("rows,r,ncols,t", [(9, 1536, 517, 80), (64, 1024, 8192, 80), (3, 300, 70, 300),
-                                            (1, 1, 1, 1), (5, 2048, 300, 2048)])
+                                            (1, 1, 1, 1), (5, 2048, 300, 2048), (4, 256, 300, 256),
+                                            (1, 652, 18432, 80)])
 @pytest.mark.parametrize("subtract", [False, True])
 def test_weighted_stream_gather(rows, r, ncols, t, subtract):
     """T_{i+1} terms with WEIGHT rows drawn inside the gather, and the same
