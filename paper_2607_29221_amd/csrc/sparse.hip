@@ -403,7 +403,26 @@ __global__ __launch_bounds__(256) void gather_cols_kernel(int64_t M, int64_t N, 
   for (int mm = 0; mm < MB; ++mm) acc[mm] = 0;
   if (n < N) {
     const int64_t p0 = row_ptr[n], p1 = row_ptr[n + 1];
-    for (int64_t p = p0 + sub; p < p1; p += 8) {
+    int64_t p = p0 + sub;
+    // four of the lane's entries in flight at once (one at a time, each
+    // entry's loads and then its gather from d waited in turn: one-token
+    // calls over 14336 rows of 80 entries took 6.9 instead of 4.8 us)
+    for (; p + 24 < p1; p += 32) {
+      uint32_t v[4];
+      int64_t col[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[q] = values[p + 8 * q];
+        col[q] = col_idx[p + 8 * q];
+      }
+#pragma unroll
+      for (int mm = 0; mm < MB; ++mm)
+        if (m0 + mm < M) {
+          const uint32_t* dr = d + (m0 + mm) * ldd;
+          acc[mm] += v[0] * dr[col[0]] + v[1] * dr[col[1]] + v[2] * dr[col[2]] + v[3] * dr[col[3]];
+        }
+    }
+    for (; p < p1; p += 8) {
       const uint32_t v = values[p];
       const int64_t col = col_idx[p];
 #pragma unroll
