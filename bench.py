@@ -689,8 +689,9 @@ def run_lpn_client_cost(dev):
     """The client's share of a decode call for the three mask depths of
     Example 4.1 -- LWE only (r = 1536), + LPN-1 (r_2 = 1024, t_2 = 80),
     + LPN-2 (r_3 = 652, t_3 = 80), all with sigma = 0.5 -- at (K, N) = (4096,
-    14336): Init X, mask and unmask (no server product), sparse LPN form,
-    device time of 20 calls replayed as a HIP graph, calls cycling through
+    14336) for 1, 8 and 64 tokens: Init X, mask and unmask (no server
+    product), sparse LPN form, device time of 20 calls replayed as a HIP
+    graph, calls cycling through
     distinct masked weights. Table "lpn-tradeoff" puts the client's
     multiplications per (m + n) l at r_1 = 1536, r_2 + t_2 = 1104 and
     r_3 + t_2 + t_3 = 812 (ratios 1, 0.719, 0.529)."""
@@ -706,7 +707,7 @@ def run_lpn_client_cost(dev):
     cfgs = (("lwe_only", PARAMS_PAPER_D1), ("lpn1_t80", PARAMS_PAPER_D2_T80), ("lpn2_t80", PARAMS_PAPER_D3_T80))
     table = {"lwe_only": 1536, "lpn1_t80": 1104, "lpn2_t80": 812}
     rows = []
-    for M in (8, 64):
+    for M in (1, 8, 64):
         Ad = torch.from_numpy(A[:M].copy()).to(dev)
         entry = {"M": M}
         for name, params in cfgs:
