@@ -36,7 +36,8 @@ def _separate(x, block, signs, qmax, u, noise):
                                                # large code ranges: the product with 1 / s is within the
                                                # rounding margin for some codes, none at qmax >= 2^20
                                                (3, 8192, 1024, 700001), (3, 28672, 4096, 300001),
-                                               (2, 8192, 8192, 500001), (2, 28672, 4096, 3000000)])
+                                               (2, 8192, 8192, 500001), (2, 28672, 4096, 3000000),
+                                               (3, 8192, 4096, 900001), (2, 16384, 16384, 2000000)])
 @pytest.mark.parametrize("with_u,with_noise", [(True, True), (False, False), (True, False)])
 def test_fused_matches_separate_passes(rows, n, block, qmax, with_u, with_noise):
     x = torch.from_numpy(outlier_activations(rows, n, rows + n)).cuda()
