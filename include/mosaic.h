@@ -78,7 +78,7 @@
 extern "C" {
 #endif
 
-#define MOSAIC_ABI_VERSION 2
+#define MOSAIC_ABI_VERSION 3
 
 typedef enum mosaic_status {
   MOSAIC_OK = 0,
@@ -211,6 +211,25 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy,
                             int32_t* y, int64_t ldo,
                             const float* s_rows, const float* s_cols, const float* bias,
                             float* y_f32, int64_t ldf, void* stream);
+
+/* mosaic_unmask with Q given as ring words, as the server returns it (the Q
+ * columns of [Y' | Q]): q is M x R uint32 with leading dimension ldq >= R,
+ * every other argument as in mosaic_unmask. Q's digit planes are formed as
+ * the product reads it, so the client's pass that converts Q to digits is
+ * not needed (one launch fewer per decode call). Requirements: M <= 16, q
+ * 16-byte aligned and ldq a multiple of 4 (else MOSAIC_ERR_UNSUPPORTED);
+ * l's digits past column R must be zero (the digit layout's padding),
+ * because the words read past column R of a row of q are whatever follows
+ * in memory. Results are bit-identical to mosaic_unmask with the digits of
+ * the same Q. */
+mosaic_status mosaic_unmask_words(const uint32_t* ym, int64_t ldy,
+                                  const uint32_t* kc, int64_t ldk,
+                                  const uint32_t* q, int64_t ldq,
+                                  const int8_t* l_dig, int64_t l_pitch,
+                                  int64_t M, int64_t N, int64_t R,
+                                  int32_t* y, int64_t ldo,
+                                  const float* s_rows, const float* s_cols, const float* bias,
+                                  float* y_f32, int64_t ldf, void* stream);
 
 /* Fused client input pass of Pi_Sec-Linear (Section 5 protocol box, online
  * step 1, then the mask of the Section 4.2 box, online step 2): for every row

@@ -51,6 +51,8 @@ _SIGNATURES = {
                                 c_i64, c_ptr, c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_unmask": ([c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64,
                        c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
+    "mosaic_unmask_words": ([c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_ptr, c_i64, c_i64, c_i64, c_i64,
+                             c_ptr, c_i64, c_ptr, c_ptr, c_ptr, c_ptr, c_i64, c_ptr], c_i32),
     "mosaic_sample_signs": ([ctypes.POINTER(MosaicRng), c_i64, c_ptr, c_ptr], c_i32),
     "mosaic_rotate_quantize_mask": ([c_ptr, c_i64, c_i64, c_i64, c_i64, c_ptr, c_i32, c_ptr, c_i64,
                                      ctypes.POINTER(MosaicRng), c_ptr, c_i64, c_ptr, c_ptr], c_i32),

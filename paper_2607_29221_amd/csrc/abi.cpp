@@ -552,6 +552,56 @@ mosaic_status mosaic_unmask(const uint32_t* ym, int64_t ldy, const uint32_t* kc,
   return hip_status(launch_ring_gemm(g, EPI_UNMASK, (hipStream_t)stream), "unmask launch");
 }
 
+mosaic_status mosaic_unmask_words(const uint32_t* ym, int64_t ldy, const uint32_t* kc, int64_t ldk, const uint32_t* q,
+                                  int64_t ldq, const int8_t* l_dig, int64_t l_pitch, int64_t M, int64_t N, int64_t R,
+                                  int32_t* y, int64_t ldo, const float* s_rows, const float* s_cols,
+                                  const float* bias, float* y_f32, int64_t ldf, void* stream) {
+  if (M < 0 || N < 0 || R < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");
+  if (M > 16) return fail(MOSAIC_ERR_UNSUPPORTED, "q as ring words needs M <= 16");
+  if (R >= 32768) return fail(MOSAIC_ERR_UNSUPPORTED, "R must be < 32768");
+  if (M == 0 || N == 0) return MOSAIC_OK;
+  if (ym == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "ym is NULL");
+  if (ldy < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldy < N");
+  if (kc != nullptr && ldk < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldk < N");
+  if (y == nullptr && y_f32 == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "no output given");
+  if (y != nullptr && ldo < N) return fail(MOSAIC_ERR_INVALID_ARG, "ldo < N");
+  if (y_f32 != nullptr && (ldf < N || s_rows == nullptr || s_cols == nullptr))
+    return fail(MOSAIC_ERR_INVALID_ARG, "y_f32 needs ldf >= N and both scale vectors");
+  if (bias != nullptr && y_f32 == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "bias needs y_f32");
+  GemmLaunch g{};
+  g.M = M;
+  g.N = N;
+  g.ym = ym;
+  g.ldy = ldy;
+  g.kc = kc;
+  g.ldk = ldk;
+  g.y = y;
+  g.ldo = ldo;
+  g.s_rows = s_rows;
+  g.s_cols = s_cols;
+  g.bias = bias;
+  g.y_f32 = y_f32;
+  g.ldf = ldf;
+  if (R > 0) {
+    if (q == nullptr) return fail(MOSAIC_ERR_INVALID_ARG, "q is NULL");
+    if (ldq < R) return fail(MOSAIC_ERR_INVALID_ARG, "ldq < R");
+    if (!aligned16(q) || ldq % 4 != 0) return fail(MOSAIC_ERR_UNSUPPORTED, "q must be 16-byte aligned, ldq a multiple of 4");
+    if (ldq > (int64_t(1) << 21)) return fail(MOSAIC_ERR_UNSUPPORTED, "q pitch above 8 MiB");
+    const mosaic_status st = check_digits(l_dig, l_pitch, N, R, "l_dig");
+    if (st != MOSAIC_OK) return st;
+    if (l_pitch > (int64_t(1) << 23)) return fail(MOSAIC_ERR_UNSUPPORTED, "digit pitch above 8 MiB");
+    g.a = (const int8_t*)q;
+    g.a_pitch = 4 * ldq;
+    g.a_last = 16 * ((R + 3) / 4);   // q's last row up to its 16-byte chunk
+    g.b = l_dig;
+    g.b_pitch = l_pitch;
+    g.Kp = padded_k(R);
+  } else if (M > 0 && N > kMaxGridThreads / M) {
+    return fail(MOSAIC_ERR_UNSUPPORTED, "matrix too large for one launch");
+  }
+  return hip_status(launch_unmask_words_a(g, (hipStream_t)stream), "unmask launch");
+}
+
 mosaic_status mosaic_hadamard_rotate(const float* x, int64_t ldx, float* y, int64_t ldy, int64_t rows, int64_t n,
                                      int64_t block, const int8_t* signs, int32_t inverse, void* stream) {
   if (rows < 0 || n < 0) return fail(MOSAIC_ERR_INVALID_ARG, "negative size");

@@ -86,6 +86,9 @@ struct GemmLaunch {
   // B given as ring words: bytes of B's last row that may be read from
   // b (its valid words from b on, rounded up to 16 bytes)
   int64_t b_last;
+  // A given as ring words (unmask of at most 16 rows): bytes of A's last
+  // row that may be read (its K valid words)
+  int64_t a_last;
   // decode kernel, EPI_ACCUM: subtract the product from c instead of adding
   bool negate;
   // tiled kernel (set by its launcher): the last split_tiles tiles run as
@@ -135,6 +138,10 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
 // words (b = first word, b_pitch = row pitch in bytes, a multiple of 16);
 // EPI_STORE or EPI_ACCUM.
 hipError_t launch_ring_gemm_words_b(const GemmLaunch& g, EpilogueKind epi, hipStream_t s);
+// Unmask (EPI_UNMASK) of at most 16 rows with A given as ring words (a,
+// a_pitch bytes per row, a_last as above): the rows' digit planes are formed
+// in registers as A is loaded.
+hipError_t launch_unmask_words_a(const GemmLaunch& g, hipStream_t s);
 // d = 0 (rows x cols, leading dimension ldd) and *count = 0 in one launch.
 hipError_t launch_clear_check(uint32_t* d, int64_t ldd, int64_t rows, int64_t cols, int64_t* count, hipStream_t s);
 

@@ -317,6 +317,22 @@ __device__ __forceinline__ void transpose4(v4i (&q)[4]) {
   swap16(q[2], q[3]);
 }
 
+// q[c] holds words 4 c .. 4 c + 3 of a 16-column group  ->  q[t] holds the
+// group's digit plane t (byte 4 c + b = digit t of word 4 c + b).
+__device__ __forceinline__ void words_to_planes(v4i (&q)[4]) {
+  uint32_t pl[4][4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const uint32_t v4[4] = {(uint32_t)q[c][0], (uint32_t)q[c][1], (uint32_t)q[c][2], (uint32_t)q[c][3]};
+    uint32_t p4[4];
+    digit_planes4(v4, p4);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) pl[t][c] = p4[t];
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t) q[t] = v4i{(int)pl[t][0], (int)pl[t][1], (int)pl[t][2], (int)pl[t][3]};
+}
+
 // Workgroup b: column tile b (16 NT rows of B), all stages, split into W
 // contiguous parts, one per wave. Load t of a wave reads bytes 64 t .. +64
 // of the stage in all 16 rows of a tile (lane (h, r) the 16 bytes at
@@ -329,7 +345,13 @@ __device__ __forceinline__ void transpose4(v4i (&q)[4]) {
 // one set only. Prefetches past the wave's last stage are clamped to that
 // stage: the duplicate request hits in cache and the loop needs no branches
 // around loads. K must be non-zero.
-template <int EPI, int MT, int NT, int S, int W>
+// AW: A arrives as ring words (a_pitch bytes per row, a_last valid bytes in
+// its last row). A stage's 64 words of a row fill the 256 bytes its digits
+// would, so lane (h, r) loads the 16 words of column group h (four 16-byte
+// loads) and turns them into that group's four digit planes in registers,
+// which is the fragment the transpose gives for digits. Words past K within
+// a row are whatever follows in memory; B's zero digits there cancel them.
+template <int EPI, int MT, int NT, int S, int W, bool AW = false>
 __global__ __launch_bounds__(64 * W) void ring_gemm_skinny_ksplit_kernel(GemmLaunch g) {
   constexpr int NOUT = MT * NT * 4;   // output registers per lane
   __shared__ uint32_t red[W][NOUT][64];
@@ -339,7 +361,7 @@ __global__ __launch_bounds__(64 * W) void ring_gemm_skinny_ksplit_kernel(GemmLau
   const int64_t n0 = (int64_t)blockIdx.x * (16 * NT);
   const int64_t rows_b = (g.N - n0) < 16 * NT ? (g.N - n0) : 16 * NT;
   const __amdgpu_buffer_rsrc_t rb = rsrc(g.b + n0 * g.b_pitch, rows_b * g.b_pitch);
-  const __amdgpu_buffer_rsrc_t ra = rsrc(g.a, g.M * g.a_pitch);
+  const __amdgpu_buffer_rsrc_t ra = rsrc(g.a, AW ? (g.M - 1) * g.a_pitch + g.a_last : g.M * g.a_pitch);
 
   const int r = lane & 15;
   const int h = lane >> 4;
@@ -347,7 +369,7 @@ __global__ __launch_bounds__(64 * W) void ring_gemm_skinny_ksplit_kernel(GemmLau
 #pragma unroll
   for (int j = 0; j < NT; ++j) ob[j] = (j * 16 + r) * (int)g.b_pitch + h * 16;
 #pragma unroll
-  for (int i = 0; i < MT; ++i) oa[i] = (i * 16 + r) * (int)g.a_pitch + h * 16;
+  for (int i = 0; i < MT; ++i) oa[i] = (i * 16 + r) * (int)g.a_pitch + (AW ? h * 64 : h * 16);
 
   // this wave's share [s0, s1) of the stages
   const int per = (stages + W - 1) / W;
@@ -371,13 +393,16 @@ __global__ __launch_bounds__(64 * W) void ring_gemm_skinny_ksplit_kernel(GemmLau
     _Pragma("unroll") for (int j = 0; j < NT; ++j)                                         \
     _Pragma("unroll") for (int t = 0; t < 4; ++t) fb[SET][j][t] = load16(rb, ob[j] + so_ + 64 * t); \
     _Pragma("unroll") for (int i = 0; i < MT; ++i)                                         \
-    _Pragma("unroll") for (int t = 0; t < 4; ++t) fa[SET][i][t] = load16(ra, oa[i] + so_ + 64 * t); \
+    _Pragma("unroll") for (int t = 0; t < 4; ++t) fa[SET][i][t] = load16(ra, oa[i] + so_ + (AW ? 16 : 64) * t); \
   } while (0)
 
 #define KS_MFMA(SET)                                                                       \
   do {                                                                                     \
     _Pragma("unroll") for (int j = 0; j < NT; ++j) transpose4(fb[SET][j]);                 \
-    _Pragma("unroll") for (int i = 0; i < MT; ++i) transpose4(fa[SET][i]);                 \
+    _Pragma("unroll") for (int i = 0; i < MT; ++i) {                                       \
+      if (AW) words_to_planes(fa[SET][i]);                                                 \
+      else transpose4(fa[SET][i]);                                                         \
+    }                                                                                      \
     _Pragma("unroll") for (int p = 0; p < 10; ++p)                                         \
     _Pragma("unroll") for (int i = 0; i < MT; ++i)                                         \
     _Pragma("unroll") for (int j = 0; j < NT; ++j)                                         \
@@ -511,11 +536,11 @@ uint32_t* unmask_scratch(const GemmLaunch& g, int64_t* ld) {
   return nullptr;
 }
 
-template <int EPI, int MT, int NT, int S, int W>
+template <int EPI, int MT, int NT, int S, int W, bool AW = false>
 hipError_t launch_ksplit(const GemmLaunch& g, hipStream_t s) {
   const int64_t tiles = (g.N + 16 * NT - 1) / (16 * NT);
-  hipLaunchKernelGGL((ring_gemm_skinny_ksplit_kernel<EPI, MT, NT, S, W>), dim3((unsigned)tiles), dim3(64 * W), 0, s,
-                     g);
+  hipLaunchKernelGGL((ring_gemm_skinny_ksplit_kernel<EPI, MT, NT, S, W, AW>), dim3((unsigned)tiles), dim3(64 * W), 0,
+                     s, g);
   return hipGetLastError();
 }
 
@@ -531,6 +556,16 @@ hipError_t launch_ring_gemm_words_b(const GemmLaunch& g, EpilogueKind epi, hipSt
   if (mt <= 1) return launch_shared_a<1, 1, true>(g, epi, s);
   if (mt == 2) return launch_shared_a<2, 2, true>(g, epi, s);
   return launch_shared_a<4, 2, true>(g, epi, s);
+}
+
+hipError_t launch_unmask_words_a(const GemmLaunch& g, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.M > 16) return hipErrorInvalidValue;
+  if (g.Kp == 0) return launch_unmask_elementwise(g, s);
+  // the single-launch kernel at every factor size: the digit conversion of
+  // A it replaces was a launch of its own
+  if (g.N <= 16 * compute_units()) return launch_ksplit<EPI_UNMASK, 1, 1, 2, 4, true>(g, s);
+  return launch_ksplit<EPI_UNMASK, 1, 2, 2, 4, true>(g, s);
 }
 
 hipError_t launch_clear_check(uint32_t* d, int64_t ldd, int64_t rows, int64_t cols, int64_t* count, hipStream_t s) {

@@ -243,6 +243,33 @@ def mosaic_unmask(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[Digi
                                      y_f32.stride(0) if y_f32 is not None else 0, _stream()), "mosaic_unmask")
 
 
+def mosaic_unmask_words(ym: torch.Tensor, kc: Optional[torch.Tensor], q: Optional[torch.Tensor],
+                        l: Optional[Digits], M: int, N: int, R: int, y: Optional[torch.Tensor] = None,
+                        s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,
+                        y_f32: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None) -> None:
+    """mosaic_unmask with q (M x R) as ring words, e.g. the Q columns of the
+    server's [Y' | Q]; at most 16 rows."""
+    _need(ym, M, N, "ym", _INT, optional=False)
+    _need(kc, M, N, "kc", _INT)
+    if R > 0:
+        _need(q, M, R, "q", _INT, optional=False)
+        _need_dig(l, N, R, "l", optional=False)
+    _need(y, M, N, "y", _INT)
+    _need(y_f32, M, N, "y_f32", (torch.float32,))
+    if y_f32 is not None:
+        _need(s_rows, 1, M, "s_rows", (torch.float32,), optional=False)
+        _need(s_cols, 1, N, "s_cols", (torch.float32,), optional=False)
+    _need(bias, 1, N, "bias", (torch.float32,))
+    _check(_lib.load().mosaic_unmask_words(ym.data_ptr(), ym.stride(0), _ptr(kc),
+                                           kc.stride(0) if kc is not None else 0,
+                                           _ptr(q), q.stride(0) if q is not None else 0,
+                                           l.ptr if l else None, l.pitch if l else 0, M, N, R,
+                                           _ptr(y), y.stride(0) if y is not None else 0,
+                                           _ptr(s_rows), _ptr(s_cols), _ptr(bias), _ptr(y_f32),
+                                           y_f32.stride(0) if y_f32 is not None else 0, _stream()),
+           "mosaic_unmask_words")
+
+
 def mosaic_rotate_quantize_mask(x: torch.Tensor, qmax: int, out_dig: Digits, block: Optional[int] = None,
                                 signs: Optional[torch.Tensor] = None, u: Optional[torch.Tensor] = None,
                                 noise: Optional[_lib.MosaicRng] = None,

@@ -323,22 +323,28 @@ def server(w: MaskedWeight, M: int, buf: CallBuffers) -> None:
 def unmask(w: MaskedWeight, M: int, buf: CallBuffers, y_f32: Optional[torch.Tensor] = None,
            s_rows: Optional[torch.Tensor] = None, s_cols: Optional[torch.Tensor] = None,
            bias: Optional[torch.Tensor] = None) -> None:
-    """Online step 5: Y = Y' - K_c - Q Lcat^T (digits of Q first). In sparse
-    mode the product covers the level-d slot (L Q_d) and each S_{i+1} Q_i is
-    subtracted by gathering from Q_i's ring words."""
+    """Online step 5: Y = Y' - K_c - Q Lcat^T (with at most 16 tokens the
+    product forms Q's digits from its ring words, else a pass converts Q
+    first). In sparse mode the product covers the level-d slot (L Q_d) and
+    each S_{i+1} Q_i is subtracted by gathering from Q_i's ring words."""
     r = list(w.params.ranks)
     sparse = w.sparse_call(M)
-    # digits of Q: the slots sit side by side in [Y' | Q] with the padded
-    # widths of Qdig, and the padding columns of Q are zero (Bext's padding
-    # rows are), so one pass converts every slot; sparse mode needs slot 0
+    # the slots sit side by side in [Y' | Q] with the padded widths of Lcat
+    # (and Qdig), and the padding columns of Q are zero (Bext's padding rows
+    # are), so one product covers every slot; sparse mode needs slot 0 only
     qw = w.Rd if sparse else w.R
-    m.mosaic_mask(None, buf.YQ[:, w.q_cols[0]: w.q_cols[0] + qw], None, M, qw, out_dig=buf.Qdig[0].whole(qw))
+    q_words = buf.YQ[:, w.q_cols[0]: w.q_cols[0] + qw]
+    kw = dict(y=buf.Y) if sparse else dict(y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32, bias=bias)
+    if M <= 16 and q_words.data_ptr() % 16 == 0 and q_words.stride(0) % 4 == 0:
+        # a few tokens: the product reads Q's ring words as the server wrote
+        # them (no conversion pass, one launch fewer per call)
+        m.mosaic_unmask_words(buf.YQ[:, : w.N], buf.UK[:, w.K:], q_words, w.Lcat[0].whole(qw), M, w.N, qw, **kw)
+    else:
+        m.mosaic_mask(None, q_words, None, M, qw, out_dig=buf.Qdig[0].whole(qw))
+        m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(qw), w.Lcat[0].whole(qw),
+                        M, w.N, qw, **kw)
     if not sparse:
-        m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.R), w.Lcat[0].whole(w.R),
-                        M, w.N, w.R, y=buf.Y, s_rows=s_rows, s_cols=s_cols, y_f32=y_f32, bias=bias)
         return
-    m.mosaic_unmask(buf.YQ[:, : w.N], buf.UK[:, w.K:], buf.Qdig[0].whole(w.Rd), w.Lcat[0].whole(w.Rd),
-                    M, w.N, w.Rd, y=buf.Y)
     gathers = [(slot, lv) for slot, lv in enumerate(w.slot_levels) if lv in w.S]
     for k, (slot, lv) in enumerate(gathers):
         c0 = w.q_cols[slot]

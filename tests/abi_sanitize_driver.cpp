@@ -105,6 +105,24 @@ int main() {
                        nullptr, 0, nullptr), INV);
   EXPECT(mosaic_unmask(Fu, 4, nullptr, 0, Fd, 256, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr, Ff,
                        nullptr, 0, nullptr), INV);     // bias without y_f32
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu, 64, Fd, 256, 17, 4, 64, (int32_t*)F, 4, nullptr, nullptr,
+                             nullptr, nullptr, 0, nullptr), UNS);     // more than 16 rows
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu, 64, Fd, 256, 4, 4, 32768, (int32_t*)F, 4, nullptr, nullptr,
+                             nullptr, nullptr, 0, nullptr), UNS);
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, nullptr, 64, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr,
+                             nullptr, nullptr, 0, nullptr), INV);     // q missing
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu, 60, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr,
+                             nullptr, nullptr, 0, nullptr), INV);     // ldq < R
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu + 1, 64, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr,
+                             nullptr, nullptr, 0, nullptr), UNS);     // q not 16-byte aligned
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu, 66, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr,
+                             nullptr, nullptr, 0, nullptr), UNS);     // ldq not a multiple of 4
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu, 64, Fd, 192, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr,
+                             nullptr, nullptr, 0, nullptr), INV);     // l pitch below its padded row
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu, 64, Fd, 256, 4, 4, 64, nullptr, 4, nullptr, nullptr, nullptr,
+                             nullptr, 0, nullptr), INV);              // no output
+  EXPECT(mosaic_unmask_words(Fu, 4, nullptr, 0, Fu, 64, Fd, 256, 4, 4, 64, (int32_t*)F, 4, nullptr, nullptr, Ff,
+                             nullptr, 0, nullptr), INV);     // bias without y_f32
 
   // rotation and quantisation
   EXPECT(mosaic_hadamard_rotate(Ff, 64, Ff, 64, 4, 64, 48, nullptr, 0, nullptr), UNS);

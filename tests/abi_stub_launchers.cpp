@@ -32,6 +32,7 @@ hipError_t launch_clear_check(uint32_t*, int64_t, int64_t, int64_t, int64_t*, hi
 hipError_t launch_ring_gemm(const GemmLaunch&, EpilogueKind, hipStream_t) STUB
 hipError_t launch_ring_gemm_skinny(const GemmLaunch&, EpilogueKind, hipStream_t) STUB
 hipError_t launch_ring_gemm_words_b(const GemmLaunch&, EpilogueKind, hipStream_t) STUB
+hipError_t launch_unmask_words_a(const GemmLaunch&, hipStream_t) STUB
 hipError_t launch_unmask_elementwise(const GemmLaunch&, hipStream_t) STUB
 hipError_t launch_hadamard(const float*, int64_t, float*, int64_t, int64_t, int64_t, int, const int8_t*, int,
                            hipStream_t) STUB

@@ -140,6 +140,33 @@ def test_unmask_validation(lib):
 
 
 @cpu_only
+def test_unmask_words_validation(lib):
+    """Q as ring words: the mosaic_unmask rules plus at most 16 rows, q
+    16-byte aligned with ldq >= R a multiple of 4."""
+    args = dict(ym=FAKE, ldy=8, kc=None, ldk=0, q=FAKE, ldq=64, l=FAKE, lp=256, M=2, N=8, R=64,
+                y=FAKE, ldo=8, sr=None, sc=None, bias=None, yf=None, ldf=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return lib.mosaic_unmask_words(a["ym"], a["ldy"], a["kc"], a["ldk"], a["q"], a["ldq"], a["l"], a["lp"],
+                                       a["M"], a["N"], a["R"], a["y"], a["ldo"], a["sr"], a["sc"], a["bias"],
+                                       a["yf"], a["ldf"], None)
+    assert call(M=17) == UNSUPPORTED
+    assert call(ym=None) == INVALID
+    assert call(y=None) == INVALID
+    assert call(ldy=7) == INVALID
+    assert call(q=None) == INVALID
+    assert call(ldq=60) == INVALID                  # ldq < R
+    assert call(q=FAKE + 4) == UNSUPPORTED          # not 16-byte aligned
+    assert call(ldq=66) == UNSUPPORTED              # rows not 16-byte aligned
+    assert call(lp=128) == INVALID
+    assert call(l=None) == INVALID
+    assert call(yf=FAKE, ldf=8) == INVALID
+    assert call(bias=FAKE) == INVALID
+    assert call(R=40000, ldq=40000, lp=4 * 40000 + 64) == UNSUPPORTED
+
+
+@cpu_only
 def test_hadamard28_validation(lib):
     def call(x=FAKE, ldx=28672, y=FAKE + (1 << 24), ldy=28672, rows=2, n=28672, signs=None, inv=0):
         return lib.mosaic_hadamard28_rotate(x, ldx, y, ldy, rows, n, signs, inv, None)

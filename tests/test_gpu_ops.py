@@ -426,6 +426,89 @@ def test_unmask_one_row_large_factor(with_f32):
         assert np.array_equal(yf.cpu().numpy(), ref)
 
 
+def _words_window(rng, q, layout):
+    """q (M x R ring words) on the device as a 16-byte aligned view with
+    rows a multiple of 4 words apart: its own rows padded to 4 words
+    ("tight") or a column window of a wider matrix ("wide", like the Q
+    columns of [Y' | Q]). The words around the view are random."""
+    M, R = q.shape
+    R4 = 4 * ((R + 3) // 4)
+    width, c0 = (R4, 0) if layout == "tight" else (R4 + 16, 4)
+    big = _random_ring(rng, (M, width))
+    big[:, c0: c0 + R] = q
+    return to_dev_ring(big)[:, c0: c0 + R]
+
+
+@pytest.mark.parametrize("M,N,R", [(1, 300, 2560), (8, 33, 64), (1, 4096, 1536), (1, 4200, 1536),
+                                   (16, 4111, 320), (3, 700, 1088), (1, 70, 5), (2, 130, 67), (5, 64, 0),
+                                   (1, 16384, 2048)])
+@pytest.mark.parametrize("layout", ["tight", "wide"])
+def test_unmask_words(M, N, R, layout):
+    """Q given as ring words (at most 16 rows): Y = Ym - Kc - Q L^T equals
+    the oracle, for ragged R (the words after column R in a row are other
+    data; L's zero digit padding cancels them), ragged column tiles of N and
+    a 128 MiB factor (16384 x 2048)."""
+    rng = _rng_np(7 * M + N + R + len(layout))
+    ym = _random_ring(rng, (M, N))
+    kc = _random_ring(rng, (M, N))
+    q = _random_ring(rng, (M, R))
+    l = _random_ring(rng, (N, R))
+    L = Digits.empty(N, max(R, 1))
+    if R:
+        m.mosaic_mask(to_dev_ring(l), None, None, N, R, out_dig=L)
+    y = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    m.mosaic_unmask_words(to_dev_ring(ym), to_dev_ring(kc), _words_window(rng, q, layout) if R else None,
+                          L if R else None, M, N, R, y=y)
+    torch.cuda.synchronize()
+    ref = ring_sub(ym, kc)
+    if R:
+        ref = ring_sub(ref, ring_matmul(q, l.T))
+    assert np.array_equal(y.cpu().numpy(), ref.view(np.int32))
+
+
+@pytest.mark.parametrize("M", [1, 16])
+@pytest.mark.parametrize("case", ["y_and_f32_bias", "f32", "y_is_ym", "y_is_kc"])
+def test_unmask_words_outputs(M, case):
+    """The word form's outputs: y with the dequantised y_f32 and a bias,
+    y_f32 alone, and y in place on ym or on kc; bit-identical to mosaic_unmask
+    with the digits of the same Q and to the oracle."""
+    N, R = 700, 1088
+    rng = _rng_np(M * 5 + len(case))
+    ym = _random_ring(rng, (M, N))
+    kc = _random_ring(rng, (M, N))
+    q = _random_ring(rng, (M, R))
+    l = _random_ring(rng, (N, R))
+    Q, L = Digits.empty(M, R), Digits.empty(N, R)
+    m.mosaic_mask(to_dev_ring(q), None, None, M, R, out_dig=Q)
+    m.mosaic_mask(to_dev_ring(l), None, None, N, R, out_dig=L)
+    sr = torch.rand(M, device="cuda") * 1e-3
+    sc = torch.rand(N, device="cuda") * 1e-3
+    want_f32 = case in ("y_and_f32_bias", "f32")
+    bd, bn = _bias(N, "aligned" if case == "y_and_f32_bias" else None, M + 3)
+    outs = []
+    for words in (True, False):
+        ymd, kcd = to_dev_ring(ym), to_dev_ring(kc)
+        y = {"y_and_f32_bias": torch.empty((M, N), dtype=torch.int32, device="cuda"),
+             "y_is_ym": ymd, "y_is_kc": kcd}.get(case)
+        yf = torch.empty((M, N), dtype=torch.float32, device="cuda") if want_f32 else None
+        kw = dict(y=y, s_rows=sr if want_f32 else None, s_cols=sc if want_f32 else None, y_f32=yf, bias=bd)
+        if words:
+            m.mosaic_unmask_words(ymd, kcd, _words_window(rng, q, "wide"), L, M, N, R, **kw)
+        else:
+            m.mosaic_unmask(ymd, kcd, Q, L, M, N, R, **kw)
+        torch.cuda.synchronize()
+        outs.append((y.cpu().numpy() if y is not None else None, yf.cpu().numpy() if yf is not None else None))
+    yi = ring_sub(ring_sub(ym, kc), ring_matmul(q, l.T)).view(np.int32)
+    (yw, fw), (yd, fd) = outs
+    if yw is not None:
+        assert np.array_equal(yw, yi) and np.array_equal(yd, yi)
+    if want_f32:
+        ref = (yi.astype(np.float32) * sr.cpu().numpy()[:, None]) * sc.cpu().numpy()[None, :]
+        if bd is not None:
+            ref = (ref + bn).astype(np.float32)
+        assert np.array_equal(fw, ref) and np.array_equal(fd, ref)
+
+
 @pytest.mark.parametrize("M", [130, 257])
 @pytest.mark.parametrize("target", ["ym", "kc"])
 def test_unmask_in_place_tiled(M, target):
