@@ -100,3 +100,32 @@ def test_mask_invariance_on_gpu():
         buf = gproto.run_call(w, torch.from_numpy(A).cuda(), 5)
         torch.cuda.synchronize()
         assert np.array_equal(buf.Y.cpu().numpy().astype(np.int64), ref)
+
+
+@pytest.mark.parametrize("M,K,N,ranks", [(1, 64, 64, (64,)), (5, 200, 152, (96, 32)), (16, 128, 260, (64,)),
+                                         (3, 96, 150, (64,)), (17, 64, 64, (64,))])
+def test_unmask_form_by_token_count(monkeypatch, M, K, N, ranks):
+    """Up to 16 tokens, with Q's columns of [Y' | Q] 16-byte aligned (N a
+    multiple of 4), unmasking reads Q as ring words (mosaic_unmask_words,
+    no conversion pass); otherwise Q is converted to digits first. Both
+    give the oracle's Y (every intermediate checked by _check_run)."""
+    calls = {"words": 0, "digits": 0}
+    words, digits = gproto.m.mosaic_unmask_words, gproto.m.mosaic_unmask
+
+    def count_words(*a, **k):
+        calls["words"] += 1
+        return words(*a, **k)
+
+    def count_digits(*a, **k):
+        if a[2] is not None:                    # a product term (not the dequantisation-only form)
+            calls["digits"] += 1
+        return digits(*a, **k)
+    monkeypatch.setattr(gproto.m, "mosaic_unmask_words", count_words)
+    monkeypatch.setattr(gproto.m, "mosaic_unmask", count_digits)
+    rng = np.random.default_rng(7 * M + N)
+    A = rng.integers(-127, 128, (M, K), dtype=np.int8)
+    W = rng.integers(-127, 128, (N, K), dtype=np.int8)
+    p = ProtocolParams(ranks=ranks, noise=NoiseSpec("dgauss", 0.5, 4), sparse_log2_inv_density=3)
+    _check_run(A, W, p, SEED + 3 * M)
+    expect_words = M <= 16 and N % 4 == 0
+    assert calls == {"words": int(expect_words), "digits": int(not expect_words)}
