@@ -34,7 +34,10 @@
 // Unmask epilogue. Its output cannot take partial products, so when an
 // output buffer of the call (y, else y_f32) shares no memory with any input,
 // the product is computed into that buffer by the shared-A kernel and an
-// elementwise pass then forms y = ym - kc - product in place. Otherwise
+// elementwise pass then forms y = ym - kc - product in place (when y is that
+// buffer and no fp32 output is asked for, the elementwise pass writes
+// y = ym - kc first and the product's partial sums are subtracted from it,
+// so y is neither cleared nor read again). Otherwise
 // ring_gemm_skinny_ksplit_kernel runs: one workgroup per column tile of 32
 // (A of at most 16 rows) or 64 rows of B computes the whole K range, its 4
 // waves splitting the stages, streaming their part of B straight into
@@ -588,7 +591,8 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
     return hipGetLastError();
   }
   if (epi == EPI_UNMASK) {
-    // The two-phase path costs two more launches (clear, elementwise): for
+    // The two-phase path costs two more launches (clear, elementwise; one,
+    // the elementwise pass before the product, when only y is written): for
     // A of at most 16 rows it pays only once the factor read is large (one
     // row against rank-1536 factors of 12-96 MiB, the single launch took
     // 0-20% less device time; at 168 MiB the two were equal).
@@ -600,6 +604,18 @@ hipError_t launch_ring_gemm_skinny(const GemmLaunch& g, EpilogueKind epi, hipStr
       p.c = prod;
       p.ldc = ldp;
       hipError_t e = hipSuccess;
+      if (prod == (uint32_t*)g.y && g.y_f32 == nullptr) {
+        // y = ym - kc first, then the product's partial sums subtracted
+        // from it atomically: no clear of y and no final pass over it
+        GemmLaunch pre = g;
+        pre.c = nullptr;
+        e = launch_unmask_elementwise(pre, s);
+        if (e != hipSuccess) return e;
+        p.negate = true;
+        if (mt <= 1) return launch_shared_a<1, 1>(p, EPI_ACCUM, s);
+        if (mt == 2) return launch_shared_a<2, 2>(p, EPI_ACCUM, s);
+        return launch_shared_a<4, 2>(p, EPI_ACCUM, s);
+      }
       if (mt <= 1) e = launch_shared_a<1, 1>(p, EPI_STORE, s);
       else if (mt == 2) e = launch_shared_a<2, 2>(p, EPI_STORE, s);
       else e = launch_shared_a<4, 2>(p, EPI_STORE, s);
