@@ -467,15 +467,15 @@ def test_unmask_words(M, N, R, layout):
 
 
 @pytest.mark.parametrize("M", [1, 16])
-@pytest.mark.parametrize("case", ["y_and_f32_bias", "f32", "y_is_ym", "y_is_kc"])
+@pytest.mark.parametrize("case", ["y_and_f32_bias", "f32", "y_is_ym", "y_is_kc", "y_no_kc"])
 def test_unmask_words_outputs(M, case):
     """The word form's outputs: y with the dequantised y_f32 and a bias,
-    y_f32 alone, and y in place on ym or on kc; bit-identical to mosaic_unmask
-    with the digits of the same Q and to the oracle."""
+    y_f32 alone, y in place on ym or on kc, and y without K_c; bit-identical
+    to mosaic_unmask with the digits of the same Q and to the oracle."""
     N, R = 700, 1088
     rng = _rng_np(M * 5 + len(case))
     ym = _random_ring(rng, (M, N))
-    kc = _random_ring(rng, (M, N))
+    kc = _random_ring(rng, (M, N)) if case != "y_no_kc" else np.zeros((M, N), dtype=np.uint32)
     q = _random_ring(rng, (M, R))
     l = _random_ring(rng, (N, R))
     Q, L = Digits.empty(M, R), Digits.empty(N, R)
@@ -487,8 +487,9 @@ def test_unmask_words_outputs(M, case):
     bd, bn = _bias(N, "aligned" if case == "y_and_f32_bias" else None, M + 3)
     outs = []
     for words in (True, False):
-        ymd, kcd = to_dev_ring(ym), to_dev_ring(kc)
+        ymd, kcd = to_dev_ring(ym), (to_dev_ring(kc) if case != "y_no_kc" else None)
         y = {"y_and_f32_bias": torch.empty((M, N), dtype=torch.int32, device="cuda"),
+             "y_no_kc": torch.empty((M, N), dtype=torch.int32, device="cuda"),
              "y_is_ym": ymd, "y_is_kc": kcd}.get(case)
         yf = torch.empty((M, N), dtype=torch.float32, device="cuda") if want_f32 else None
         kw = dict(y=y, s_rows=sr if want_f32 else None, s_cols=sc if want_f32 else None, y_f32=yf, bias=bd)
