@@ -33,7 +33,8 @@
 // the time the next barrier needs them (4-7% faster than spreading them one
 // load and three reads per group). The fragments are double-buffered in
 // registers. One barrier per stage publishes stage s+1 and retires the slot
-// of stage s, which the loads of stage s then refill.
+// of stage s, which the loads of stage s then refill. All stages but the
+// last four run in a loop with no tests (every stage refills and reads).
 //
 // LDS rows are 128 bytes (8 chunks of 16 bytes); chunk c of row R sits in
 // slot c ^ ((R >> 1) & 7). Sixteen lanes reading one chunk of 16 consecutive
@@ -270,10 +271,11 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
 
   // group g of a stage: MFMAs 5g .. 5g+4, then (g < 2) direct loads 2g, 2g+1
   // of stage S+4 and (g < 3) fragment reads 4g .. 4g+3 of stage S+1
-#define MOSAIC_STAGE(CUR, NXT, S)                                                          \
+#define MOSAIC_STAGE(CUR, NXT, S) MOSAIC_STAGE_IF(CUR, NXT, S, (S) + NSTAGE < stages, (S) + 1 < stages)
+#define MOSAIC_STAGE_IF(CUR, NXT, S, REFILL, NEXT)                                         \
   do {                                                                                     \
-    const bool refill_ = (S) + NSTAGE < stages;                                            \
-    const bool next_ = (S) + 1 < stages;                                                   \
+    const bool refill_ = (REFILL);                                                         \
+    const bool next_ = (NEXT);                                                             \
     _Pragma("unroll") for (int gq = 0; gq < 4; ++gq) {                                     \
       _Pragma("unroll") for (int u = 0; u < 5; ++u) MOSAIC_MFMA(CUR, gq * 5 + u);          \
       if (gq < 2 && refill_) {                                                             \
@@ -305,7 +307,24 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   // stage S have completed (the pin); the barrier then makes stage S+1
   // visible to every wave and guarantees nobody still reads stage S's slot,
   // which stage S's loads refill with stage S+4.
-  for (int s = 0; s < stages; s += 2) {
+  // The steady state, where every stage refills its slot and reads the next
+  // one, runs as a loop without conditions: one basic block per two stages,
+  // which the scheduler interleaves freely within the pinned groups (the
+  // server products 1.5-3% faster than with the tests inside every stage);
+  // the last four stages (all of them when there are fewer than six) take
+  // the general loop.
+  int s = 0;
+  for (; s + NSTAGE + 2 <= stages; s += 2) {
+    wait_loads(NSTAGE - 2);
+    MOSAIC_PIN(0);
+    __builtin_amdgcn_s_barrier();
+    MOSAIC_STAGE_IF(0, 1, s, true, true);
+    wait_loads(NSTAGE - 2);
+    MOSAIC_PIN(1);
+    __builtin_amdgcn_s_barrier();
+    MOSAIC_STAGE_IF(1, 0, s + 1, true, true);
+  }
+  for (; s < stages; s += 2) {
     wait_loads(imin(NSTAGE - 2, stages - 2 - s));
     MOSAIC_PIN(0);
     __builtin_amdgcn_s_barrier();
@@ -321,6 +340,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
 #undef MOSAIC_PIN
 #undef MOSAIC_MFMA
 #undef MOSAIC_STAGE
+#undef MOSAIC_STAGE_IF
 
   // epilogue: recombine the shift classes and write. Output layout of the
   // 32 x 32 MFMA: register v of lane l holds row 8 (v / 4) + 4 (l / 32) + v % 4,

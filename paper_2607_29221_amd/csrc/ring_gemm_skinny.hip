@@ -19,7 +19,10 @@
 // product into C with 32-bit atomics (exact in the ring; C is cleared first
 // for a plain store). Both operands of a stage are staged in LDS by direct
 // buffer-to-LDS loads, three stages resident and loads issued two stages
-// ahead, so data in flight costs no registers. The waves of a workgroup
+// ahead, so data in flight costs no registers; the units with a fetch two
+// ahead run in a loop with no tests on the unit index and LDS slots taken in
+// rotation (one-token products at 4096 x 4096 2-7% faster than with the
+// tests and a 64-bit slot modulo in every unit). The waves of a workgroup
 // split the tile's columns (32 each, 4 column groups): the A stage is
 // fetched once per workgroup and read from LDS by every wave, where a split
 // of K between the waves would fetch all of A once per wave and need a
@@ -202,21 +205,12 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
     if (s < cnt) fetch(s);
 
   int64_t ct = u0 / stages, cst = u0 - ct * stages;   // (tile, stage) being computed
-  for (int64_t k = 0; k < cnt; ++k) {
-    // Unit k has landed once at most the later units this wave already
-    // issued are in flight (vector-memory counts return in order; atomics
-    // of earlier flushes only make the wait longer). The barrier then
-    // publishes everyone's loads of unit k and guarantees that no wave still
-    // reads unit k - 1, whose slot the next fetch refills.
-    if (k + 1 < cnt) wait_vm<QU>();
-    else wait_vm<0>();
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    if (k + SA_NS - 1 < cnt) fetch((int)((k + SA_NS - 1) % SA_NS));
-
-    const char* sa = lds + (int)(k % SA_NS) * STG + wm * MTW * 16 * ROWB;
-    const char* sb = lds + (int)(k % SA_NS) * STG + ASZ + wn * 16 * SA_NTW * ROWB;
+  // one unit: fragments from LDS slot `slot`, the ten limb products, and the
+  // tile's partial product added into C after its last stage (or the range's
+  // last unit)
+  auto unit = [&](int slot, bool last) __attribute__((always_inline)) {
+    const char* sa = lds + slot * STG + wm * MTW * 16 * ROWB;
+    const char* sb = lds + slot * STG + ASZ + wn * 16 * SA_NTW * ROWB;
     v4i fa[MTW][4], fb[SA_NTW][4];
 #pragma unroll
     for (int j = 0; j < SA_NTW; ++j)
@@ -256,7 +250,7 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
           acc[i][j][kLimbA[p] + kLimbB[p]] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
               fa[i][kLimbA[p]], fb[j][kLimbB[p]], acc[i][j][kLimbA[p] + kLimbB[p]], 0, 0, 0);
 
-    if (++cst == stages || k == cnt - 1) {
+    if (++cst == stages || last) {
       // add this tile's partial product into C. Output layout of the 16 x 16
       // MFMA: register v of lane l holds row 4 (l / 16) + v, column l % 16.
       const int64_t n0 = ct * SA_BN + wn * 16 * SA_NTW;
@@ -277,6 +271,33 @@ __global__ __launch_bounds__(64 * WM * SA_WN, 1) void ring_gemm_skinny_kernel(Ge
       cst = 0;
       ++ct;
     }
+  };
+  // Unit k has landed once at most the later units this wave already issued
+  // are in flight (vector-memory counts return in order; atomics of earlier
+  // flushes only make the wait longer). The barrier then publishes
+  // everyone's loads of unit k and guarantees that no wave still reads unit
+  // k - 1, whose slot the next fetch refills. While the unit SA_NS - 1 ahead
+  // exists the loop runs without tests on k; the last units take the
+  // general form. Slots rotate 0, 1, .., SA_NS - 1.
+  int64_t k = 0;
+  int cs = 0;
+  for (; k + SA_NS - 1 < cnt; ++k) {
+    wait_vm<QU>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    fetch(cs == 0 ? SA_NS - 1 : cs - 1);
+    unit(cs, false);
+    cs = cs + 1 == SA_NS ? 0 : cs + 1;
+  }
+  for (; k < cnt; ++k) {
+    if (k + 1 < cnt) wait_vm<QU>();
+    else wait_vm<0>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    unit(cs, k == cnt - 1);
+    cs = cs + 1 == SA_NS ? 0 : cs + 1;
   }
   wait_vm<0>();   // no direct load outlives the workgroup's LDS
 }
