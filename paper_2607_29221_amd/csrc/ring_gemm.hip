@@ -26,12 +26,14 @@
 // filled by direct buffer-to-LDS loads issued four stages ahead: stage s's
 // fragments are read into registers during stage s-1, so once the barrier
 // before stage s has passed, its slot is free and the loads of stage s+4 go
-// there. Each wave runs a stage as four groups of 5 MFMAs; the memory work
-// is front-loaded, pinned by scheduling barriers: the 4 direct loads follow
-// the first two groups, the 12 LDS reads of stage s+1's fragments the first
-// three, so the reads have completed and the loads are well on their way by
-// the time the next barrier needs them (4-7% faster than spreading them one
-// load and three reads per group). The fragments are double-buffered in
+// there. Each wave runs a stage as four groups of 5 MFMAs, pinned by
+// scheduling barriers: the 12 LDS reads of stage s+1's fragments follow the
+// first three groups (four each), so they have completed by the time the
+// next barrier needs them, and one of the wave's 4 direct loads follows
+// each group (whole bench steps over the three server shapes 1.2-1.6%
+// faster than with the 4 loads after the first two groups, 0.3-0.5% faster
+// than with one load and three reads after every group, 4% faster than with
+// six reads after each of the first two). The fragments are double-buffered in
 // registers. One barrier per stage publishes stage s+1 and retires the slot
 // of stage s, which the loads of stage s then refill. All stages but the
 // last four run in a loop with no tests (every stage refills and reads).
@@ -269,8 +271,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
         __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[SET][i_][a_], fb[SET][b_], acc[i_][a_ + b_], 0, 0, 0); \
   } while (0)
 
-  // group g of a stage: MFMAs 5g .. 5g+4, then (g < 2) direct loads 2g, 2g+1
-  // of stage S+4 and (g < 3) fragment reads 4g .. 4g+3 of stage S+1
+  // group g of a stage: MFMAs 5g .. 5g+4, then direct load g of stage S+4
+  // and (g < 3) fragment reads 4g .. 4g+3 of stage S+1
 #define MOSAIC_STAGE(CUR, NXT, S) MOSAIC_STAGE_IF(CUR, NXT, S, (S) + NSTAGE < stages, (S) + 1 < stages)
 #define MOSAIC_STAGE_IF(CUR, NXT, S, REFILL, NEXT)                                         \
   do {                                                                                     \
@@ -278,9 +280,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
     const bool next_ = (NEXT);                                                             \
     _Pragma("unroll") for (int gq = 0; gq < 4; ++gq) {                                     \
       _Pragma("unroll") for (int u = 0; u < 5; ++u) MOSAIC_MFMA(CUR, gq * 5 + u);          \
-      if (gq < 2 && refill_) {                                                             \
-        MOSAIC_DMA((S) + NSTAGE, 2 * gq);                                                  \
-        MOSAIC_DMA((S) + NSTAGE, 2 * gq + 1);                                              \
+      if (refill_) {                                                                       \
+        MOSAIC_DMA((S) + NSTAGE, gq);                                                      \
       }                                                                                    \
       if (gq < 3 && next_) {                                                               \
         _Pragma("unroll") for (int r = 0; r < 4; ++r) MOSAIC_READ((S) + 1, NXT, 4 * gq + r); \
