@@ -36,7 +36,13 @@
 // six reads after each of the first two). The fragments are double-buffered in
 // registers. One barrier per stage publishes stage s+1 and retires the slot
 // of stage s, which the loads of stage s then refill. All stages but the
-// last four run in a loop with no tests (every stage refills and reads).
+// last four run in a loop with no tests (every stage refills and reads),
+// four stages per iteration. LDS holds the A tiles of the four slots first
+// and then their B tiles (16 KiB each), so that every fragment read
+// addresses its slot and tile by an immediate offset from one of the
+// lane's eight fragment offsets: that loop computes no addresses in vector
+// registers (0.8% faster whole bench steps than slots of A and B together,
+// whose third and fourth slots lie beyond the 64 KiB offset range).
 //
 // LDS rows are 128 bytes (8 chunks of 16 bytes); chunk c of row R sits in
 // slot c ^ ((R >> 1) & 7). Sixteen lanes reading one chunk of 16 consecutive
@@ -214,7 +220,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   for (int t = 0; t < 4; ++t) {
     const int p = ((lane >> 5) * 4 + t) ^ f;
     fo[t] = (wm * 64 + rr) * ROWB + p * 16;
-    fo[4 + t] = OPS + (wn * 32 + rr) * ROWB + p * 16;
+    fo[4 + t] = NSTAGE * OPS + (wn * 32 + rr) * ROWB + p * 16;
   }
 
   v16i acc[2][4];
@@ -229,12 +235,12 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
 
 #define MOSAIC_DMA(S, k)                                                                   \
   dma16(((k) & 1) ? rsb : rsa,                                                            \
-        lds_wave + ((S) % NSTAGE) * STAGE + ((k) & 1) * OPS + ((k) >> 1) * 8 * ROWB, voff[k], \
+        lds_wave + ((S) & (NSTAGE - 1)) * OPS + ((k) & 1) * NSTAGE * OPS + ((k) >> 1) * 8 * ROWB, voff[k], \
         (S) * ROWB)
 
 #define MOSAIC_READ(S, SET, idx)                                                           \
   do {                                                                                     \
-    const char* base_ = lds + ((S) % NSTAGE) * STAGE;                                      \
+    const char* base_ = lds + ((S) & (NSTAGE - 1)) * OPS;                                  \
     if ((idx) < 8) {                                                                       \
       const int i_ = (idx) >> 2, t_ = (idx) & 3;                                           \
       const uint4 v_ = *(const uint4*)(base_ + i_ * 32 * ROWB + fo[t_]);                   \
@@ -309,22 +315,27 @@ __global__ __launch_bounds__(NTHREADS, 1) void ring_gemm_kernel(GemmLaunch g) {
   // visible to every wave and guarantees nobody still reads stage S's slot,
   // which stage S's loads refill with stage S+4.
   // The steady state, where every stage refills its slot and reads the next
-  // one, runs as a loop without conditions: one basic block per two stages,
-  // which the scheduler interleaves freely within the pinned groups (the
-  // server products 1.5-3% faster than with the tests inside every stage);
-  // the last four stages (all of them when there are fewer than six) take
-  // the general loop.
-  int s = 0;
-  for (; s + NSTAGE + 2 <= stages; s += 2) {
-    wait_loads(NSTAGE - 2);
-    MOSAIC_PIN(0);
-    __builtin_amdgcn_s_barrier();
-    MOSAIC_STAGE_IF(0, 1, s, true, true);
-    wait_loads(NSTAGE - 2);
-    MOSAIC_PIN(1);
-    __builtin_amdgcn_s_barrier();
-    MOSAIC_STAGE_IF(1, 0, s + 1, true, true);
+  // one, runs as a loop without conditions: one basic block per four stages
+  // (slots 0..3 in turn), which the scheduler interleaves freely within the
+  // pinned groups (the server products 1.5-3% faster than with the tests
+  // inside every stage); the remaining stages (the last four to six, or all
+  // of them below eight) take the general loop.
+  int it = 0;
+  for (; NSTAGE * it + 2 * NSTAGE <= stages; ++it) {
+    const int s4 = NSTAGE * it;
+#pragma unroll
+    for (int h = 0; h < NSTAGE; h += 2) {
+      wait_loads(NSTAGE - 2);
+      MOSAIC_PIN(0);
+      __builtin_amdgcn_s_barrier();
+      MOSAIC_STAGE_IF(0, 1, s4 + h, true, true);
+      wait_loads(NSTAGE - 2);
+      MOSAIC_PIN(1);
+      __builtin_amdgcn_s_barrier();
+      MOSAIC_STAGE_IF(1, 0, s4 + h + 1, true, true);
+    }
   }
+  int s = NSTAGE * it;
   for (; s < stages; s += 2) {
     wait_loads(imin(NSTAGE - 2, stages - 2 - s));
     MOSAIC_PIN(0);
