@@ -138,6 +138,22 @@ def test_masked_matmul_mid_size(M, N, K):
     assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
 
 
+@pytest.mark.parametrize("K", [192, 256, 288, 320, 448, 512, 1536])
+def test_masked_matmul_stage_loop_forms(K):
+    """Whole-tile products (144 tiles: one round, no split-K pieces) whose
+    32-column stage counts take each form of the stage loop: below eight
+    stages the general loop only (K = 192: 6 stages); exactly eight (the
+    four-stage loop once, then the last four as straight code); 4 q + 2
+    stages (K = 288 and 320: 10, K padded to a multiple of 64; 448: 14),
+    whose last six take the general loop; multiples of four (512: 16, 1536:
+    48). The last tile is ragged in both dimensions."""
+    rng = _rng_np(K + 17)
+    M, N = 2000, 1100
+    a = _random_ring(rng, (M, K), edge=True)
+    b = _random_ring(rng, (N, K), edge=True)
+    assert np.array_equal(_gemm(a, b), ring_matmul(a, b.T))
+
+
 def test_masked_matmul_split_output_window():
     """Split-K pieces writing into a window of a wider C (ldc > N, a column
     offset): the clear before a store and the atomic adds touch only the
